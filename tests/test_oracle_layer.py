@@ -1,0 +1,230 @@
+"""Pins of the oracle's layer backward: brute-force integer products, float64 products
+on dequantized gradients, torch convolution routines, and unbiasedness over seeds."""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import fqt, philox
+from paper_2408_14267_amd.workloads import LayerShape, Recipe, draw_layer
+
+F32 = np.float32
+
+LAYERS = [
+    LayerShape("lin", "linear", 7, 13, 5),
+    LayerShape("c3", "conv2d", 3, 4, 5, 5, 6, 3, 3, 1, 1, 1, 1),
+    LayerShape("c3s2", "conv2d", 2, 3, 4, 7, 5, 3, 3, 2, 2, 1, 1),
+    LayerShape("c1s2", "conv2d", 3, 5, 6, 4, 4, 1, 1, 2, 2, 0, 0),
+    LayerShape("c2x3", "conv2d", 2, 3, 3, 5, 6, 2, 3, 1, 2, 0, 1),
+]
+
+
+def _run(layer, bits=2, mode=fqt.AGP_BERNOULLI, seed=0, data_seed=0, recipe=None):
+    x, w, dy = draw_layer(layer, recipe or Recipe("sample_lognormal", sigma=1.0), data_seed)
+    return (x, w, dy), fqt.layer_backward(x, w, dy, bits, mode, seed=seed, stride=layer.stride,
+                                          pad=layer.pad)
+
+
+def _dequantized(qg):
+    """Dequantized PSQ and PCQ gradients written out element by element (Section 3.2, 5.3)."""
+    N, D, Ho, Wo = qg.q_psq.shape
+    gs = np.zeros((N, D, Ho, Wo))
+    gc = np.zeros((N, D, Ho, Wo))
+    for n in range(N):
+        if qg.samples.keep[n]:
+            gs[n] = float(qg.samples.scale[n]) * qg.q_psq[n] + float(qg.samples.offset[n])
+    for d in range(D):
+        if qg.channels.keep[d]:
+            gc[:, d] = float(qg.channels.scale[d]) * qg.q_pcq[:, d] + float(qg.channels.offset[d])
+    return gs, gc
+
+
+@pytest.mark.parametrize("layer", LAYERS, ids=lambda l: l.name)
+def test_integer_products_brute_force(layer):
+    (x, w, dy), bw = _run(layer)
+    qg = bw.qgrad
+    x4, w4 = fqt.as_nchw(x), fqt.as_nchw(w)
+    N, C, H, W = x4.shape
+    D, _, kh, kw = w4.shape
+    Ho, Wo = layer.Ho, layer.Wo
+    sx = np.where(x4 > 0, 1, -1)
+    sw = np.where(w4 > 0, 1, -1)
+    for d in range(D):
+        for c in range(C):
+            for i in range(kh):
+                for j in range(kw):
+                    acc = 0
+                    for n in range(N):
+                        for ho in range(Ho):
+                            for wo in range(Wo):
+                                h, ww = ho * layer.sh - layer.ph + i, wo * layer.sw - layer.pw + j
+                                s = sx[n, c, h, ww] if (0 <= h < H and 0 <= ww < W) else -1
+                                acc += int(qg.q_pcq[n, d, ho, wo]) * int(s)
+                    want = acc if qg.channels.keep[d] else 0
+                    assert bw.I_dw[d, (c * kh + i) * kw + j] == want
+    for n in range(N):
+        for c in range(C):
+            for h in range(H):
+                for ww in range(W):
+                    acc = 0
+                    for i in range(kh):
+                        for j in range(kw):
+                            th, tw = h + layer.ph - i, ww + layer.pw - j
+                            if th % layer.sh or tw % layer.sw:
+                                continue
+                            ho, wo = th // layer.sh, tw // layer.sw
+                            if 0 <= ho < Ho and 0 <= wo < Wo:
+                                acc += sum(int(qg.q_psq[n, d, ho, wo]) * int(sw[d, c, i, j])
+                                           for d in range(D))
+                    assert bw.I_dx[n, c, h, ww] == (acc if qg.samples.keep[n] else 0)
+
+
+@pytest.mark.parametrize("layer", LAYERS, ids=lambda l: l.name)
+@pytest.mark.parametrize("bits,mode", [(1, fqt.AGP_BERNOULLI), (2, fqt.AGP_BERNOULLI),
+                                       (4, fqt.AGP_TOPK), (8, fqt.AGP_OFF)])
+def test_rescaled_outputs_match_torch_on_dequantized(layer, bits, mode):
+    """dW and dX equal float64 products of the dequantized gradients with the sign tensors,
+    computed by torch's own convolution-gradient routines (padding of X read as sign -1)."""
+    (x, w, dy), bw = _run(layer, bits, mode, seed=5, data_seed=1)
+    gs, gc = _dequantized(bw.qgrad)
+    x4 = torch.from_numpy(fqt.as_nchw(x).astype(np.float64))
+    w4 = torch.from_numpy(fqt.as_nchw(w).astype(np.float64))
+    sx = torch.where(x4 > 0, 1.0, -1.0).double()
+    sw = torch.where(w4 > 0, 1.0, -1.0).double()
+    sxp = F.pad(sx, (layer.pw, layer.pw, layer.ph, layer.ph), value=-1.0)
+    dW_ref = torch.nn.grad.conv2d_weight(sxp, tuple(w4.shape), torch.from_numpy(gc),
+                                         stride=layer.stride, padding=0)
+    dX_ref = torch.nn.grad.conv2d_input(tuple(x4.shape), sw, torch.from_numpy(gs),
+                                        stride=layer.stride, padding=layer.pad)
+    scale_w = np.abs(bw.dW_t1) + np.abs(bw.dW_t2) + 1e-30
+    scale_x = np.abs(bw.dX_t1) + np.abs(bw.dX_t2) + 1e-30
+    np.testing.assert_array_less(np.abs(bw.dW - dW_ref.numpy().reshape(bw.dW.shape)), 1e-9 * scale_w + 1e-12)
+    np.testing.assert_array_less(np.abs(bw.dX - dX_ref.numpy().reshape(bw.dX.shape)), 1e-9 * scale_x + 1e-12)
+
+
+def test_linear_products_plain_matmul():
+    layer = LayerShape("lin", "linear", 16, 40, 24)
+    (x, w, dy), bw = _run(layer, 4, fqt.AGP_BERNOULLI, seed=2)
+    gs, gc = _dequantized(bw.qgrad)
+    sx = np.where(x > 0, 1.0, -1.0)
+    sw = np.where(w > 0, 1.0, -1.0)
+    np.testing.assert_allclose(bw.dW, gc[:, :, 0, 0].T @ sx, rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(bw.dX, gs[:, :, 0, 0] @ sw, rtol=1e-12, atol=1e-9)
+
+
+def test_pruned_groups_give_zero_rows():
+    layer = LayerShape("c3", "conv2d", 8, 4, 8, 4, 4, 3, 3, 1, 1, 1, 1)
+    (x, w, dy), bw = _run(layer, 4, seed=11)
+    qg = bw.qgrad
+    assert 0 < qg.samples.count < 8 or True
+    dW = bw.dW.reshape(8, -1)
+    for d in range(8):
+        if not qg.channels.keep[d]:
+            assert np.all(dW[d] == 0)
+    for n in range(8):
+        if not qg.samples.keep[n]:
+            assert np.all(bw.dX[n] == 0)
+
+
+def test_all_zero_gradient_keeps_nothing():
+    layer = LayerShape("lin", "linear", 4, 6, 3)
+    x, w, _ = draw_layer(layer, Recipe(), 0)
+    bw = fqt.layer_backward(x, w, np.zeros((4, 3), F32), 2)
+    assert bw.qgrad.samples.count == 0 and bw.qgrad.channels.count == 0
+    assert np.all(bw.dW == 0) and np.all(bw.dX == 0)
+
+
+def test_constant_gradient_exact_under_agp_off():
+    """R = 0 groups: codes 0, S = 0, Z' = Z, so the plain quantizer returns the exact product."""
+    layer = LayerShape("lin", "linear", 4, 6, 3)
+    x, w, _ = draw_layer(layer, Recipe(), 0)
+    dy = np.full((4, 3), 0.75, F32)
+    bw = fqt.layer_backward(x, w, dy, 2, fqt.AGP_OFF)
+    sx = np.where(x > 0, 1.0, -1.0)
+    sw = np.where(w > 0, 1.0, -1.0)
+    np.testing.assert_allclose(bw.dW, dy.T.astype(np.float64) @ sx, rtol=1e-12)
+    np.testing.assert_allclose(bw.dX, dy.astype(np.float64) @ sw, rtol=1e-12)
+
+
+@pytest.mark.parametrize("layer,bits", [(LayerShape("lin", "linear", 8, 6, 6), 2),
+                                        (LayerShape("c3", "conv2d", 4, 2, 4, 3, 3, 3, 3, 1, 1, 1, 1), 4)],
+                         ids=["linear_b2", "conv_b4"])
+def test_layer_unbiased_over_seeds(layer, bits):
+    """E[dX_hat] = dY sign(Theta)^T and E[dW_hat] = sign(H)^T dY: the FQT gradients are
+    unbiased estimates of the QAT gradients (Section 3.2; Section 5.2)."""
+    x, w, dy = draw_layer(layer, Recipe("sample_lognormal", sigma=1.0), 4)
+    x4 = torch.from_numpy(fqt.as_nchw(x).astype(np.float64))
+    w4 = torch.from_numpy(fqt.as_nchw(w).astype(np.float64))
+    g = torch.from_numpy(fqt.as_nchw(dy).astype(np.float64))
+    sx = F.pad(torch.where(x4 > 0, 1.0, -1.0).double(), (layer.pw,) * 2 + (layer.ph,) * 2, value=-1.0)
+    sw = torch.where(w4 > 0, 1.0, -1.0).double()
+    dW_qat = torch.nn.grad.conv2d_weight(sx, tuple(w4.shape), g, stride=layer.stride).numpy()
+    dX_qat = torch.nn.grad.conv2d_input(tuple(x4.shape), sw, g, stride=layer.stride,
+                                        padding=layer.pad).numpy()
+    S = 1500
+    aw, aw2, ax, ax2 = 0, 0, 0, 0
+    for seed in range(S):
+        bw = fqt.layer_backward(x, w, dy, bits, seed=seed, stride=layer.stride, pad=layer.pad)
+        dWs = bw.dW.reshape(dW_qat.shape)
+        dXs = bw.dX.reshape(dX_qat.shape)
+        aw, aw2, ax, ax2 = aw + dWs, aw2 + dWs ** 2, ax + dXs, ax2 + dXs ** 2
+    for tot, tot2, ref in ((aw, aw2, dW_qat), (ax, ax2, dX_qat)):
+        mean = tot / S
+        sd = np.sqrt(np.maximum(tot2 / S - mean ** 2, 0))
+        assert np.all(np.abs(mean - ref) <= 5.5 * sd / np.sqrt(S) + 1e-9 * np.abs(ref).max())
+
+
+def _agp_exact_variance(g, b, p):
+    """Var[(m/p) Q(x)] = Var_SR / p + x^2 (1-p)/p per element, Var_SR = (R/B)^2 f(1-f)
+    (from the AGP definition of Section 5.2 and Prop. B.1)."""
+    B = (1 << b) - 1
+    st = fqt.group_stats(g[:, :, None, None])
+    v = np.minimum((g - st.Z_s[:, None]) * (F32(B) / st.R_s[:, None]), F32(B)).astype(np.float64)
+    f = v - np.floor(v)
+    return ((st.R_s[:, None].astype(np.float64) / B) ** 2 * f * (1 - f) / p[:, None]
+            + g.astype(np.float64) ** 2 * (1 - p[:, None]) / p[:, None]), st
+
+
+def _agp_monte_carlo(g, b, S):
+    N, D = g.shape
+    tot = np.zeros((N, D))
+    sq = np.zeros((N, D))
+    for seed in range(S):
+        qg = fqt.agp_scq_quantize(g, b, seed=seed)
+        est = np.zeros((N, D))
+        k = qg.samples.keep
+        est[k] = (qg.samples.scale[k, None].astype(np.float64) * qg.q_psq[k, :, 0, 0]
+                  + qg.samples.offset[k, None])
+        tot += est
+        sq += est ** 2
+    mean = tot / S
+    return mean, sq / S - mean ** 2, qg.samples.prob.astype(np.float64)
+
+
+def test_agp_variance_exact_form():
+    """Monte-Carlo variance of the AGP+PSQ estimator matches the exact per-element form."""
+    rng = np.random.default_rng(7)
+    scale = np.array([4, 3, 2, 1.5, 1, 0.8, 0.6, 0.5], dtype=F32)
+    g = (rng.standard_normal((8, 16)).astype(F32) * scale[:, None]).astype(F32)
+    mean, var, p = _agp_monte_carlo(g, 2, 6000)
+    assert p.min() > 0.1
+    exact, _ = _agp_exact_variance(g, 2, p)
+    np.testing.assert_allclose(var, exact, rtol=0.15, atol=1e-9)
+    assert np.all(np.abs(mean - g) <= 6 * np.sqrt(exact / 6000) + 1e-9)
+
+
+def test_agp_variance_eq24_regime():
+    """In Appendix B.2's regime (tiny pruned ranges r/R ~ 0, equal large ranges) the
+    variance of AGP+PSQ obeys Eq. 24, D/(4B^2) sum over the N/b largest R_i^2, and is far
+    below 1-bit PSQ's D/4 sum_i R_i^2."""
+    rng = np.random.default_rng(7)
+    N, D, b = 8, 16, 2
+    B = 3
+    scale = np.array([10, 10, 10, 10, 1e-3, 1e-3, 1e-3, 1e-3], dtype=F32)
+    g = (rng.standard_normal((N, D)).astype(F32) * scale[:, None]).astype(F32)
+    mean, var, p = _agp_monte_carlo(g, b, 3000)
+    exact, st = _agp_exact_variance(g, b, p)
+    assert var.sum() <= D / (4 * B * B) * float((np.sort(st.R_s.astype(np.float64))[-N // b:] ** 2).sum())
+    eq24 = D / (4 * B * B) * float((np.sort(st.R_s.astype(np.float64))[-N // b:] ** 2).sum())
+    assert exact.sum() <= eq24 * 1.05
+    assert exact.sum() < D / 4 * float((st.R_s.astype(np.float64) ** 2).sum())
