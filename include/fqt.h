@@ -1,0 +1,205 @@
+/*
+ * fqt.h -- C ABI of libfqt, the MI355X (gfx950) backward pass of binary linear and
+ * convolution layers under 1-bit fully quantized training with Activation
+ * Gradient Pruning (AGP) and Sample-Channel joint Quantization (SCQ).
+ *
+ * Method: Gao et al., "1-Bit FQT: Pushing the Limit of Fully Quantized Training
+ * to 1-bit" (arXiv 2408.14267).  Section 5.2 defines AGP and the lossless
+ * bit-plane decomposition, Section 5.3 SCQ (per-sample codes feed the
+ * activation gradient dX, per-channel codes feed the weight gradient dW),
+ * Appendix C Alg. 1 the backward sequence (pruner, PSQ/PCQ, encoders, binary
+ * products, dequantization), Alg. 2 the row encoder, and the Unfolder/Folder
+ * for convolutions.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are NCHW, torch layout: X [N][C][H][W], W [D][C][kh][kw],
+ *    dY [N][D][Ho][Wo], dX like X, dW like W (fp32).  A linear layer is the
+ *    case H = W = kh = kw = 1 (X [N][C], W [D][C], dY [N][D]).
+ *  - Every tensor pointer is a DEVICE pointer on the current HIP device; the
+ *    caller owns all memory; the library never allocates, never synchronizes
+ *    the stream and keeps no state between calls.  Work is enqueued on
+ *    `hip_stream` (a hipStream_t; NULL = the null stream); outputs are valid
+ *    once that stream has reached the enqueued work.
+ *  - Descriptor structs are HOST pointers, read during the call only.
+ *  - Arguments are validated on the host before anything is launched; a
+ *    failing validation returns a negative fqt_status and launches nothing.
+ *    A failed launch returns FQT_E_HIP.  No C++ exception crosses the ABI.
+ *  - Alignment: float/bf16 tensors 16 bytes, uint64 bit arrays 8 bytes, int32
+ *    and float32 arrays 4 bytes, workspaces 256 bytes (FQT_E_ALIGN otherwise).
+ *  - Bit packing: bit j of a packed line is bit (j % 64) of 64-bit word j / 64,
+ *    least significant bit first; ragged tails are zero.  A set bit is +1, a
+ *    clear bit -1 (sign(x) = -1 for x <= 0, Section 5.1), or a code bit.
+ *  - Inputs must be finite; NaN/Inf gradients give unspecified codes.
+ */
+#ifndef FQT_H
+#define FQT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FQT_OK = 0,
+  FQT_E_INVAL = -1,     /* scalar argument out of range (kind, bits, agp_mode, axis, ...)   */
+  FQT_E_DTYPE = -2,     /* unsupported dtype or dtype combination                           */
+  FQT_E_SHAPE = -3,     /* non-positive or inconsistent dims, or a size limit exceeded      */
+  FQT_E_WORKSPACE = -4, /* workspace smaller than fqt_workspace_size() reports              */
+  FQT_E_ALIGN = -5,     /* a pointer violates the alignment rule above                      */
+  FQT_E_NULL = -6,      /* a required pointer is NULL                                       */
+  FQT_E_HIP = -7        /* a HIP runtime call or kernel launch failed                       */
+} fqt_status;
+
+typedef enum { FQT_F32 = 0, FQT_BF16 = 1 } fqt_dtype;
+
+typedef enum { FQT_LINEAR = 0, FQT_CONV2D = 1 } fqt_layer_kind;
+
+typedef enum {
+  FQT_AGP_BERNOULLI = 0, /* Section 5.2: p_i proportional to the group range, sum p_i = G/b,
+                            capped at 1 (water-filling), masks m_i ~ Bern(p_i), 1/p rescale */
+  FQT_AGP_TOPK = 1,      /* Appendix B.2's limit p in {0,1}: keep the max(1, G/b) largest
+                            ranges, no rescale (biased; provided for study)                */
+  FQT_AGP_OFF = 2        /* plain b-bit PSQ/PCQ (Section 5.2): every group kept, p = 1      */
+} fqt_agp_mode;
+
+/* Limits.  The AGP sort of one group set runs in one workgroup's LDS. */
+#define FQT_MAX_BITS 8
+#define FQT_MAX_AGP_GROUPS 16384   /* N and D bound for BERNOULLI / TOPK               */
+
+/* Layer geometry (Section 3, Eq. 1-3; Appendix C Unfolder: X_u is NHW x CK^2).
+ * Ho = (H + 2 ph - kh) / sh + 1 and Wo likewise must be >= 1.
+ * dy_dtype, x_dtype, dx_dtype: FQT_F32 or FQT_BF16; w_dtype: FQT_F32 or FQT_BF16.
+ * N*Ho*Wo, N*C*H*W and N*D*Ho*Wo must stay below 2^31. */
+typedef struct {
+  int32_t kind;                       /* fqt_layer_kind                                  */
+  int32_t dy_dtype, x_dtype, w_dtype, dx_dtype;
+  int64_t N, C, H, W, D;              /* linear: H = W = 1, C = in features, D = out     */
+  int32_t kh, kw, sh, sw, ph, pw;     /* linear: 1, 1, 1, 1, 0, 0                        */
+} fqt_layer_desc;
+
+/* Quantizer configuration (Section 3.2 quantizer; Section 5.2 AGP keep ratio 1/b).
+ * The random words come from Philox4x32-10 (Salmon et al., SC'11) with key = seed
+ * and counter (lo32(i >> 2), hi32(i >> 2) | stream << 30, layer_id, step), word i & 3,
+ * where i is the element's NCHW index of dY (stream 0), the sample id (stream 1)
+ * or the output-channel id (stream 2). */
+typedef struct {
+  int32_t bits;                       /* b in [1, FQT_MAX_BITS]: code width of kept groups  */
+  int32_t agp_mode;                   /* fqt_agp_mode                                       */
+  uint64_t seed;
+  uint32_t step;
+  uint32_t layer_id;
+} fqt_quant_cfg;
+
+/* Quantized output gradient (Section 5.3, SCQ; Appendix C Alg. 1 quantization and
+ * encoding).  All members are device pointers sized to capacity; the caller owns
+ * them.  With P = Ho*Wo, R = N*P, Wd = ceil(D/64), Wr = ceil(R/64), b = bits:
+ *   psq_planes  uint64 [b][R][Wd]   PSQ code planes, plane k = bit k of the code; row
+ *                                   j*P + p holds pixel p of the j-th kept sample
+ *                                   (kept samples in ascending order), packed along D.
+ *                                   Rows >= count*P are left untouched.
+ *   pcq_planes  uint64 [b][D][Wr]   PCQ code planes; row j holds the j-th kept channel,
+ *                                   packed along (n, ho, wo).  Rows >= count untouched.
+ *   psq_kept    int32 [N]           kept sample ids ascending, then pruned ids ascending
+ *   psq_count   int32 [1]           number of kept samples
+ *   psq_scale   float [N]           S_n = R_n / (B p_n) if kept, else 0
+ *   psq_offset  float [N]           Z'_n = Z_n / p_n if kept, else 0
+ *   psq_prob    float [N]           keep probability p_n
+ *   pcq_*       the same for the D output channels. */
+typedef struct {
+  uint64_t *psq_planes;
+  uint64_t *pcq_planes;
+  int32_t *psq_kept, *psq_count, *pcq_kept, *pcq_count;
+  float *psq_scale, *psq_offset, *psq_prob;
+  float *pcq_scale, *pcq_offset, *pcq_prob;
+} fqt_qgrad;
+
+/* Element counts of the two plane arrays of fqt_qgrad (host call, no device work). */
+int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                    int64_t *psq_words, int64_t *pcq_words);
+
+/* Workspace sizes (host call).  which = FQT_WS_QUANTIZE for fqt_agp_scq_quantize,
+ * FQT_WS_LAYER for fqt_layer_backward (which holds an fqt_qgrad and the packed signs
+ * inside it).  The library carves the workspace; its contents need no initialisation
+ * and are garbage after the call. */
+#define FQT_WS_QUANTIZE 0
+#define FQT_WS_LAYER 1
+int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
+                       size_t *bytes);
+
+/* AGP + SCQ quantization of dY (Section 5.2 AGP; Section 5.3 SCQ; Appendix C Alg. 1
+ * pruner, PSQ/PCQ, row/column encoders).  Per-sample and per-channel range R = max - min
+ * and zero point Z = min (float32); AGP keep probabilities and Bernoulli masks for both
+ * group sets; for every element of a kept sample (kept channel) a b-bit stochastic
+ * rounding code q = floor(v) + [u24 < frac(v) 2^24], v = clamp((x - Z) * (B / R), 0, B)
+ * in float32, B = 2^b - 1, one Philox word per element shared by its PSQ and PCQ code;
+ * codes split into b bit planes and packed (row encoder along D for PSQ, column encoder
+ * along N*Ho*Wo for PCQ).  dY has desc->dy_dtype.  Writes every member of *out.
+ * ws: >= fqt_workspace_size(FQT_WS_QUANTIZE) bytes. */
+int fqt_agp_scq_quantize(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *dY,
+                         const fqt_qgrad *out, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Sign-bit packing (Section 5.1 binarizer; Appendix C Alg. 2 row/column encoders and
+ * the Unfolder).  src has dtype `dtype` (FQT_F32 / FQT_BF16).
+ *   axis = FQT_PACK_ALONG_COLS: src is a row-major [rows][cols] matrix with leading
+ *          dimension ld (elements); dst is uint64 [rows][ceil(cols/64)], bit j of line i
+ *          = src[i][j] > 0.
+ *   axis = FQT_PACK_ALONG_ROWS: same src; dst is uint64 [cols][ceil(rows/64)], bit i of
+ *          line j = src[i][j] > 0 (the column encoder; W [D][C*kh*kw] packed along D).
+ *   axis = FQT_PACK_IM2COL: src is the conv input X of `conv`; rows/cols/ld are ignored;
+ *          dst is uint64 [C*kh*kw][ceil(N*Ho*Wo/64)], bit (n, ho, wo) of line (c, i, j)
+ *          = X[n][c][ho*sh - ph + i][wo*sw - pw + j] > 0, and 0 (sign -1) where that
+ *          position lies in the zero padding.
+ * linesum (optional, int32 [lines]) receives sum over the line of the +-1 signs,
+ * 2 * popcount - length.  conv must be non-NULL exactly for FQT_PACK_IM2COL. */
+#define FQT_PACK_ALONG_ROWS 0
+#define FQT_PACK_ALONG_COLS 1
+#define FQT_PACK_IM2COL 2
+int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, int64_t ld,
+                  int32_t axis, const fqt_layer_desc *conv, uint64_t *dst, int32_t *linesum,
+                  void *hip_stream);
+
+/* Weight-gradient product with PCQ codes (Section 5.3, SCQ; Appendix C Alg. 1 binary
+ * product and dequantization; {0,1} <-> {+-1} conversion):
+ *   I[d][k]  = sum_r q_pcq[d][r] * s_X[r][k]   (k over C*kh*kw, r over N*Ho*Wo), computed
+ *              as sum_p 2^p (2 popcount(a_p & t) - popcount(a_p)) over packed words;
+ *   dW[d][k] = S_d * I[d][k] + Z'_d * c_X[k] in float32 for kept channels, 0 for pruned.
+ * xsign: uint64 [C*kh*kw][ceil(N*Ho*Wo/64)] (fqt_pack_bits IM2COL, or ALONG_ROWS of X for
+ * a linear layer); xsign_sum: int32 [C*kh*kw], c_X = its line sums.  dW: float [D][C*kh*kw].
+ * I_out (optional): int32 [D][C*kh*kw] receives I (0 in pruned rows). */
+int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                       const fqt_qgrad *q, const uint64_t *xsign, const int32_t *xsign_sum,
+                       float *dW, int32_t *I_out, void *hip_stream);
+
+/* Activation-gradient product with PSQ codes (Section 5.3, SCQ; Appendix C Alg. 1, and
+ * the Folder for convolutions):
+ *   I[n][c][h][w] = sum over kernel taps (i, j) that map an output pixel (ho, wo) onto
+ *                   (h, w) of sum_d q_psq[n][d][ho][wo] * s_W[d][c][i][j];
+ *   c[c][h][w]    = sum over the same taps of sum_d s_W[d][c][i][j];
+ *   dX            = S_n * I + Z'_n * c in float32 (rounded to bf16 if dx_dtype is bf16)
+ *                   for kept samples, 0 for pruned samples.
+ * This is the unfolded product followed by the folder, taken in integers.  wsign: uint64
+ * [C*kh*kw][ceil(D/64)] (fqt_pack_bits ALONG_ROWS of W viewed as [D][C*kh*kw]);
+ * wsign_sum: int32 [C*kh*kw].  dX: [N][C][H][W] of dx_dtype.  I_out (optional): int32
+ * [N][C][H][W]. */
+int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                       const fqt_qgrad *q, const uint64_t *wsign, const int32_t *wsign_sum,
+                       void *dX, int32_t *I_out, void *hip_stream);
+
+/* Whole layer backward (Appendix C Alg. 1 backward; Section 5.3's final form):
+ * quantize dY, pack sign(X) (im2col for conv) and sign(W), then both products.
+ * X: x_dtype, W: w_dtype, dY: dy_dtype, dX: dx_dtype, dW: float32.
+ * ws: >= fqt_workspace_size(FQT_WS_LAYER) bytes, 256-byte aligned. */
+int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
+                       const void *W, const void *dY, void *dX, float *dW, void *ws,
+                       size_t ws_bytes, void *hip_stream);
+
+/* Static description of a status code. */
+const char *fqt_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FQT_H */

@@ -1,0 +1,287 @@
+// C ABI of libfqt: argument validation, workspace carving and the entry points.
+// Every check runs on the host before anything is launched.
+#include "fqt_internal.hpp"
+
+namespace fqt {
+
+namespace {
+constexpr int64_t LIMIT31 = (int64_t(1) << 31) - 1;
+
+bool dtype_ok(int t) { return t == FQT_F32 || t == FQT_BF16; }
+size_t dtype_size(int t) { return t == FQT_BF16 ? 2 : 4; }
+
+// Sub-allocator over a caller-provided workspace: 256-byte aligned slices.
+struct Carver {
+  char *base;
+  size_t off = 0;
+  template <typename T>
+  T *take(size_t count) {
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += align256(count * sizeof(T));
+    return p;
+  }
+};
+
+struct LayerWs {
+  QuantWs qws;
+  fqt_qgrad q;
+  uint64_t *xsign, *wsign;
+  int32_t *xsum, *wsum;
+};
+
+size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
+  Carver c{static_cast<char *>(ws)};
+  LayerWs w{};
+  w.qws.smin = c.take<int32_t>(L.N);
+  w.qws.smax = c.take<int32_t>(L.N);
+  w.qws.cmin = c.take<int32_t>(L.D);
+  w.qws.cmax = c.take<int32_t>(L.D);
+  w.qws.sp = c.take<GroupParam>(L.N);
+  w.qws.cp = c.take<GroupParam>(L.D);
+  w.q.psq_planes = c.take<uint64_t>(size_t(bits) * L.R * L.Wd);
+  w.q.pcq_planes = c.take<uint64_t>(size_t(bits) * L.D * L.Wr);
+  w.q.psq_kept = c.take<int32_t>(L.N);
+  w.q.psq_count = c.take<int32_t>(1);
+  w.q.pcq_kept = c.take<int32_t>(L.D);
+  w.q.pcq_count = c.take<int32_t>(1);
+  w.q.psq_scale = c.take<float>(L.N);
+  w.q.psq_offset = c.take<float>(L.N);
+  w.q.psq_prob = c.take<float>(L.N);
+  w.q.pcq_scale = c.take<float>(L.D);
+  w.q.pcq_offset = c.take<float>(L.D);
+  w.q.pcq_prob = c.take<float>(L.D);
+  w.xsign = c.take<uint64_t>(size_t(L.K) * L.Wr);
+  w.xsum = c.take<int32_t>(L.K);
+  w.wsign = c.take<uint64_t>(size_t(L.K) * L.Wd);
+  w.wsum = c.take<int32_t>(L.K);
+  if (out) *out = w;
+  return c.off;
+}
+
+int check_qgrad(const fqt_qgrad *q, bool psq, bool pcq) {
+  if (!q) return FQT_E_NULL;
+  if (psq) {
+    if (!q->psq_planes || !q->psq_kept || !q->psq_count || !q->psq_scale || !q->psq_offset ||
+        !q->psq_prob)
+      return FQT_E_NULL;
+    if (!aligned(q->psq_planes, 8) || !aligned(q->psq_kept, 4) || !aligned(q->psq_count, 4) ||
+        !aligned(q->psq_scale, 4) || !aligned(q->psq_offset, 4) || !aligned(q->psq_prob, 4))
+      return FQT_E_ALIGN;
+  }
+  if (pcq) {
+    if (!q->pcq_planes || !q->pcq_kept || !q->pcq_count || !q->pcq_scale || !q->pcq_offset ||
+        !q->pcq_prob)
+      return FQT_E_NULL;
+    if (!aligned(q->pcq_planes, 8) || !aligned(q->pcq_kept, 4) || !aligned(q->pcq_count, 4) ||
+        !aligned(q->pcq_scale, 4) || !aligned(q->pcq_offset, 4) || !aligned(q->pcq_prob, 4))
+      return FQT_E_ALIGN;
+  }
+  return FQT_OK;
+}
+
+#define FQT_TRY(expr)              \
+  do {                             \
+    const int st__ = (expr);       \
+    if (st__ != FQT_OK) return st__; \
+  } while (0)
+
+}  // namespace
+
+int make_layer(const fqt_layer_desc *d, Layer *L) {
+  if (!d) return FQT_E_NULL;
+  if (d->kind != FQT_LINEAR && d->kind != FQT_CONV2D) return FQT_E_INVAL;
+  if (!dtype_ok(d->dy_dtype) || !dtype_ok(d->x_dtype) || !dtype_ok(d->w_dtype) ||
+      !dtype_ok(d->dx_dtype))
+    return FQT_E_DTYPE;
+  if (d->N <= 0 || d->C <= 0 || d->H <= 0 || d->W <= 0 || d->D <= 0) return FQT_E_SHAPE;
+  if (d->kh <= 0 || d->kw <= 0 || d->sh <= 0 || d->sw <= 0 || d->ph < 0 || d->pw < 0)
+    return FQT_E_SHAPE;
+  if (d->kind == FQT_LINEAR &&
+      (d->H != 1 || d->W != 1 || d->kh != 1 || d->kw != 1 || d->sh != 1 || d->sw != 1 ||
+       d->ph != 0 || d->pw != 0))
+    return FQT_E_SHAPE;
+  if (d->H + 2 * int64_t(d->ph) < d->kh || d->W + 2 * int64_t(d->pw) < d->kw) return FQT_E_SHAPE;
+  if (d->N > FQT_MAX_AGP_GROUPS || d->D > FQT_MAX_AGP_GROUPS) return FQT_E_SHAPE;
+  Layer l;
+  l.kind = d->kind;
+  l.dy_t = d->dy_dtype; l.x_t = d->x_dtype; l.w_t = d->w_dtype; l.dx_t = d->dx_dtype;
+  l.N = d->N; l.C = d->C; l.H = d->H; l.W = d->W; l.D = d->D;
+  l.kh = d->kh; l.kw = d->kw; l.sh = d->sh; l.sw = d->sw; l.ph = d->ph; l.pw = d->pw;
+  l.Ho = (l.H + 2 * l.ph - l.kh) / l.sh + 1;
+  l.Wo = (l.W + 2 * l.pw - l.kw) / l.sw + 1;
+  if (l.C > LIMIT31 || l.H > LIMIT31 || l.W > LIMIT31) return FQT_E_SHAPE;
+  l.P = l.Ho * l.Wo;
+  l.HW = l.H * l.W;
+  l.K = l.C * l.kh * l.kw;
+  if (l.P > LIMIT31 || l.HW > LIMIT31 || l.K > LIMIT31) return FQT_E_SHAPE;
+  l.R = l.N * l.P;
+  if (l.R > LIMIT31 || l.N * l.C > LIMIT31 / l.HW || l.N * l.D > LIMIT31 / l.P) return FQT_E_SHAPE;
+  l.Wd = (l.D + 63) / 64;
+  l.Wr = (l.R + 63) / 64;
+  *L = l;
+  return FQT_OK;
+}
+
+int check_cfg(const fqt_quant_cfg *c, const Layer &) {
+  if (!c) return FQT_E_NULL;
+  if (c->bits < 1 || c->bits > FQT_MAX_BITS) return FQT_E_INVAL;
+  if (c->agp_mode != FQT_AGP_BERNOULLI && c->agp_mode != FQT_AGP_TOPK &&
+      c->agp_mode != FQT_AGP_OFF)
+    return FQT_E_INVAL;
+  return FQT_OK;
+}
+
+size_t quant_ws_bytes(const Layer &L) {
+  return 2 * align256(size_t(L.N) * 4) + 2 * align256(size_t(L.D) * 4) +
+         align256(size_t(L.N) * sizeof(GroupParam)) + align256(size_t(L.D) * sizeof(GroupParam));
+}
+
+void carve_quant_ws(void *ws, const Layer &L, QuantWs *q) {
+  Carver c{static_cast<char *>(ws)};
+  q->smin = c.take<int32_t>(L.N);
+  q->smax = c.take<int32_t>(L.N);
+  q->cmin = c.take<int32_t>(L.D);
+  q->cmax = c.take<int32_t>(L.D);
+  q->sp = c.take<GroupParam>(L.N);
+  q->cp = c.take<GroupParam>(L.D);
+}
+
+}  // namespace fqt
+
+using namespace fqt;
+
+extern "C" {
+
+const char *fqt_status_string(int status) {
+  switch (status) {
+    case FQT_OK: return "FQT_OK: success";
+    case FQT_E_INVAL: return "FQT_E_INVAL: scalar argument out of range";
+    case FQT_E_DTYPE: return "FQT_E_DTYPE: unsupported dtype or dtype combination";
+    case FQT_E_SHAPE: return "FQT_E_SHAPE: invalid or unsupported shape";
+    case FQT_E_WORKSPACE: return "FQT_E_WORKSPACE: workspace too small";
+    case FQT_E_ALIGN: return "FQT_E_ALIGN: pointer misaligned";
+    case FQT_E_NULL: return "FQT_E_NULL: required pointer is NULL";
+    case FQT_E_HIP: return "FQT_E_HIP: HIP runtime or launch failure";
+    default: return "unknown fqt status";
+  }
+}
+
+int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int64_t *psq_words,
+                    int64_t *pcq_words) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  if (!psq_words || !pcq_words) return FQT_E_NULL;
+  *psq_words = int64_t(cfg->bits) * L.R * L.Wd;
+  *pcq_words = int64_t(cfg->bits) * L.D * L.Wr;
+  return FQT_OK;
+}
+
+int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
+                       size_t *bytes) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  if (!bytes) return FQT_E_NULL;
+  if (which == FQT_WS_QUANTIZE) *bytes = quant_ws_bytes(L);
+  else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, cfg->bits, nullptr);
+  else return FQT_E_INVAL;
+  return FQT_OK;
+}
+
+int fqt_agp_scq_quantize(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *dY,
+                         const fqt_qgrad *out, void *ws, size_t ws_bytes, void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_qgrad(out, true, true));
+  if (!dY || !ws) return FQT_E_NULL;
+  if (!aligned(dY, 16) || !aligned(ws, 256)) return FQT_E_ALIGN;
+  if (ws_bytes < quant_ws_bytes(L)) return FQT_E_WORKSPACE;
+  QuantWs q;
+  carve_quant_ws(ws, L, &q);
+  return launch_quantize(L, *cfg, dY, *out, q, static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, int64_t ld,
+                  int32_t axis, const fqt_layer_desc *conv, uint64_t *dst, int32_t *linesum,
+                  void *hip_stream) {
+  if (!src || !dst) return FQT_E_NULL;
+  if (!dtype_ok(dtype)) return FQT_E_DTYPE;
+  if (!aligned(src, dtype_size(dtype)) || !aligned(dst, 8) || (linesum && !aligned(linesum, 4)))
+    return FQT_E_ALIGN;
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (axis == FQT_PACK_IM2COL) {
+    if (!conv) return FQT_E_NULL;
+    Layer L;
+    FQT_TRY(make_layer(conv, &L));
+    if (int64_t(L.K) * L.Wr > LIMIT31 * 4) return FQT_E_SHAPE;
+    return launch_pack_bits(src, dtype, 0, 0, 0, axis, &L, dst, linesum, s);
+  }
+  if (axis != FQT_PACK_ALONG_ROWS && axis != FQT_PACK_ALONG_COLS) return FQT_E_INVAL;
+  if (conv) return FQT_E_INVAL;
+  if (rows <= 0 || cols <= 0 || ld < cols) return FQT_E_SHAPE;
+  if (axis == FQT_PACK_ALONG_ROWS && ((rows + 63) / 64 > 65535 || (cols + 63) / 64 > LIMIT31))
+    return FQT_E_SHAPE;
+  if (axis == FQT_PACK_ALONG_COLS && rows * ((cols + 63) / 64) > LIMIT31 * 4) return FQT_E_SHAPE;
+  if (rows > LIMIT31 || cols > LIMIT31) return FQT_E_SHAPE;
+  return launch_pack_bits(src, dtype, rows, cols, ld, axis, nullptr, dst, linesum, s);
+}
+
+int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
+                       const uint64_t *xsign, const int32_t *xsign_sum, float *dW, int32_t *I_out,
+                       void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_qgrad(q, false, true));
+  if (!xsign || !xsign_sum || !dW) return FQT_E_NULL;
+  if (!aligned(xsign, 8) || !aligned(xsign_sum, 4) || !aligned(dW, 4) ||
+      (I_out && !aligned(I_out, 4)))
+    return FQT_E_ALIGN;
+  return launch_gemm_dw(L, *cfg, *q, xsign, xsign_sum, dW, I_out,
+                        static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
+                       const uint64_t *wsign, const int32_t *wsign_sum, void *dX, int32_t *I_out,
+                       void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_qgrad(q, true, false));
+  if (!wsign || !wsign_sum || !dX) return FQT_E_NULL;
+  if (!aligned(wsign, 8) || !aligned(wsign_sum, 4) || !aligned(dX, dtype_size(L.dx_t)) ||
+      (I_out && !aligned(I_out, 4)))
+    return FQT_E_ALIGN;
+  return launch_gemm_dx(L, *cfg, *q, wsign, wsign_sum, dX, I_out,
+                        static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
+                       const void *W, const void *dY, void *dX, float *dW, void *ws,
+                       size_t ws_bytes, void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  if (!X || !W || !dY || !dX || !dW || !ws) return FQT_E_NULL;
+  if (!aligned(dY, 16) || !aligned(X, dtype_size(L.x_t)) || !aligned(W, dtype_size(L.w_t)) ||
+      !aligned(dX, dtype_size(L.dx_t)) || !aligned(dW, 4) || !aligned(ws, 256))
+    return FQT_E_ALIGN;
+  if (ws_bytes < carve_layer_ws(nullptr, L, cfg->bits, nullptr)) return FQT_E_WORKSPACE;
+  LayerWs w;
+  carve_layer_ws(ws, L, cfg->bits, &w);
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
+  if (L.kind == FQT_LINEAR)
+    FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,
+                             w.xsum, s));
+  else
+    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, w.xsum, s));
+  FQT_TRY(launch_pack_bits(W, L.w_t, L.D, L.K, L.K, FQT_PACK_ALONG_ROWS, nullptr, w.wsign, w.wsum,
+                           s));
+  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, w.xsum, dW, nullptr, s));
+  return launch_gemm_dx(L, *cfg, w.q, w.wsign, w.wsum, dX, nullptr, s);
+}
+
+}  // extern "C"

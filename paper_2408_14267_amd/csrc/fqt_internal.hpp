@@ -1,0 +1,154 @@
+// Internal declarations of libfqt: validated layer geometry, workspace carving,
+// kernel launchers and the device helpers shared by the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fqt.h"
+
+namespace fqt {
+
+// ----------------------------------------------------------------------------- host side
+
+// Layer geometry after validation; every derived size the kernels need.
+struct Layer {
+  int kind;
+  int dy_t, x_t, w_t, dx_t;
+  int64_t N, C, H, W, D;
+  int kh, kw, sh, sw, ph, pw;
+  int64_t Ho, Wo;
+  int64_t P;    // output pixels per sample, Ho*Wo
+  int64_t R;    // rows of the unfolded gradient, N*P
+  int64_t K;    // unfolded weight width, C*kh*kw
+  int64_t HW;   // input pixels per sample, H*W
+  int64_t Wd;   // 64-bit words of a line packed along D
+  int64_t Wr;   // 64-bit words of a line packed along R
+};
+
+// Per-group parameters the quantize kernel reads (written by the select kernel).
+struct GroupParam {
+  float z;        // zero point Z (the group minimum)
+  float inv;      // B / R in float32, 0 when R == 0
+  int32_t rank;   // position among the kept groups (ascending ids), -1 if pruned
+  int32_t pad;
+};
+
+// Quantize workspace: ordered-int min/max keys of both group sets, and their params.
+struct QuantWs {
+  int32_t *smin, *smax;    // [N]
+  int32_t *cmin, *cmax;    // [D]
+  GroupParam *sp;          // [N]
+  GroupParam *cp;          // [D]
+};
+
+int make_layer(const fqt_layer_desc *d, Layer *L);
+int check_cfg(const fqt_quant_cfg *c, const Layer &L);
+size_t quant_ws_bytes(const Layer &L);
+void carve_quant_ws(void *ws, const Layer &L, QuantWs *q);
+inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Launchers (stream-ordered, no synchronisation).  They return an fqt_status.
+int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
+                    const QuantWs &w, hipStream_t s);
+int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                     const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s);
+int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                   const uint64_t *xsign, const int32_t *xsum, float *dW, int32_t *I_out,
+                   hipStream_t s);
+int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                   const uint64_t *wsign, const int32_t *wsum, void *dX, int32_t *I_out,
+                   hipStream_t s);
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
+inline int last_launch_status() { return hip_status(hipGetLastError()); }
+
+// ----------------------------------------------------------------------------- device side
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the 4x32 S-box
+// with multipliers M0 = 0xD2511F53, M1 = 0xCD9E8D57 and Weyl key increments
+// W0 = 0x9E3779B9, W1 = 0xBB67AE85 between rounds.
+struct Ctr4 {
+  uint32_t v[4];
+};
+
+__device__ __forceinline__ Ctr4 philox4x32_10(Ctr4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c.v[0];
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.v[0]);
+    const uint32_t lo1 = 0xCD9E8D57u * c.v[2];
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.v[2]);
+    Ctr4 n;
+    n.v[0] = hi1 ^ c.v[1] ^ k0;
+    n.v[1] = lo1;
+    n.v[2] = hi0 ^ c.v[3] ^ k1;
+    n.v[3] = lo0;
+    c = n;
+  }
+  return c;
+}
+
+enum : uint32_t { STREAM_ELEM = 0, STREAM_SAMPLE = 1, STREAM_CHANNEL = 2 };
+
+// The four words of the Philox block holding items 4*blk .. 4*blk+3 of a stream.
+__device__ __forceinline__ Ctr4 philox_block(uint64_t blk, uint32_t stream, uint64_t seed,
+                                             uint32_t step, uint32_t layer) {
+  Ctr4 c;
+  c.v[0] = static_cast<uint32_t>(blk);
+  c.v[1] = (static_cast<uint32_t>(blk >> 32) & 0x3FFFFFFFu) | (stream << 30);
+  c.v[2] = layer;
+  c.v[3] = step;
+  return philox4x32_10(c, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32));
+}
+
+// Order-preserving map float -> int32 (for atomicMin/atomicMax on float values).
+__device__ __forceinline__ int32_t f2key(float f) {
+  const int32_t i = __float_as_int(f);
+  return i >= 0 ? i : (i ^ 0x7FFFFFFF);
+}
+__device__ __forceinline__ float key2f(int32_t k) {
+  return __int_as_float(k >= 0 ? k : (k ^ 0x7FFFFFFF));
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+// float32 -> bfloat16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Load one element of a float32 or bfloat16 tensor as float32.
+__device__ __forceinline__ float load_elem(const void *p, int dtype, int64_t i) {
+  return dtype == FQT_BF16 ? bf16_to_f32(static_cast<const uint16_t *>(p)[i])
+                           : static_cast<const float *>(p)[i];
+}
+
+// Load four consecutive elements starting at i (i % 4 == 0, base 16-byte aligned).
+__device__ __forceinline__ void load_quad(const void *p, int dtype, int64_t i, float out[4]) {
+  if (dtype == FQT_BF16) {
+    const uint2 v = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(p) + i);
+    out[0] = __uint_as_float(v.x << 16);
+    out[1] = __uint_as_float(v.x & 0xFFFF0000u);
+    out[2] = __uint_as_float(v.y << 16);
+    out[3] = __uint_as_float(v.y & 0xFFFF0000u);
+  } else {
+    const float4 v = *reinterpret_cast<const float4 *>(static_cast<const float *>(p) + i);
+    out[0] = v.x;
+    out[1] = v.y;
+    out[2] = v.z;
+    out[3] = v.w;
+  }
+}
+
+__device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }
+
+}  // namespace fqt

@@ -1,0 +1,196 @@
+"""ctypes binding of libfqt (the C ABI declared in include/fqt.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libfqt.so.  Functions keep the C names; tensors are torch tensors
+on the current HIP device (their data pointers are passed through) and
+`stream` defaults to torch's current stream.  A non-zero status raises
+FqtError.  Importing this module raises if libfqt.so has not been built --
+there is no fallback path.
+"""
+import ctypes
+import os
+from ctypes import POINTER, Structure, c_char_p, c_int, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfqt.so")
+
+FQT_OK = 0
+FQT_E_INVAL, FQT_E_DTYPE, FQT_E_SHAPE, FQT_E_WORKSPACE, FQT_E_ALIGN, FQT_E_NULL, FQT_E_HIP = range(-1, -8, -1)
+FQT_F32, FQT_BF16 = 0, 1
+FQT_LINEAR, FQT_CONV2D = 0, 1
+FQT_AGP_BERNOULLI, FQT_AGP_TOPK, FQT_AGP_OFF = 0, 1, 2
+FQT_PACK_ALONG_ROWS, FQT_PACK_ALONG_COLS, FQT_PACK_IM2COL = 0, 1, 2
+FQT_WS_QUANTIZE, FQT_WS_LAYER = 0, 1
+FQT_MAX_BITS = 8
+FQT_MAX_AGP_GROUPS = 16384
+EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_agp_scq_quantize",
+            "fqt_pack_bits", "fqt_binary_gemm_dw", "fqt_binary_gemm_dx", "fqt_layer_backward")
+
+
+class FqtError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {fqt_status_string(status)} ({status})")
+
+
+class fqt_layer_desc(Structure):
+    _fields_ = [("kind", c_int32), ("dy_dtype", c_int32), ("x_dtype", c_int32),
+                ("w_dtype", c_int32), ("dx_dtype", c_int32),
+                ("N", c_int64), ("C", c_int64), ("H", c_int64), ("W", c_int64), ("D", c_int64),
+                ("kh", c_int32), ("kw", c_int32), ("sh", c_int32), ("sw", c_int32),
+                ("ph", c_int32), ("pw", c_int32)]
+
+
+class fqt_quant_cfg(Structure):
+    _fields_ = [("bits", c_int32), ("agp_mode", c_int32), ("seed", c_uint64),
+                ("step", c_uint32), ("layer_id", c_uint32)]
+
+
+class fqt_qgrad(Structure):
+    _fields_ = [("psq_planes", c_void_p), ("pcq_planes", c_void_p),
+                ("psq_kept", c_void_p), ("psq_count", c_void_p),
+                ("pcq_kept", c_void_p), ("pcq_count", c_void_p),
+                ("psq_scale", c_void_p), ("psq_offset", c_void_p), ("psq_prob", c_void_p),
+                ("pcq_scale", c_void_p), ("pcq_offset", c_void_p), ("pcq_prob", c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                           "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(LIB_PATH)
+    D, Q, G = POINTER(fqt_layer_desc), POINTER(fqt_quant_cfg), POINTER(fqt_qgrad)
+    sig = {
+        "fqt_status_string": (c_char_p, [c_int]),
+        "fqt_qgrad_words": (c_int, [D, Q, POINTER(c_int64), POINTER(c_int64)]),
+        "fqt_workspace_size": (c_int, [D, Q, c_int32, POINTER(c_size_t)]),
+        "fqt_agp_scq_quantize": (c_int, [D, Q, c_void_p, G, c_void_p, c_size_t, c_void_p]),
+        "fqt_pack_bits": (c_int, [c_void_p, c_int32, c_int64, c_int64, c_int64, c_int32, D,
+                                  c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dw": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dx": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_size_t, c_void_p]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+# ----------------------------------------------------------------------------- marshalling helpers
+
+def _ptr(t):
+    return None if t is None else c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(status, where):
+    if status != FQT_OK:
+        raise FqtError(status, where)
+
+
+def dtype_code(dt):
+    if dt in (torch.float32, "f32"):
+        return FQT_F32
+    if dt in (torch.bfloat16, "bf16"):
+        return FQT_BF16
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def layer_desc(shape, dy_dtype=FQT_F32, x_dtype=FQT_F32, w_dtype=FQT_F32, dx_dtype=FQT_F32):
+    """fqt_layer_desc from an object with kind/N/C/H/W/D/kh/kw/sh/sw/ph/pw attributes."""
+    return fqt_layer_desc(FQT_LINEAR if shape.kind == "linear" else FQT_CONV2D,
+                          dy_dtype, x_dtype, w_dtype, dx_dtype,
+                          shape.N, shape.C, shape.H, shape.W, shape.D,
+                          shape.kh, shape.kw, shape.sh, shape.sw, shape.ph, shape.pw)
+
+
+def quant_cfg(bits, agp_mode=FQT_AGP_BERNOULLI, seed=0, step=0, layer_id=0):
+    return fqt_quant_cfg(bits, agp_mode, seed, step, layer_id)
+
+
+# ----------------------------------------------------------------------------- C entry points
+
+def fqt_status_string(status):
+    return _lib.fqt_status_string(status).decode()
+
+
+def fqt_qgrad_words(desc, cfg):
+    a, b = c_int64(), c_int64()
+    _check(_lib.fqt_qgrad_words(desc, cfg, ctypes.byref(a), ctypes.byref(b)), "fqt_qgrad_words")
+    return a.value, b.value
+
+
+def fqt_workspace_size(desc, cfg, which=FQT_WS_LAYER):
+    n = c_size_t()
+    _check(_lib.fqt_workspace_size(desc, cfg, which, ctypes.byref(n)), "fqt_workspace_size")
+    return n.value
+
+
+def fqt_agp_scq_quantize(desc, cfg, dY, qgrad, ws, stream=None):
+    _check(_lib.fqt_agp_scq_quantize(desc, cfg, _ptr(dY), ctypes.byref(qgrad.struct), _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream(stream)),
+           "fqt_agp_scq_quantize")
+
+
+def fqt_pack_bits(src, dtype, rows, cols, ld, axis, conv, dst, linesum=None, stream=None):
+    _check(_lib.fqt_pack_bits(_ptr(src), dtype, rows, cols, ld, axis,
+                              ctypes.byref(conv) if conv is not None else None,
+                              _ptr(dst), _ptr(linesum), _stream(stream)), "fqt_pack_bits")
+
+
+def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, xsign_sum, dW, I_out=None, stream=None):
+    _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign),
+                                   _ptr(xsign_sum), _ptr(dW), _ptr(I_out), _stream(stream)),
+           "fqt_binary_gemm_dw")
+
+
+def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, wsign_sum, dX, I_out=None, stream=None):
+    _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign),
+                                   _ptr(wsign_sum), _ptr(dX), _ptr(I_out), _stream(stream)),
+           "fqt_binary_gemm_dx")
+
+
+def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):
+    _check(_lib.fqt_layer_backward(desc, cfg, _ptr(X), _ptr(W), _ptr(dY), _ptr(dX), _ptr(dW),
+                                   _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "fqt_layer_backward")
+
+
+# ----------------------------------------------------------------------------- buffers
+
+class QGrad:
+    """Device buffers of one fqt_qgrad (allocated with torch), plus the ctypes struct."""
+
+    def __init__(self, desc, cfg, device="cuda"):
+        psq_words, pcq_words = fqt_qgrad_words(desc, cfg)
+        N, D = desc.N, desc.D
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        self.psq_planes = torch.empty(psq_words, dtype=torch.int64, device=device)
+        self.pcq_planes = torch.empty(pcq_words, dtype=torch.int64, device=device)
+        self.psq_kept, self.psq_count = torch.empty(N, **i32), torch.empty(1, **i32)
+        self.pcq_kept, self.pcq_count = torch.empty(D, **i32), torch.empty(1, **i32)
+        self.psq_scale, self.psq_offset, self.psq_prob = (torch.empty(N, **f32) for _ in range(3))
+        self.pcq_scale, self.pcq_offset, self.pcq_prob = (torch.empty(D, **f32) for _ in range(3))
+        self.struct = fqt_qgrad(*(t.data_ptr() for t in (
+            self.psq_planes, self.pcq_planes, self.psq_kept, self.psq_count, self.pcq_kept,
+            self.pcq_count, self.psq_scale, self.psq_offset, self.psq_prob, self.pcq_scale,
+            self.pcq_offset, self.pcq_prob)))
+
+
+def workspace(desc, cfg, which=FQT_WS_LAYER, device="cuda"):
+    """A 256-byte aligned uint8 workspace tensor of the size the library asks for."""
+    n = fqt_workspace_size(desc, cfg, which)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)

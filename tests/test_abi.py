@@ -1,0 +1,108 @@
+"""Host-side checks of the C ABI: the library loads, exports what include/fqt.h declares,
+and validates arguments before launching anything (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fqt.h")
+
+fqt = pytest.importorskip("paper_2408_14267_amd.fqt", reason="libfqt.so not built")
+
+from paper_2408_14267_amd.workloads import LayerShape, WORKLOADS  # noqa: E402
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|const char \*)\s*(fqt_\w+)\(", text, flags=re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) == 8
+    lib = ctypes.CDLL(fqt.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(fqt.EXPORTED) == names
+
+
+def test_status_strings():
+    for s in range(-7, 1):
+        assert fqt.fqt_status_string(s).startswith("FQT_")
+    assert "unknown" in fqt.fqt_status_string(5)
+
+
+def _desc(**kw):
+    L = WORKLOADS["vgg_cifar_conv3x3_256"].layers[0]
+    d = fqt.layer_desc(L)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("kind", 7, fqt.FQT_E_INVAL), ("dy_dtype", 3, fqt.FQT_E_DTYPE), ("N", 0, fqt.FQT_E_SHAPE),
+    ("D", -1, fqt.FQT_E_SHAPE), ("kh", 0, fqt.FQT_E_SHAPE), ("sh", 0, fqt.FQT_E_SHAPE),
+    ("ph", -1, fqt.FQT_E_SHAPE), ("kh", 11, fqt.FQT_E_SHAPE), ("N", 16385, fqt.FQT_E_SHAPE),
+    ("D", 20000, fqt.FQT_E_SHAPE)])
+def test_descriptor_validation(field, value, status):
+    with pytest.raises(fqt.FqtError) as e:
+        fqt.fqt_workspace_size(_desc(**{field: value}), fqt.quant_cfg(4))
+    assert e.value.status == status
+
+
+def test_linear_geometry_must_be_trivial():
+    d = fqt.layer_desc(LayerShape("fc", "linear", 8, 16, 4))
+    d.kh = 3
+    with pytest.raises(fqt.FqtError) as e:
+        fqt.fqt_workspace_size(d, fqt.quant_cfg(2))
+    assert e.value.status == fqt.FQT_E_SHAPE
+
+
+@pytest.mark.parametrize("bits,mode", [(0, 0), (9, 0), (2, 3), (2, -1)])
+def test_cfg_validation(bits, mode):
+    with pytest.raises(fqt.FqtError) as e:
+        fqt.fqt_workspace_size(_desc(), fqt.quant_cfg(bits, mode))
+    assert e.value.status == fqt.FQT_E_INVAL
+
+
+def test_workspace_and_plane_sizes():
+    d = _desc()
+    c = fqt.quant_cfg(4)
+    psq, pcq = fqt.fqt_qgrad_words(d, c)
+    R = 128 * 64
+    assert psq == 4 * R * 4 and pcq == 4 * 256 * (R // 64)
+    ws_layer = fqt.fqt_workspace_size(d, c, fqt.FQT_WS_LAYER)
+    ws_q = fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE)
+    assert ws_layer > (psq + pcq) * 8 > ws_q > 0
+    with pytest.raises(fqt.FqtError):
+        fqt.fqt_workspace_size(d, c, 7)
+
+
+def test_null_and_small_workspace_rejected_before_launch():
+    lib = fqt._lib
+    d = _desc()
+    c = fqt.quant_cfg(4)
+    fake = ctypes.c_void_p(1 << 20)          # never dereferenced: validation fails first
+    st = lib.fqt_layer_backward(ctypes.byref(d), ctypes.byref(c), None, fake, fake, fake, fake,
+                                fake, 1 << 30, None)
+    assert st == fqt.FQT_E_NULL
+    st = lib.fqt_layer_backward(ctypes.byref(d), ctypes.byref(c), fake, fake, fake, fake, fake,
+                                fake, 16, None)
+    assert st == fqt.FQT_E_WORKSPACE
+    mis = ctypes.c_void_p((1 << 20) + 4)
+    st = lib.fqt_layer_backward(ctypes.byref(d), ctypes.byref(c), fake, fake, mis, fake, fake,
+                                fake, 1 << 30, None)
+    assert st == fqt.FQT_E_ALIGN
+    st = lib.fqt_pack_bits(fake, 0, 10, 10, 5, fqt.FQT_PACK_ALONG_COLS, None, fake, None, None)
+    assert st == fqt.FQT_E_SHAPE
+    st = lib.fqt_pack_bits(fake, 0, 10, 10, 10, 5, None, fake, None, None)
+    assert st == fqt.FQT_E_INVAL
+    st = lib.fqt_pack_bits(fake, 0, 0, 0, 0, fqt.FQT_PACK_IM2COL, None, fake, None, None)
+    assert st == fqt.FQT_E_NULL
+    q = fqt.fqt_qgrad()
+    st = lib.fqt_binary_gemm_dw(ctypes.byref(d), ctypes.byref(c), ctypes.byref(q), fake, fake,
+                                fake, None, None)
+    assert st == fqt.FQT_E_NULL

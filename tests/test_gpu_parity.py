@@ -1,0 +1,244 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bit-exact: group selection (counts, kept-id partition), scale/offset/probability
+bits, packed PSQ/PCQ planes, packed sign bits and line sums, and the integer
+outputs of both products.  Rescaled float32 gradients: |gpu - oracle| <=
+1e-5 * (|S I| + |Z' c|) elementwise (2^-8 for bfloat16 outputs), a bound that
+stays meaningful where the two terms cancel.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import fqt as ofqt
+from paper_2408_14267_amd.workloads import WORKLOADS, LayerShape, Recipe, draw_layer
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _fqt():
+    from paper_2408_14267_amd import fqt
+    return fqt
+
+
+CASES = [
+    # name, layer, bits, mode, recipe, dtype
+    ("linear_32x256x128_b2", WORKLOADS["linear_32x256x128"].layers[0], 2, 0,
+     WORKLOADS["linear_32x256x128"].recipe, "f32"),
+    ("conv_ragged_b3", LayerShape("c", "conv2d", 5, 7, 70, 9, 9, 3, 3, 1, 1, 1, 1), 3, 0,
+     Recipe("sample_lognormal", sigma=1.5), "f32"),
+    ("conv_s2_b2", LayerShape("c", "conv2d", 6, 16, 32, 11, 11, 3, 3, 2, 2, 1, 1), 2, 0,
+     Recipe("channel_lognormal", sigma=1.5), "f32"),
+    ("conv1x1_s2_b4", LayerShape("c", "conv2d", 4, 64, 128, 8, 8, 1, 1, 2, 2, 0, 0), 4, 0,
+     Recipe("student_t", df=3.0), "f32"),
+    ("conv7x7_s2_b4", LayerShape("c", "conv2d", 4, 3, 64, 32, 32, 7, 7, 2, 2, 3, 3), 4, 0,
+     Recipe("student_t", df=3.0), "f32"),
+    ("linear_ragged_b8", LayerShape("fc", "linear", 37, 300, 77), 8, 0,
+     Recipe("sample_lognormal", sigma=2.0), "f32"),
+    ("linear_b1", LayerShape("fc", "linear", 64, 512, 128), 1, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv_p49_b4", LayerShape("c", "conv2d", 3, 5, 8, 7, 7, 3, 3, 1, 1, 1, 1), 4, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv_bf16_b2", LayerShape("c", "conv2d", 8, 32, 64, 14, 14, 3, 3, 1, 1, 1, 1), 2, 0,
+     Recipe("channel_lognormal", sigma=1.5), "bf16"),
+    ("conv_topk_b4", LayerShape("c", "conv2d", 16, 8, 24, 6, 6, 3, 3, 1, 1, 1, 1), 4, 1,
+     Recipe("sample_lognormal", sigma=2.0), "f32"),
+    ("conv_off_b2", LayerShape("c", "conv2d", 4, 8, 12, 5, 5, 3, 3, 1, 1, 1, 1), 2, 2,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv_1x1map_b4", LayerShape("c", "conv2d", 128, 16, 32, 1, 1, 3, 3, 1, 1, 1, 1), 4, 0,
+     Recipe("student_t", df=3.0), "f32"),
+    ("linear_N1_D1", LayerShape("fc", "linear", 1, 5, 1), 2, 0, Recipe(), "f32"),
+    ("linear_wideD_b4", LayerShape("fc", "linear", 8, 64, 5000), 4, 0,
+     Recipe("channel_lognormal", sigma=1.5), "f32"),
+]
+
+
+def _announce(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _to_dev(a, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def _u64(t):
+    return t.cpu().numpy().view(np.uint64)
+
+
+def _bits32(a):
+    return np.asarray(a, dtype=np.float32).view(np.uint32)
+
+
+def _assert_rescaled(got, ref, t1, t2, rel, what):
+    g = got.float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+    bound = rel * (np.abs(t1) + np.abs(t2)) + 1e-30
+    bad = np.abs(g - ref) > bound
+    assert not bad.any(), f"{what}: {int(bad.sum())} of {bad.size} outside tolerance; " \
+                          f"first at {np.argwhere(bad)[0]}"
+
+
+def _run_case(layer, bits, mode, recipe, dtype, seed=0, step=3, layer_id=5, data_seed=0):
+    fqt = _fqt()
+    x, w, dy = draw_layer(layer, recipe, data_seed, dtype)
+    ref = ofqt.layer_backward(x, w, dy, bits, mode, seed=seed, step=step, layer_id=layer_id,
+                              stride=layer.stride, pad=layer.pad)
+    dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
+    desc = fqt.layer_desc(layer, dy_dtype=dt, x_dtype=dt, w_dtype=fqt.FQT_F32, dx_dtype=dt)
+    cfg = fqt.quant_cfg(bits, mode, seed, step, layer_id)
+    X, W, dY = _to_dev(x, dtype), _to_dev(w, "f32"), _to_dev(dy, dtype)
+    return fqt, ref, desc, cfg, X, W, dY
+
+
+def _check_quantize(fqt, ref, desc, cfg, dY, layer, bits):
+    q = fqt.QGrad(desc, cfg)
+    ws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE)
+    fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, ws)
+    torch.cuda.synchronize()
+    N, D, P = layer.N, layer.D, layer.Ho * layer.Wo
+    R = N * P
+    Wd, Wr = (D + 63) // 64, (R + 63) // 64
+    for name, grp, kept, count, scale, offset, prob in (
+            ("samples", ref.qgrad.samples, q.psq_kept, q.psq_count, q.psq_scale, q.psq_offset,
+             q.psq_prob),
+            ("channels", ref.qgrad.channels, q.pcq_kept, q.pcq_count, q.pcq_scale, q.pcq_offset,
+             q.pcq_prob)):
+        assert int(count.item()) == grp.count, name
+        assert np.array_equal(kept.cpu().numpy(), grp.kept_ids), name
+        assert np.array_equal(_bits32(prob.cpu().numpy()), _bits32(grp.prob)), name + " prob"
+        assert np.array_equal(_bits32(scale.cpu().numpy()), _bits32(grp.scale)), name + " scale"
+        assert np.array_equal(_bits32(offset.cpu().numpy()), _bits32(grp.offset)), name + " offset"
+    ks, kc = ref.qgrad.samples.count, ref.qgrad.channels.count
+    psq = _u64(q.psq_planes).reshape(bits, R, Wd)[:, :ks * P]
+    pcq = _u64(q.pcq_planes).reshape(bits, D, Wr)[:, :kc]
+    assert np.array_equal(psq, ref.qgrad.psq_planes), "psq planes"
+    assert np.array_equal(pcq, ref.qgrad.pcq_planes), "pcq planes"
+    return q
+
+
+def _check_signs(fqt, ref, desc, layer, X, W, x_dt):
+    K = layer.C * layer.kh * layer.kw
+    R = layer.N * layer.Ho * layer.Wo
+    Wd, Wr = (layer.D + 63) // 64, (R + 63) // 64
+    xs = torch.empty(K * Wr, dtype=torch.int64, device="cuda")
+    xsum = torch.empty(K, dtype=torch.int32, device="cuda")
+    ws_ = torch.empty(K * Wd, dtype=torch.int64, device="cuda")
+    wsum = torch.empty(K, dtype=torch.int32, device="cuda")
+    if layer.kind == "linear":
+        fqt.fqt_pack_bits(X, x_dt, layer.N, layer.C, layer.C, fqt.FQT_PACK_ALONG_ROWS, None, xs, xsum)
+    else:
+        fqt.fqt_pack_bits(X, x_dt, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc, xs, xsum)
+    fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K, fqt.FQT_PACK_ALONG_ROWS, None, ws_, wsum)
+    torch.cuda.synchronize()
+    assert np.array_equal(_u64(xs).reshape(K, Wr), ofqt.pack_words(ref.xbits)), "x sign bits"
+    assert np.array_equal(_u64(ws_).reshape(K, Wd), ofqt.pack_words(ref.wbits)), "w sign bits"
+    assert np.array_equal(xsum.cpu().numpy(), ref.xsign_colsum), "x line sums"
+    assert np.array_equal(wsum.cpu().numpy(), ref.wsign_colsum), "w line sums"
+    return xs, xsum, ws_, wsum
+
+
+@pytest.mark.parametrize("name,layer,bits,mode,recipe,dtype", CASES, ids=[c[0] for c in CASES])
+def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
+    _announce(f"[gpu parity] {name}: {layer} b={bits} mode={mode} {dtype}")
+    fqt, ref, desc, cfg, X, W, dY = _run_case(layer, bits, mode, recipe, dtype)
+    x_dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
+    q = _check_quantize(fqt, ref, desc, cfg, dY, layer, bits)
+    xs, xsum, ws_, wsum = _check_signs(fqt, ref, desc, layer, X, W, x_dt)
+
+    D, K = layer.D, layer.C * layer.kh * layer.kw
+    dW = torch.empty(D, K, dtype=torch.float32, device="cuda")
+    I_dw = torch.empty(D, K, dtype=torch.int32, device="cuda")
+    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, xsum, dW, I_dw)
+    dX = torch.empty(X.shape, dtype=X.dtype, device="cuda")
+    I_dx = torch.empty(layer.N, layer.C, layer.H, layer.W, dtype=torch.int32, device="cuda")
+    fqt.fqt_binary_gemm_dx(desc, cfg, q, ws_, wsum, dX, I_dx)
+    torch.cuda.synchronize()
+    assert np.array_equal(I_dw.cpu().numpy(), ref.I_dw), "dW integer product"
+    assert np.array_equal(I_dx.cpu().numpy(), ref.I_dx), "dX integer product"
+    _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
+    _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 2.0 ** -8 if dtype == "bf16" else 1e-5, "dX")
+
+    # The whole-layer entry point gives the same bits as the component calls.
+    dX2 = torch.empty_like(dX)
+    dW2 = torch.empty_like(dW)
+    fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX2, dW2, fqt.workspace(desc, cfg))
+    torch.cuda.synchronize()
+    assert torch.equal(dX2.view(torch.int16 if dtype == "bf16" else torch.int32),
+                       dX.view(torch.int16 if dtype == "bf16" else torch.int32))
+    assert torch.equal(dW2.view(torch.int32), dW.view(torch.int32))
+
+
+def test_full_vgg_cifar_conv_layer():
+    """The benchmarked workload (VGG-16 CIFAR 3x3 conv 256->256 on 8x8, N=128, b=4) in the
+    launch configuration the benchmark times, compared in full."""
+    wl = WORKLOADS["vgg_cifar_conv3x3_256"]
+    layer = wl.layers[0]
+    _announce(f"[gpu parity] full {wl.name}")
+    fqt, ref, desc, cfg, X, W, dY = _run_case(layer, wl.bits, wl.agp_mode, wl.recipe, wl.dtype,
+                                             seed=wl.philox_seed, step=0, layer_id=0,
+                                             data_seed=wl.seed)
+    _check_quantize(fqt, ref, desc, cfg, dY, layer, wl.bits)
+    dX = torch.empty_like(X)
+    dW = torch.empty_like(W)
+    ws = fqt.workspace(desc, cfg)
+    for _ in range(2):      # a repeated call on a reused workspace gives the same result
+        fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws)
+        torch.cuda.synchronize()
+        _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
+        _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
+    assert 0 < ref.qgrad.samples.count < layer.N and 0 < ref.qgrad.channels.count < layer.D
+
+
+def test_all_zero_gradient():
+    fqt = _fqt()
+    layer = LayerShape("c", "conv2d", 4, 8, 16, 6, 6, 3, 3, 1, 1, 1, 1)
+    _announce("[gpu parity] all-zero dY")
+    x, w, _ = draw_layer(layer, Recipe(), 0)
+    desc = fqt.layer_desc(layer)
+    cfg = fqt.quant_cfg(4)
+    X, W = _to_dev(x, "f32"), _to_dev(w, "f32")
+    dY = torch.zeros(layer.dy_shape, device="cuda")
+    dX = torch.full_like(X, 7.0)
+    dW = torch.full_like(W, 7.0)
+    fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, fqt.workspace(desc, cfg))
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dX).item() == 0 and torch.count_nonzero(dW).item() == 0
+
+
+def test_constant_gradient_exact_with_agp_off():
+    fqt = _fqt()
+    layer = LayerShape("fc", "linear", 16, 40, 24)
+    _announce("[gpu parity] constant dY, AGP off")
+    x, w, _ = draw_layer(layer, Recipe(), 0)
+    dy = np.full(layer.dy_shape, 0.75, np.float32)
+    desc = fqt.layer_desc(layer)
+    cfg = fqt.quant_cfg(2, fqt.FQT_AGP_OFF)
+    X, W, dY = (_to_dev(a, "f32") for a in (x, w, dy))
+    dX, dW = torch.empty_like(X), torch.empty_like(W)
+    fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, fqt.workspace(desc, cfg))
+    torch.cuda.synchronize()
+    sx, sw = np.where(x > 0, 1.0, -1.0), np.where(w > 0, 1.0, -1.0)
+    np.testing.assert_allclose(dW.cpu().numpy(), dy.T.astype(np.float64) @ sx, rtol=1e-6)
+    np.testing.assert_allclose(dX.cpu().numpy(), dy.astype(np.float64) @ sw, rtol=1e-6)
+
+
+def test_seed_step_layer_change_the_draws():
+    fqt = _fqt()
+    layer = LayerShape("fc", "linear", 32, 64, 48)
+    _announce("[gpu parity] seeds")
+    x, w, dy = draw_layer(layer, Recipe("sample_lognormal", sigma=1.0), 0)
+    desc = fqt.layer_desc(layer)
+    outs = []
+    for seed, step, lid in ((0, 0, 0), (1, 0, 0), (0, 1, 0), (0, 0, 1)):
+        cfg = fqt.quant_cfg(2, 0, seed, step, lid)
+        X, W, dY = (_to_dev(a, "f32") for a in (x, w, dy))
+        dX, dW = torch.empty_like(X), torch.empty_like(W)
+        fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, fqt.workspace(desc, cfg))
+        torch.cuda.synchronize()
+        ref = ofqt.layer_backward(x, w, dy, 2, 0, seed=seed, step=step, layer_id=lid)
+        _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
+        outs.append(dX.cpu())
+    assert all(not torch.equal(outs[0], o) for o in outs[1:])
