@@ -139,8 +139,8 @@ def main():
     fqt.fqt_pack_bits(X, fqt.FQT_F32, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc, xs, xsum, stream)
     fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K, fqt.FQT_PACK_ALONG_ROWS, None, wsg, wsum, stream)
     kernels = {
-        "gemm_dw": lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, xsum, dW, None, stream),
-        "gemm_dx": lambda: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsg, wsum, dX, None, stream),
+        "gemm_dw": lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, None, stream),
+        "gemm_dx": lambda: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsg, dX, None, stream),
     }
     per = {}
     for name, fn in kernels.items():

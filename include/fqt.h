@@ -25,8 +25,9 @@
  *  - Arguments are validated on the host before anything is launched; a
  *    failing validation returns a negative fqt_status and launches nothing.
  *    A failed launch returns FQT_E_HIP.  No C++ exception crosses the ABI.
- *  - Alignment: float/bf16 tensors 16 bytes, uint64 bit arrays 8 bytes, int32
- *    and float32 arrays 4 bytes, workspaces 256 bytes (FQT_E_ALIGN otherwise).
+ *  - Alignment: dY 16 bytes, other float/bf16 tensors their element size, uint64 bit
+ *    arrays 8 bytes, byte-code arrays 16 bytes, int32 and float32 arrays 4 bytes,
+ *    workspaces 256 bytes (FQT_E_ALIGN otherwise).
  *  - Bit packing: bit j of a packed line is bit (j % 64) of 64-bit word j / 64,
  *    least significant bit first; ragged tails are zero.  A set bit is +1, a
  *    clear bit -1 (sign(x) = -1 for x <= 0, Section 5.1), or a code bit.
@@ -72,7 +73,7 @@ typedef enum {
 /* Layer geometry (Section 3, Eq. 1-3; Appendix C Unfolder: X_u is NHW x CK^2).
  * Ho = (H + 2 ph - kh) / sh + 1 and Wo likewise must be >= 1.
  * dy_dtype, x_dtype, dx_dtype: FQT_F32 or FQT_BF16; w_dtype: FQT_F32 or FQT_BF16.
- * N*Ho*Wo, N*C*H*W and N*D*Ho*Wo must stay below 2^31. */
+ * N*Ho*Wo, N*C*H*W, N*D*Ho*Wo and D*C*kh*kw must stay below 2^31. */
 typedef struct {
   int32_t kind;                       /* fqt_layer_kind                                  */
   int32_t dy_dtype, x_dtype, w_dtype, dx_dtype;
@@ -102,6 +103,9 @@ typedef struct {
  *                                   Rows >= count*P are left untouched.
  *   pcq_planes  uint64 [b][D][Wr]   PCQ code planes; row j holds the j-th kept channel,
  *                                   packed along (n, ho, wo).  Rows >= count untouched.
+ *   psq_codes   uint8 [R][Wd*64]    the same PSQ codes one byte each (the operand of the
+ *                                   int8 products), rows as in psq_planes, bytes past D = 0
+ *   pcq_codes   uint8 [D][Wr*64]    the PCQ codes one byte each, bytes past R = 0
  *   psq_kept    int32 [N]           kept sample ids ascending, then pruned ids ascending
  *   psq_count   int32 [1]           number of kept samples
  *   psq_scale   float [N]           S_n = R_n / (B p_n) if kept, else 0
@@ -111,14 +115,18 @@ typedef struct {
 typedef struct {
   uint64_t *psq_planes;
   uint64_t *pcq_planes;
+  uint8_t *psq_codes;                 /* 16-byte aligned */
+  uint8_t *pcq_codes;                 /* 16-byte aligned */
   int32_t *psq_kept, *psq_count, *pcq_kept, *pcq_count;
   float *psq_scale, *psq_offset, *psq_prob;
   float *pcq_scale, *pcq_offset, *pcq_prob;
 } fqt_qgrad;
 
-/* Element counts of the two plane arrays of fqt_qgrad (host call, no device work). */
+/* Element counts of the plane arrays (uint64 words) and the code arrays (bytes) of
+ * fqt_qgrad (host call, no device work). */
 int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
-                    int64_t *psq_words, int64_t *pcq_words);
+                    int64_t *psq_words, int64_t *pcq_words, int64_t *psq_code_bytes,
+                    int64_t *pcq_code_bytes);
 
 /* Workspace sizes (host call).  which = FQT_WS_QUANTIZE for fqt_agp_scq_quantize,
  * FQT_WS_LAYER for fqt_layer_backward (which holds an fqt_qgrad and the packed signs
@@ -136,7 +144,8 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
  * rounding code q = floor(v) + [u24 < frac(v) 2^24], v = clamp((x - Z) * (B / R), 0, B)
  * in float32, B = 2^b - 1, one Philox word per element shared by its PSQ and PCQ code;
  * codes split into b bit planes and packed (row encoder along D for PSQ, column encoder
- * along N*Ho*Wo for PCQ).  dY has desc->dy_dtype.  Writes every member of *out.
+ * along N*Ho*Wo for PCQ), and the same codes as bytes.  dY has desc->dy_dtype.  Writes
+ * every member of *out.
  * ws: >= fqt_workspace_size(FQT_WS_QUANTIZE) bytes. */
 int fqt_agp_scq_quantize(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *dY,
                          const fqt_qgrad *out, void *ws, size_t ws_bytes, void *hip_stream);
@@ -163,15 +172,16 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
 
 /* Weight-gradient product with PCQ codes (Section 5.3, SCQ; Appendix C Alg. 1 binary
  * product and dequantization; {0,1} <-> {+-1} conversion):
- *   I[d][k]  = sum_r q_pcq[d][r] * s_X[r][k]   (k over C*kh*kw, r over N*Ho*Wo), computed
- *              as sum_p 2^p (2 popcount(a_p & t) - popcount(a_p)) over packed words;
- *   dW[d][k] = S_d * I[d][k] + Z'_d * c_X[k] in float32 for kept channels, 0 for pruned.
+ *   I[d][k]  = sum_r q_pcq[d][r] * s_X[r][k]   (k over C*kh*kw, r over N*Ho*Wo);
+ *   dW[d][k] = S_d * I[d][k] + Z'_d * c_X[k] in float32 for kept channels, 0 for pruned,
+ *   with c_X[k] = sum_r s_X[r][k] (the zero-point term).
+ * Computed on int8 MFMA from q->pcq_codes and the packed signs (unpacked in registers).
  * xsign: uint64 [C*kh*kw][ceil(N*Ho*Wo/64)] (fqt_pack_bits IM2COL, or ALONG_ROWS of X for
- * a linear layer); xsign_sum: int32 [C*kh*kw], c_X = its line sums.  dW: float [D][C*kh*kw].
- * I_out (optional): int32 [D][C*kh*kw] receives I (0 in pruned rows). */
+ * a linear layer).  dW: float [D][C*kh*kw].  I_out (optional): int32 [D][C*kh*kw] receives
+ * I (0 in pruned rows). */
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
-                       const fqt_qgrad *q, const uint64_t *xsign, const int32_t *xsign_sum,
-                       float *dW, int32_t *I_out, void *hip_stream);
+                       const fqt_qgrad *q, const uint64_t *xsign, float *dW, int32_t *I_out,
+                       void *hip_stream);
 
 /* Activation-gradient product with PSQ codes (Section 5.3, SCQ; Appendix C Alg. 1, and
  * the Folder for convolutions):
@@ -180,13 +190,13 @@ int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
  *   c[c][h][w]    = sum over the same taps of sum_d s_W[d][c][i][j];
  *   dX            = S_n * I + Z'_n * c in float32 (rounded to bf16 if dx_dtype is bf16)
  *                   for kept samples, 0 for pruned samples.
- * This is the unfolded product followed by the folder, taken in integers.  wsign: uint64
- * [C*kh*kw][ceil(D/64)] (fqt_pack_bits ALONG_ROWS of W viewed as [D][C*kh*kw]);
- * wsign_sum: int32 [C*kh*kw].  dX: [N][C][H][W] of dx_dtype.  I_out (optional): int32
- * [N][C][H][W]. */
+ * This is the unfolded product followed by the folder, taken in integers, on int8 MFMA
+ * from q->psq_codes.  wsign: uint64 [C*kh*kw][ceil(D/64)] (fqt_pack_bits ALONG_ROWS of W
+ * viewed as [D][C*kh*kw]).  kh*kw <= 64.  dX: [N][C][H][W] of dx_dtype.  I_out (optional):
+ * int32 [N][C][H][W]. */
 int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
-                       const fqt_qgrad *q, const uint64_t *wsign, const int32_t *wsign_sum,
-                       void *dX, int32_t *I_out, void *hip_stream);
+                       const fqt_qgrad *q, const uint64_t *wsign, void *dX, int32_t *I_out,
+                       void *hip_stream);
 
 /* Whole layer backward (Appendix C Alg. 1 backward; Section 5.3's final form):
  * quantize dY, pack sign(X) (im2col for conv) and sign(W), then both products.

@@ -26,20 +26,25 @@ struct LayerWs {
   QuantWs qws;
   fqt_qgrad q;
   uint64_t *xsign, *wsign;
-  int32_t *xsum, *wsum;
 };
+
+void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
+  q->part_c = c->take<int2>(size_t(L.D) * L.Wr);
+  q->part_s = c->take<int2>(size_t(L.Wd) * L.R);
+  q->skey = c->take<int2>(L.N);
+  q->ckey = c->take<int2>(L.D);
+  q->sp = c->take<GroupParam>(L.N);
+  q->cp = c->take<GroupParam>(L.D);
+}
 
 size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
   Carver c{static_cast<char *>(ws)};
   LayerWs w{};
-  w.qws.smin = c.take<int32_t>(L.N);
-  w.qws.smax = c.take<int32_t>(L.N);
-  w.qws.cmin = c.take<int32_t>(L.D);
-  w.qws.cmax = c.take<int32_t>(L.D);
-  w.qws.sp = c.take<GroupParam>(L.N);
-  w.qws.cp = c.take<GroupParam>(L.D);
+  carve_quant_ws(&c, L, &w.qws);
   w.q.psq_planes = c.take<uint64_t>(size_t(bits) * L.R * L.Wd);
   w.q.pcq_planes = c.take<uint64_t>(size_t(bits) * L.D * L.Wr);
+  w.q.psq_codes = c.take<uint8_t>(size_t(L.R) * L.Wd * 64);
+  w.q.pcq_codes = c.take<uint8_t>(size_t(L.D) * L.Wr * 64);
   w.q.psq_kept = c.take<int32_t>(L.N);
   w.q.psq_count = c.take<int32_t>(1);
   w.q.pcq_kept = c.take<int32_t>(L.D);
@@ -51,9 +56,7 @@ size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
   w.q.pcq_offset = c.take<float>(L.D);
   w.q.pcq_prob = c.take<float>(L.D);
   w.xsign = c.take<uint64_t>(size_t(L.K) * L.Wr);
-  w.xsum = c.take<int32_t>(L.K);
   w.wsign = c.take<uint64_t>(size_t(L.K) * L.Wd);
-  w.wsum = c.take<int32_t>(L.K);
   if (out) *out = w;
   return c.off;
 }
@@ -61,18 +64,20 @@ size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
 int check_qgrad(const fqt_qgrad *q, bool psq, bool pcq) {
   if (!q) return FQT_E_NULL;
   if (psq) {
-    if (!q->psq_planes || !q->psq_kept || !q->psq_count || !q->psq_scale || !q->psq_offset ||
-        !q->psq_prob)
+    if (!q->psq_planes || !q->psq_codes || !q->psq_kept || !q->psq_count || !q->psq_scale ||
+        !q->psq_offset || !q->psq_prob)
       return FQT_E_NULL;
-    if (!aligned(q->psq_planes, 8) || !aligned(q->psq_kept, 4) || !aligned(q->psq_count, 4) ||
+    if (!aligned(q->psq_planes, 8) || !aligned(q->psq_codes, 16) || !aligned(q->psq_kept, 4) ||
+        !aligned(q->psq_count, 4) ||
         !aligned(q->psq_scale, 4) || !aligned(q->psq_offset, 4) || !aligned(q->psq_prob, 4))
       return FQT_E_ALIGN;
   }
   if (pcq) {
-    if (!q->pcq_planes || !q->pcq_kept || !q->pcq_count || !q->pcq_scale || !q->pcq_offset ||
-        !q->pcq_prob)
+    if (!q->pcq_planes || !q->pcq_codes || !q->pcq_kept || !q->pcq_count || !q->pcq_scale ||
+        !q->pcq_offset || !q->pcq_prob)
       return FQT_E_NULL;
-    if (!aligned(q->pcq_planes, 8) || !aligned(q->pcq_kept, 4) || !aligned(q->pcq_count, 4) ||
+    if (!aligned(q->pcq_planes, 8) || !aligned(q->pcq_codes, 16) || !aligned(q->pcq_kept, 4) ||
+        !aligned(q->pcq_count, 4) ||
         !aligned(q->pcq_scale, 4) || !aligned(q->pcq_offset, 4) || !aligned(q->pcq_prob, 4))
       return FQT_E_ALIGN;
   }
@@ -116,6 +121,7 @@ int make_layer(const fqt_layer_desc *d, Layer *L) {
   if (l.P > LIMIT31 || l.HW > LIMIT31 || l.K > LIMIT31) return FQT_E_SHAPE;
   l.R = l.N * l.P;
   if (l.R > LIMIT31 || l.N * l.C > LIMIT31 / l.HW || l.N * l.D > LIMIT31 / l.P) return FQT_E_SHAPE;
+  if (l.D * l.K > LIMIT31) return FQT_E_SHAPE;
   l.Wd = (l.D + 63) / 64;
   l.Wr = (l.R + 63) / 64;
   *L = l;
@@ -132,18 +138,15 @@ int check_cfg(const fqt_quant_cfg *c, const Layer &) {
 }
 
 size_t quant_ws_bytes(const Layer &L) {
-  return 2 * align256(size_t(L.N) * 4) + 2 * align256(size_t(L.D) * 4) +
-         align256(size_t(L.N) * sizeof(GroupParam)) + align256(size_t(L.D) * sizeof(GroupParam));
+  Carver c{nullptr};
+  QuantWs q;
+  carve_quant_ws(&c, L, &q);
+  return c.off;
 }
 
 void carve_quant_ws(void *ws, const Layer &L, QuantWs *q) {
   Carver c{static_cast<char *>(ws)};
-  q->smin = c.take<int32_t>(L.N);
-  q->smax = c.take<int32_t>(L.N);
-  q->cmin = c.take<int32_t>(L.D);
-  q->cmax = c.take<int32_t>(L.D);
-  q->sp = c.take<GroupParam>(L.N);
-  q->cp = c.take<GroupParam>(L.D);
+  carve_quant_ws(&c, L, q);
 }
 
 }  // namespace fqt
@@ -167,13 +170,15 @@ const char *fqt_status_string(int status) {
 }
 
 int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int64_t *psq_words,
-                    int64_t *pcq_words) {
+                    int64_t *pcq_words, int64_t *psq_code_bytes, int64_t *pcq_code_bytes) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
-  if (!psq_words || !pcq_words) return FQT_E_NULL;
+  if (!psq_words || !pcq_words || !psq_code_bytes || !pcq_code_bytes) return FQT_E_NULL;
   *psq_words = int64_t(cfg->bits) * L.R * L.Wd;
   *pcq_words = int64_t(cfg->bits) * L.D * L.Wr;
+  *psq_code_bytes = L.R * L.Wd * 64;
+  *pcq_code_bytes = L.D * L.Wr * 64;
   return FQT_OK;
 }
 
@@ -229,33 +234,27 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
 }
 
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
-                       const uint64_t *xsign, const int32_t *xsign_sum, float *dW, int32_t *I_out,
-                       void *hip_stream) {
+                       const uint64_t *xsign, float *dW, int32_t *I_out, void *hip_stream) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
   FQT_TRY(check_qgrad(q, false, true));
-  if (!xsign || !xsign_sum || !dW) return FQT_E_NULL;
-  if (!aligned(xsign, 8) || !aligned(xsign_sum, 4) || !aligned(dW, 4) ||
-      (I_out && !aligned(I_out, 4)))
-    return FQT_E_ALIGN;
-  return launch_gemm_dw(L, *cfg, *q, xsign, xsign_sum, dW, I_out,
-                        static_cast<hipStream_t>(hip_stream));
+  if (!xsign || !dW) return FQT_E_NULL;
+  if (!aligned(xsign, 8) || !aligned(dW, 4) || (I_out && !aligned(I_out, 4))) return FQT_E_ALIGN;
+  return launch_gemm_dw(L, *cfg, *q, xsign, dW, I_out, static_cast<hipStream_t>(hip_stream));
 }
 
 int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
-                       const uint64_t *wsign, const int32_t *wsign_sum, void *dX, int32_t *I_out,
-                       void *hip_stream) {
+                       const uint64_t *wsign, void *dX, int32_t *I_out, void *hip_stream) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
   FQT_TRY(check_qgrad(q, true, false));
-  if (!wsign || !wsign_sum || !dX) return FQT_E_NULL;
-  if (!aligned(wsign, 8) || !aligned(wsign_sum, 4) || !aligned(dX, dtype_size(L.dx_t)) ||
-      (I_out && !aligned(I_out, 4)))
+  if (!wsign || !dX) return FQT_E_NULL;
+  if (!aligned(wsign, 8) || !aligned(dX, dtype_size(L.dx_t)) || (I_out && !aligned(I_out, 4)))
     return FQT_E_ALIGN;
-  return launch_gemm_dx(L, *cfg, *q, wsign, wsign_sum, dX, I_out,
-                        static_cast<hipStream_t>(hip_stream));
+  if (L.kh * L.kw > 64) return FQT_E_SHAPE;
+  return launch_gemm_dx(L, *cfg, *q, wsign, dX, I_out, static_cast<hipStream_t>(hip_stream));
 }
 
 int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
@@ -272,16 +271,17 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   LayerWs w;
   carve_layer_ws(ws, L, cfg->bits, &w);
   const hipStream_t s = static_cast<hipStream_t>(hip_stream);
-  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
+  if (L.kh * L.kw > 64) return FQT_E_SHAPE;
   if (L.kind == FQT_LINEAR)
     FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,
-                             w.xsum, s));
+                             nullptr, s));
   else
-    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, w.xsum, s));
-  FQT_TRY(launch_pack_bits(W, L.w_t, L.D, L.K, L.K, FQT_PACK_ALONG_ROWS, nullptr, w.wsign, w.wsum,
-                           s));
-  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, w.xsum, dW, nullptr, s));
-  return launch_gemm_dx(L, *cfg, w.q, w.wsign, w.wsum, dX, nullptr, s);
+    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s));
+  FQT_TRY(launch_pack_bits(W, L.w_t, L.D, L.K, L.K, FQT_PACK_ALONG_ROWS, nullptr, w.wsign,
+                           nullptr, s));
+  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
+  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, dW, nullptr, s));
+  return launch_gemm_dx(L, *cfg, w.q, w.wsign, dX, nullptr, s);
 }
 
 }  // extern "C"

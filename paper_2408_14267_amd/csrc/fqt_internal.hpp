@@ -34,13 +34,38 @@ struct GroupParam {
   int32_t pad;
 };
 
-// Quantize workspace: ordered-int min/max keys of both group sets, and their params.
+// Quantize workspace: per-tile partial min/max keys, the reduced keys of both group
+// sets, and the per-group parameters of the quantizer.
 struct QuantWs {
-  int32_t *smin, *smax;    // [N]
-  int32_t *cmin, *cmax;    // [D]
+  int2 *part_c;            // [D][ceil(R/64)]   channel partials of each 64-row tile
+  int2 *part_s;            // [ceil(D/64)][R]   row partials of each 64-channel tile
+  int2 *skey;              // [N] (min, max) ordered-int keys of each sample
+  int2 *ckey;              // [D] (min, max) keys of each output channel
   GroupParam *sp;          // [N]
   GroupParam *cp;          // [D]
 };
+
+// Division by a fixed divisor for numerators below 2^31:
+// q = (n * m) >> s with l = ceil(log2 d), m = ceil(2^(32+l) / d), s = 32 + l.
+// The rounding error of m is below d, so n * (m*d - 2^s) / (d 2^s) < 1/(2d) never
+// carries the quotient past the next integer.
+struct FastDiv {
+  uint64_t m;
+  uint32_t s;
+  uint32_t d;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((uint64_t(1) << l) < d) ++l;
+  FastDiv f;
+  f.m = ((uint64_t(1) << (32 + l)) + d - 1) / d;
+  f.s = 32 + l;
+  f.d = d;
+  return f;
+}
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
+  return static_cast<uint32_t>((uint64_t(n) * f.m) >> f.s);
+}
 
 int make_layer(const fqt_layer_desc *d, Layer *L);
 int check_cfg(const fqt_quant_cfg *c, const Layer &L);
@@ -55,11 +80,9 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                      const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s);
 int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *xsign, const int32_t *xsum, float *dW, int32_t *I_out,
-                   hipStream_t s);
+                   const uint64_t *xsign, float *dW, int32_t *I_out, hipStream_t s);
 int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *wsign, const int32_t *wsum, void *dX, int32_t *I_out,
-                   hipStream_t s);
+                   const uint64_t *wsign, void *dX, int32_t *I_out, hipStream_t s);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }
@@ -126,15 +149,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
-// Load one element of a float32 or bfloat16 tensor as float32.
-__device__ __forceinline__ float load_elem(const void *p, int dtype, int64_t i) {
-  return dtype == FQT_BF16 ? bf16_to_f32(static_cast<const uint16_t *>(p)[i])
-                           : static_cast<const float *>(p)[i];
+// Load one element of a float32 (DT = FQT_F32) or bfloat16 (FQT_BF16) tensor as float32.
+// The dtype is a template parameter so that a load carries no branch and a run of
+// loads issues back to back before the first use.
+template <int DT>
+__device__ __forceinline__ float load_elem(const void *p, int64_t i) {
+  if (DT == FQT_BF16) return bf16_to_f32(static_cast<const uint16_t *>(p)[i]);
+  return static_cast<const float *>(p)[i];
 }
 
 // Load four consecutive elements starting at i (i % 4 == 0, base 16-byte aligned).
-__device__ __forceinline__ void load_quad(const void *p, int dtype, int64_t i, float out[4]) {
-  if (dtype == FQT_BF16) {
+template <int DT>
+__device__ __forceinline__ void load_quad(const void *p, int64_t i, float out[4]) {
+  if (DT == FQT_BF16) {
     const uint2 v = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(p) + i);
     out[0] = __uint_as_float(v.x << 16);
     out[1] = __uint_as_float(v.x & 0xFFFF0000u);
@@ -147,6 +174,13 @@ __device__ __forceinline__ void load_quad(const void *p, int dtype, int64_t i, f
     out[2] = v.z;
     out[3] = v.w;
   }
+}
+
+// Calls F.template operator()<DT>() with DT the compile-time dtype code of `dt`.
+template <typename F>
+__host__ void dispatch_dtype(int dt, F &&f) {
+  if (dt == FQT_BF16) f.template operator()<FQT_BF16>();
+  else f.template operator()<FQT_F32>();
 }
 
 __device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }

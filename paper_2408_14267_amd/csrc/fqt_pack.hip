@@ -10,8 +10,9 @@ constexpr int THREADS = 256;
 constexpr int WAVES = THREADS / 64;
 
 // Along the columns of a row-major [rows][cols] matrix: word w of row i.
+template <int DT>
 __global__ __launch_bounds__(THREADS) void k_pack_along_cols(const void *__restrict__ src,
-                                                             int dtype, int64_t rows,
+                                                             int64_t rows,
                                                              int64_t cols, int64_t ld,
                                                              uint64_t *__restrict__ dst) {
   const int lane = threadIdx.x & 63;
@@ -20,24 +21,32 @@ __global__ __launch_bounds__(THREADS) void k_pack_along_cols(const void *__restr
   if (item >= rows * nw) return;
   const int64_t i = item / nw, w = item - i * nw;
   const int64_t j = (w << 6) + lane;
-  const bool bit = j < cols && load_elem(src, dtype, i * ld + j) > 0.0f;
+  const float v = j < cols ? load_elem<DT>(src, i * ld + j) : 0.0f;
+  const bool bit = v > 0.0f;
   const uint64_t m = __ballot(bit);
   if (lane == 0) dst[i * nw + w] = m;
 }
 
 // Down the rows (transposing): 64x64 tile staged in LDS, read back column-wise.
+template <int DT>
 __global__ __launch_bounds__(THREADS) void k_pack_along_rows(const void *__restrict__ src,
-                                                             int dtype, int64_t rows,
+                                                             int64_t rows,
                                                              int64_t cols, int64_t ld,
                                                              uint64_t *__restrict__ dst) {
   __shared__ uint8_t bits[64][64 + 4];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int64_t c0 = int64_t(blockIdx.x) * 64, r0 = int64_t(blockIdx.y) * 64;
   const int64_t nw = (rows + 63) >> 6;
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {   // unconditional loads (element 0 outside) issue back to back
+    const int64_t r = r0 + wave + 4 * i, c = c0 + lane;
+    v[i] = load_elem<DT>(src, (r < rows && c < cols) ? r * ld + c : 0);
+  }
+#pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int rr = wave + 4 * i;
-    const int64_t r = r0 + rr, c = c0 + lane;
-    bits[rr][lane] = (r < rows && c < cols && load_elem(src, dtype, r * ld + c) > 0.0f) ? 1 : 0;
+    const int64_t r = r0 + wave + 4 * i, c = c0 + lane;
+    bits[wave + 4 * i][lane] = (r < rows && c < cols && v[i] > 0.0f) ? 1 : 0;
   }
   __syncthreads();
   for (int i = 0; i < 16; ++i) {
@@ -50,33 +59,85 @@ __global__ __launch_bounds__(THREADS) void k_pack_along_rows(const void *__restr
 }
 
 struct Im2colGeom {
-  int64_t N, C, H, W, Ho, Wo, P, R, K, nw;
+  uint32_t C, H, W, Wo, P, R, nw, cgroups;
   int kh, kw, sh, sw, ph, pw;
+  FastDiv divP, divWo, divNw;
 };
 
+constexpr int IM2COL_CPW = 4;   // channels per wave sharing one index decomposition
+
 // Bit-im2col: line (c, i, j), bit (n, ho, wo) = X[n][c][ho*sh - ph + i][wo*sw - pw + j] > 0;
-// positions in the zero padding give bit 0 (sign -1).
-__global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict__ x, int dtype,
-                                                         Im2colGeom g,
+// positions in the zero padding give bit 0 (sign -1).  One wave owns 64 consecutive
+// (n, ho, wo) of IM2COL_CPW channels: one index decomposition per lane serves every
+// channel and kernel tap.  The words of a channel's taps are gathered into lanes
+// 0..taps-1 and stored by one instruction.  KH, KW > 0 fix the kernel size at compile
+// time (fully unrolled); 0 reads it from the geometry.
+template <int DT, int KH, int KW>
+__global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict__ x, Im2colGeom g,
                                                          uint64_t *__restrict__ dst) {
   const int lane = threadIdx.x & 63;
-  const int64_t item = int64_t(blockIdx.x) * WAVES + (threadIdx.x >> 6);
-  if (item >= g.K * g.nw) return;
-  const int64_t line = item / g.nw, w = item - line * g.nw;
-  const int64_t c = line / (g.kh * g.kw);
-  const int tap = int(line - c * g.kh * g.kw);
-  const int i = tap / g.kw, j = tap - (tap / g.kw) * g.kw;
-  const int64_t r = (w << 6) + lane;
-  bool bit = false;
-  if (r < g.R) {
-    const int64_t n = r / g.P, pix = r - n * g.P;
-    const int64_t ho = pix / g.Wo, wo = pix - ho * g.Wo;
-    const int64_t h = ho * g.sh - g.ph + i, ww = wo * g.sw - g.pw + j;
-    if (h >= 0 && h < g.H && ww >= 0 && ww < g.W)
-      bit = load_elem(x, dtype, ((n * g.C + c) * g.H + h) * g.W + ww) > 0.0f;
+  const uint32_t item = blockIdx.x * WAVES + (threadIdx.x >> 6);
+  if (item >= g.cgroups * g.nw) return;
+  const uint32_t cg = fdiv(item, g.divNw), w = item - cg * g.nw;
+  const uint32_t r0 = (w << 6) + lane;
+  const bool valid = r0 < g.R;
+  const uint32_t r = valid ? r0 : 0;
+  const uint32_t n = fdiv(r, g.divP), pix = r - n * g.P;
+  const uint32_t ho = fdiv(pix, g.divWo), wo = pix - ho * g.Wo;
+  const int h0 = int(ho) * g.sh - g.ph, w0 = int(wo) * g.sw - g.pw;
+  const int kh = KH > 0 ? KH : g.kh, kw = KW > 0 ? KW : g.kw;
+  const int taps = kh * kw;
+  uint32_t hok = 0, wok = 0;
+  for (int i = 0; i < kh; ++i) hok |= uint32_t(valid && h0 + i >= 0 && h0 + i < int(g.H)) << i;
+  for (int j = 0; j < kw; ++j) wok |= uint32_t(w0 + j >= 0 && w0 + j < int(g.W)) << j;
+  const int plane = int(g.H * g.W);
+  int base = (int(n * g.C + cg * IM2COL_CPW) * int(g.H) + h0) * int(g.W) + w0;
+  for (int cc = 0; cc < IM2COL_CPW; ++cc, base += plane) {
+    const uint32_t c = cg * IM2COL_CPW + cc;
+    if (c >= g.C) break;
+    uint64_t mine = 0;
+    if constexpr (KH > 0) {
+      float v[KH * KW];
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int j = 0; j < KW; ++j) {
+          const bool ok = (hok >> i) & (wok >> j) & 1u;
+          v[i * KW + j] = load_elem<DT>(x, ok ? base + i * int(g.W) + j : 0);
+        }
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int j = 0; j < KW; ++j) {
+          const bool ok = (hok >> i) & (wok >> j) & 1u;
+          const uint64_t m = __ballot(ok && v[i * KW + j] > 0.0f);
+          if (lane == i * KW + j) mine = m;
+        }
+      if (lane < KH * KW) dst[(size_t(c) * (KH * KW) + lane) * g.nw + w] = mine;
+    } else {
+      for (int t0 = 0; t0 < taps; t0 += 16) {
+        int ti = t0 / kw, tj = t0 - ti * kw;
+        float v[16];
+        uint32_t okm = 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const bool ok = t0 + u < taps && ((hok >> ti) & (wok >> tj) & 1u);
+          okm |= uint32_t(ok) << u;
+          v[u] = load_elem<DT>(x, ok ? base + ti * int(g.W) + tj : 0);
+          if (++tj == kw) {
+            tj = 0;
+            ++ti;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const uint64_t m = __ballot(((okm >> u) & 1u) && v[u] > 0.0f);
+          if (lane == u) mine = m;
+        }
+        if (lane < 16 && t0 + lane < taps) dst[(size_t(c) * taps + t0 + lane) * g.nw + w] = mine;
+      }
+    }
   }
-  const uint64_t m = __ballot(bit);
-  if (lane == 0) dst[line * g.nw + w] = m;
 }
 
 // linesum[l] = sum of the +-1 signs of line l = 2 * popcount - len.
@@ -103,23 +164,39 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     nw = (cols + 63) / 64;
     lines = rows;
     len = cols;
-    hipLaunchKernelGGL(k_pack_along_cols, dim3(blocks_for(rows * nw)), dim3(THREADS), 0, s, src,
-                       dtype, rows, cols, ld, dst);
+    dispatch_dtype(dtype, [&]<int DT>() {
+      hipLaunchKernelGGL(k_pack_along_cols<DT>, dim3(blocks_for(rows * nw)), dim3(THREADS), 0, s,
+                         src, rows, cols, ld, dst);
+    });
   } else if (axis == FQT_PACK_ALONG_ROWS) {
     nw = (rows + 63) / 64;
     lines = cols;
     len = rows;
-    hipLaunchKernelGGL(k_pack_along_rows, dim3(unsigned((cols + 63) / 64), unsigned(nw)),
-                       dim3(THREADS), 0, s, src, dtype, rows, cols, ld, dst);
+    dispatch_dtype(dtype, [&]<int DT>() {
+      hipLaunchKernelGGL(k_pack_along_rows<DT>, dim3(unsigned((cols + 63) / 64), unsigned(nw)),
+                         dim3(THREADS), 0, s, src, rows, cols, ld, dst);
+    });
   } else {
     const Layer &L = *conv;
-    Im2colGeom g{L.N, L.C, L.H, L.W, L.Ho, L.Wo, L.P, L.R, L.K, L.Wr,
-                 L.kh, L.kw, L.sh, L.sw, L.ph, L.pw};
+    const uint32_t cgroups = uint32_t((L.C + IM2COL_CPW - 1) / IM2COL_CPW);
+    Im2colGeom g{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
+                 uint32_t(L.R), uint32_t(L.Wr), cgroups, L.kh, L.kw, L.sh, L.sw, L.ph, L.pw,
+                 make_fastdiv(uint32_t(L.P)), make_fastdiv(uint32_t(L.Wo)),
+                 make_fastdiv(uint32_t(L.Wr))};
     nw = L.Wr;
     lines = L.K;
     len = L.R;
-    hipLaunchKernelGGL(k_pack_im2col, dim3(blocks_for(L.K * L.Wr)), dim3(THREADS), 0, s, src,
-                       dtype, g, dst);
+    const dim3 grid(blocks_for(int64_t(cgroups) * L.Wr));
+    dispatch_dtype(dtype, [&]<int DT>() {
+      if (L.kh == 1 && L.kw == 1)
+        hipLaunchKernelGGL((k_pack_im2col<DT, 1, 1>), grid, dim3(THREADS), 0, s, src, g, dst);
+      else if (L.kh == 3 && L.kw == 3)
+        hipLaunchKernelGGL((k_pack_im2col<DT, 3, 3>), grid, dim3(THREADS), 0, s, src, g, dst);
+      else if (L.kh == 7 && L.kw == 7)
+        hipLaunchKernelGGL((k_pack_im2col<DT, 7, 7>), grid, dim3(THREADS), 0, s, src, g, dst);
+      else
+        hipLaunchKernelGGL((k_pack_im2col<DT, 0, 0>), grid, dim3(THREADS), 0, s, src, g, dst);
+    });
   }
   if (last_launch_status() != FQT_OK) return FQT_E_HIP;
   if (linesum) {

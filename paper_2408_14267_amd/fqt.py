@@ -49,6 +49,7 @@ class fqt_quant_cfg(Structure):
 
 class fqt_qgrad(Structure):
     _fields_ = [("psq_planes", c_void_p), ("pcq_planes", c_void_p),
+                ("psq_codes", c_void_p), ("pcq_codes", c_void_p),
                 ("psq_kept", c_void_p), ("psq_count", c_void_p),
                 ("pcq_kept", c_void_p), ("pcq_count", c_void_p),
                 ("psq_scale", c_void_p), ("psq_offset", c_void_p), ("psq_prob", c_void_p),
@@ -63,13 +64,14 @@ def _load():
     D, Q, G = POINTER(fqt_layer_desc), POINTER(fqt_quant_cfg), POINTER(fqt_qgrad)
     sig = {
         "fqt_status_string": (c_char_p, [c_int]),
-        "fqt_qgrad_words": (c_int, [D, Q, POINTER(c_int64), POINTER(c_int64)]),
+        "fqt_qgrad_words": (c_int, [D, Q, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64),
+                                    POINTER(c_int64)]),
         "fqt_workspace_size": (c_int, [D, Q, c_int32, POINTER(c_size_t)]),
         "fqt_agp_scq_quantize": (c_int, [D, Q, c_void_p, G, c_void_p, c_size_t, c_void_p]),
         "fqt_pack_bits": (c_int, [c_void_p, c_int32, c_int64, c_int64, c_int64, c_int32, D,
                                   c_void_p, c_void_p, c_void_p]),
-        "fqt_binary_gemm_dw": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
-        "fqt_binary_gemm_dx": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dw": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dx": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p]),
         "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
     }
@@ -127,9 +129,10 @@ def fqt_status_string(status):
 
 
 def fqt_qgrad_words(desc, cfg):
-    a, b = c_int64(), c_int64()
-    _check(_lib.fqt_qgrad_words(desc, cfg, ctypes.byref(a), ctypes.byref(b)), "fqt_qgrad_words")
-    return a.value, b.value
+    """(psq plane words, pcq plane words, psq code bytes, pcq code bytes)."""
+    v = [c_int64() for _ in range(4)]
+    _check(_lib.fqt_qgrad_words(desc, cfg, *(ctypes.byref(x) for x in v)), "fqt_qgrad_words")
+    return tuple(x.value for x in v)
 
 
 def fqt_workspace_size(desc, cfg, which=FQT_WS_LAYER):
@@ -150,16 +153,14 @@ def fqt_pack_bits(src, dtype, rows, cols, ld, axis, conv, dst, linesum=None, str
                               _ptr(dst), _ptr(linesum), _stream(stream)), "fqt_pack_bits")
 
 
-def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, xsign_sum, dW, I_out=None, stream=None):
-    _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign),
-                                   _ptr(xsign_sum), _ptr(dW), _ptr(I_out), _stream(stream)),
-           "fqt_binary_gemm_dw")
+def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, I_out=None, stream=None):
+    _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign), _ptr(dW),
+                                   _ptr(I_out), _stream(stream)), "fqt_binary_gemm_dw")
 
 
-def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, wsign_sum, dX, I_out=None, stream=None):
-    _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign),
-                                   _ptr(wsign_sum), _ptr(dX), _ptr(I_out), _stream(stream)),
-           "fqt_binary_gemm_dx")
+def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, dX, I_out=None, stream=None):
+    _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign), _ptr(dX),
+                                   _ptr(I_out), _stream(stream)), "fqt_binary_gemm_dx")
 
 
 def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):
@@ -174,18 +175,21 @@ class QGrad:
     """Device buffers of one fqt_qgrad (allocated with torch), plus the ctypes struct."""
 
     def __init__(self, desc, cfg, device="cuda"):
-        psq_words, pcq_words = fqt_qgrad_words(desc, cfg)
+        psq_words, pcq_words, psq_bytes, pcq_bytes = fqt_qgrad_words(desc, cfg)
         N, D = desc.N, desc.D
         i32 = dict(dtype=torch.int32, device=device)
         f32 = dict(dtype=torch.float32, device=device)
         self.psq_planes = torch.empty(psq_words, dtype=torch.int64, device=device)
         self.pcq_planes = torch.empty(pcq_words, dtype=torch.int64, device=device)
+        self.psq_codes = torch.empty(psq_bytes, dtype=torch.uint8, device=device)
+        self.pcq_codes = torch.empty(pcq_bytes, dtype=torch.uint8, device=device)
         self.psq_kept, self.psq_count = torch.empty(N, **i32), torch.empty(1, **i32)
         self.pcq_kept, self.pcq_count = torch.empty(D, **i32), torch.empty(1, **i32)
         self.psq_scale, self.psq_offset, self.psq_prob = (torch.empty(N, **f32) for _ in range(3))
         self.pcq_scale, self.pcq_offset, self.pcq_prob = (torch.empty(D, **f32) for _ in range(3))
         self.struct = fqt_qgrad(*(t.data_ptr() for t in (
-            self.psq_planes, self.pcq_planes, self.psq_kept, self.psq_count, self.pcq_kept,
+            self.psq_planes, self.pcq_planes, self.psq_codes, self.pcq_codes,
+            self.psq_kept, self.psq_count, self.pcq_kept,
             self.pcq_count, self.psq_scale, self.psq_offset, self.psq_prob, self.pcq_scale,
             self.pcq_offset, self.pcq_prob)))
 

@@ -71,9 +71,10 @@ def test_cfg_validation(bits, mode):
 def test_workspace_and_plane_sizes():
     d = _desc()
     c = fqt.quant_cfg(4)
-    psq, pcq = fqt.fqt_qgrad_words(d, c)
+    psq, pcq, psq_b, pcq_b = fqt.fqt_qgrad_words(d, c)
     R = 128 * 64
     assert psq == 4 * R * 4 and pcq == 4 * 256 * (R // 64)
+    assert psq_b == R * 256 and pcq_b == 256 * R
     ws_layer = fqt.fqt_workspace_size(d, c, fqt.FQT_WS_LAYER)
     ws_q = fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE)
     assert ws_layer > (psq + pcq) * 8 > ws_q > 0
@@ -104,5 +105,5 @@ def test_null_and_small_workspace_rejected_before_launch():
     assert st == fqt.FQT_E_NULL
     q = fqt.fqt_qgrad()
     st = lib.fqt_binary_gemm_dw(ctypes.byref(d), ctypes.byref(c), ctypes.byref(q), fake, fake,
-                                fake, None, None)
+                                None, None)
     assert st == fqt.FQT_E_NULL

@@ -52,6 +52,10 @@ CASES = [
     ("linear_N1_D1", LayerShape("fc", "linear", 1, 5, 1), 2, 0, Recipe(), "f32"),
     ("linear_wideD_b4", LayerShape("fc", "linear", 8, 64, 5000), 4, 0,
      Recipe("channel_lognormal", sigma=1.5), "f32"),
+    ("conv5x5_b2", LayerShape("c", "conv2d", 3, 6, 40, 10, 10, 5, 5, 1, 1, 2, 2), 2, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv2x3_mixed_stride_b3", LayerShape("c", "conv2d", 2, 5, 9, 6, 7, 2, 3, 1, 2, 0, 1), 3, 0,
+     Recipe("channel_lognormal", sigma=1.0), "f32"),
 ]
 
 
@@ -116,6 +120,12 @@ def _check_quantize(fqt, ref, desc, cfg, dY, layer, bits):
     pcq = _u64(q.pcq_planes).reshape(bits, D, Wr)[:, :kc]
     assert np.array_equal(psq, ref.qgrad.psq_planes), "psq planes"
     assert np.array_equal(pcq, ref.qgrad.pcq_planes), "pcq planes"
+    psq_codes = q.psq_codes.cpu().numpy().reshape(R, Wd * 64)[:ks * P]
+    pcq_codes = q.pcq_codes.cpu().numpy().reshape(D, Wr * 64)[:kc]
+    assert np.array_equal(psq_codes[:, :D], ref.qgrad.psq_rows), "psq codes"
+    assert not psq_codes[:, D:].any(), "psq code padding"
+    assert np.array_equal(pcq_codes[:, :R], ref.qgrad.pcq_rows), "pcq codes"
+    assert not pcq_codes[:, R:].any(), "pcq code padding"
     return q
 
 
@@ -151,10 +161,10 @@ def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
     D, K = layer.D, layer.C * layer.kh * layer.kw
     dW = torch.empty(D, K, dtype=torch.float32, device="cuda")
     I_dw = torch.empty(D, K, dtype=torch.int32, device="cuda")
-    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, xsum, dW, I_dw)
+    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, I_dw)
     dX = torch.empty(X.shape, dtype=X.dtype, device="cuda")
     I_dx = torch.empty(layer.N, layer.C, layer.H, layer.W, dtype=torch.int32, device="cuda")
-    fqt.fqt_binary_gemm_dx(desc, cfg, q, ws_, wsum, dX, I_dx)
+    fqt.fqt_binary_gemm_dx(desc, cfg, q, ws_, dX, I_dx)
     torch.cuda.synchronize()
     assert np.array_equal(I_dw.cpu().numpy(), ref.I_dw), "dW integer product"
     assert np.array_equal(I_dx.cpu().numpy(), ref.I_dx), "dX integer product"
