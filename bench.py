@@ -23,12 +23,35 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOAD = "vgg_cifar_conv3x3_256"
-HBM_PEAK_GBS = 8000.0
-# Integer VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane-instructions/s.
-VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
-# Popcount engine: one 64-bit AND + popcount-accumulate is 4 lane-instructions
-# (2 v_and_b32, 2 v_bcnt_u32_b32) for 64 binary MACs = 128 binary ops.
-POPC_PEAK_TOPS = VALU_LANE_OPS * 128 / 4 / 1e12
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
+
+# HBM traffic per launch from rocprofv3 counter runs of this benchmark (FETCH_SIZE and
+# WRITE_SIZE in KiB per dispatch, one run each), scaled by what the same counters read for
+# a 256 MiB device copy in those runs (FETCH_SIZE reads half the copied bytes).  A figure is
+# reported only while its kernel source is byte-identical to the one it was measured on.
+FETCH_SCALE = 262144.0 / 131083.5
+WRITE_SCALE = 1.0
+TRAFFIC = {
+    "gemm_dx": ("paper_2408_14267_amd/csrc/fqt_gemm.hip",
+                "db5b31697abfb99c80455e7067d86be6160a3c641492b71d4f28677402bbbf77", 2284.5, 8192.0),
+    "gemm_dw": ("paper_2408_14267_amd/csrc/fqt_gemm.hip",
+                "db5b31697abfb99c80455e7067d86be6160a3c641492b71d4f28677402bbbf77", 3504.3, 2304.0),
+    "pack_x": ("paper_2408_14267_amd/csrc/fqt_pack.hip",
+               "8e9562687eb104217ff2bb49dccdcab296c4037ddb36d98efdd665cfb51cf5f2", 4121.7, 2304.0),
+}
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel`, or None when not measured on its current source."""
+    import hashlib
+    if kernel not in TRAFFIC:
+        return None
+    src, sha, fetch_kib, write_kib = TRAFFIC[kernel]
+    with open(os.path.join(ROOT, src), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != sha:
+            return None
+    return (fetch_kib * FETCH_SCALE + write_kib * WRITE_SCALE) * 1024.0
 
 
 def parse():
@@ -40,6 +63,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="bound on the CPU oracle sample (seconds of work)")
     p.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="first run a plain device copy of this many MiB (three times), so that "
+                        "a counter run can scale FETCH_SIZE / WRITE_SIZE by a known byte count")
     return p.parse_args()
 
 
@@ -80,6 +106,13 @@ def main():
     wl = WORKLOADS[WORKLOAD]
     layer = wl.layers[0]
     dev = torch.device("cuda:0")
+    if args.calib_copy_mib:
+        src = torch.ones(args.calib_copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     x, w, dy = draw_layer(layer, wl.recipe, wl.seed, wl.dtype)
     X, W, dY = (torch.from_numpy(a).to(dev) for a in (x, w, dy))
     dX, dW = torch.empty_like(X), torch.empty_like(W)
@@ -107,52 +140,83 @@ def main():
         step()
     ms_eager = timed(step, args.steps)
 
-    ms_graph = None
-    if not args.no_graph:
+    def graph_of(fn, reps):
+        """A HIP graph of `reps` back-to-back calls of fn(stream), captured on a side stream."""
         g = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         side.wait_stream(stream)
         with torch.cuda.stream(side):
-            step_s = lambda: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, side)
-            step_s()
+            fn(side)
             torch.cuda.synchronize()
             with torch.cuda.graph(g, stream=side):
-                step_s()
+                for _ in range(reps):
+                    fn(side)
         torch.cuda.synchronize()
+        return g
+
+    ms_graph = None
+    if not args.no_graph:
+        g = graph_of(lambda st: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st), 1)
         for _ in range(args.warmup):
             g.replay()
         ms_graph = timed(g.replay, args.steps)
     ms = ms_graph if ms_graph is not None else ms_eager
 
-    # Per-product timing of the dominant kernel: the two products are single-kernel
-    # entry points; events bracket each launch on the stream it is issued on.
+    # Single-kernel entry points, each timed as a graph of REPS back-to-back launches replayed
+    # on `stream` between two HIP events (eager launches of a few-microsecond kernel would
+    # time the host instead).
     q = fqt.QGrad(desc, cfg, device=dev)
     qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
     K = layer.C * layer.kh * layer.kw
-    R = layer.N * layer.Ho * layer.Wo
+    P = layer.Ho * layer.Wo
+    R = layer.N * P
     Wd, Wr = (layer.D + 63) // 64, (R + 63) // 64
     xs = torch.empty(K * Wr, dtype=torch.int64, device=dev)
-    xsum = torch.empty(K, dtype=torch.int32, device=dev)
     wsg = torch.empty(K * Wd, dtype=torch.int64, device=dev)
-    wsum = torch.empty(K, dtype=torch.int32, device=dev)
-    fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, stream)
-    fqt.fqt_pack_bits(X, fqt.FQT_F32, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc, xs, xsum, stream)
-    fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K, fqt.FQT_PACK_ALONG_ROWS, None, wsg, wsum, stream)
-    kernels = {
-        "gemm_dw": lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, None, stream),
-        "gemm_dx": lambda: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsg, dX, None, stream),
+    entries = {
+        "quantize(4 kernels)": lambda st: fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st),
+        "pack_x": lambda st: fqt.fqt_pack_bits(X, fqt.FQT_F32, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc,
+                                               xs, None, st),
+        "pack_w": lambda st: fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K,
+                                               fqt.FQT_PACK_ALONG_ROWS, None, wsg, None, st),
+        "gemm_dw": lambda st: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, None, st),
+        "gemm_dx": lambda st: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsg, dX, None, st),
     }
+    REPS = 20
     per = {}
-    for name, fn in kernels.items():
-        for _ in range(args.warmup):
-            fn()
-        per[name] = timed(fn, args.steps)
-    dom = max(per, key=per.get)
-    # Algorithmic binary ops of one product launch (binary-equivalent, as the paper counts).
-    achieved = 2 * macs / (per[dom] * 1e-3) / 1e12
-    roofline = {"bound": "alu", "achieved": achieved, "peak": POPC_PEAK_TOPS, "unit": "TOPS",
-                "frac": achieved / POPC_PEAK_TOPS, "traffic": None, "kernel": dom,
-                "kernel_ms": per[dom]}
+    for name, fn in entries.items():
+        if args.no_graph:
+            for _ in range(args.warmup):
+                fn(stream)
+            per[name] = timed(lambda: fn(stream), args.steps)
+            continue
+        gk = graph_of(fn, REPS)
+        for _ in range(max(1, args.warmup // REPS)):
+            gk.replay()
+        per[name] = timed(gk.replay, max(1, args.steps // REPS)) / REPS
+    ks, kc = int(q.psq_count.item()), int(q.pcq_count.item())
+    b = wl.bits
+    # Algorithmic bytes (each tensor crosses HBM once; codes at b bits, signs at 1 bit) and
+    # int8 MFMA ops (2 * M * N * K over the kept rows) of each single-kernel entry.
+    work = {
+        "pack_x": (X.numel() * 4 + K * Wr * 8, 0),
+        "pack_w": (W.numel() * 4 + K * Wd * 8, 0),
+        "gemm_dw": (kc * R * b // 8 + K * Wr * 8 + dW.numel() * 4, 2 * kc * K * R),
+        "gemm_dx": (ks * P * layer.D * b // 8 + K * Wd * 8 + dX.numel() * 4,
+                    2 * ks * layer.H * layer.W * layer.C * K * layer.D // layer.C),
+    }
+    dom = max(work, key=lambda k: per[k])
+    nbytes, nops = work[dom]
+    t_s = per[dom] * 1e-3
+    if nbytes / (HBM_PEAK_GBS * 1e9) >= nops / (MFMA_I8_PEAK_TOPS * 1e12):
+        roofline = {"bound": "hbm", "achieved": nbytes / t_s / 1e9, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": nbytes / t_s / 1e9 / HBM_PEAK_GBS}
+    else:
+        roofline = {"bound": "mfma", "achieved": nops / t_s / 1e12, "peak": MFMA_I8_PEAK_TOPS,
+                    "unit": "TOPS", "frac": nops / t_s / 1e12 / MFMA_I8_PEAK_TOPS}
+    roofline.update({"traffic": measured_traffic(dom), "kernel": dom, "kernel_ms": per[dom],
+                     "algorithmic_bytes": nbytes, "int8_ops": nops,
+                     "kept_samples": ks, "kept_channels": kc})
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -169,7 +233,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u1",
+        "dtype": "u1/i8->i32",
         "data": "synthetic",
         "config": {"workload": WORKLOAD, "layer": "conv3x3 256->256, 8x8, stride 1, pad 1",
                    "batch": layer.N, "bits": wl.bits, "agp": "bernoulli", "inputs": "f32",

@@ -96,6 +96,14 @@ struct Ctr4 {
   uint32_t v[4];
 };
 
+// Word j (0..3, known only at run time) of a Philox block, by selects: indexing the
+// array with a run-time value would move it to scratch memory.
+__device__ __forceinline__ uint32_t ctr_word(const Ctr4 &c, uint32_t j) {
+  const uint32_t lo = (j & 1u) ? c.v[1] : c.v[0];
+  const uint32_t hi = (j & 1u) ? c.v[3] : c.v[2];
+  return (j & 2u) ? hi : lo;
+}
+
 __device__ __forceinline__ Ctr4 philox4x32_10(Ctr4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {

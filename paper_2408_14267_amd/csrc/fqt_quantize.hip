@@ -372,7 +372,7 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
         keep = true;
       } else if (A > 0 && w_rem > 0 && w > 0) {
         const Ctr4 u = philox_block(uint64_t(i) >> 2, S.stream, a.seed, a.step, a.layer);
-        const uint32_t u32 = u.v[i & 3];
+        const uint32_t u32 = ctr_word(u, uint32_t(i) & 3u);
         uint64_t lh, ll;
         mul_32x64(u32, uint64_t(b) * w_rem, lh, ll);
         const uint64_t aw = uint64_t(A) * w;     // < 2^55
@@ -554,7 +554,7 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
         const uint32_t e = elem_index(g, d, r);
         const float xv = load_elem<DT>(a.dy, e) + 0.0f;
         const Ctr4 u = philox_block(e >> 2, STREAM_ELEM, a.seed, a.step, a.layer);
-        const uint32_t uw = u.v[e & 3];
+        const uint32_t uw = ctr_word(u, e & 3u);
         if (ps.rank >= 0) qs = sr_code(xv, ps.z, ps.inv, Bf, uw);
         if (pc.rank >= 0) qc = sr_code(xv, pc.z, pc.inv, Bf, uw);
       }
