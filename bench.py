@@ -167,20 +167,20 @@ def main():
     # time the host instead).
     q = fqt.QGrad(desc, cfg, device=dev)
     qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
+    dws = fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW, device=dev)
     K = layer.C * layer.kh * layer.kw
     P = layer.Ho * layer.Wo
     R = layer.N * P
     Wd, Wr = (layer.D + 63) // 64, (R + 63) // 64
-    xs = torch.empty(K * Wr, dtype=torch.int64, device=dev)
-    wsg = torch.empty(K * Wd, dtype=torch.int64, device=dev)
+    xs = torch.empty(Wr * K, dtype=torch.int64, device=dev)
+    wsb = torch.empty(K, 64 * Wd, dtype=torch.int8, device=dev)
+    wls = torch.empty(K, dtype=torch.int32, device=dev)
     entries = {
         "quantize(4 kernels)": lambda st: fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st),
-        "pack_x": lambda st: fqt.fqt_pack_bits(X, fqt.FQT_F32, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc,
-                                               xs, None, st),
-        "pack_w": lambda st: fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K,
-                                               fqt.FQT_PACK_ALONG_ROWS, None, wsg, None, st),
-        "gemm_dw": lambda st: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, None, st),
-        "gemm_dx": lambda st: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsg, dX, None, st),
+        "pack_x": lambda st: fqt.fqt_pack_input_signs(desc, X, xs, st),
+        "pack_w": lambda st: fqt.fqt_pack_weight_signs(desc, W, wsb, wls, st),
+        "gemm_dw": lambda st: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, dws, None, st),
+        "gemm_dx": lambda st: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsb, wls, dX, None, st),
     }
     REPS = 20
     per = {}

@@ -73,7 +73,9 @@ typedef enum {
 /* Layer geometry (Section 3, Eq. 1-3; Appendix C Unfolder: X_u is NHW x CK^2).
  * Ho = (H + 2 ph - kh) / sh + 1 and Wo likewise must be >= 1.
  * dy_dtype, x_dtype, dx_dtype: FQT_F32 or FQT_BF16; w_dtype: FQT_F32 or FQT_BF16.
- * N*Ho*Wo, N*C*H*W, N*D*Ho*Wo and D*C*kh*kw must stay below 2^31. */
+ * N*Ho*Wo, N*C*H*W, N*D*Ho*Wo and D*C*kh*kw must stay below 2^31, and so must the
+ * byte sizes of the code arrays and of the weight-sign bytes: N*Ho*Wo * 64*ceil(D/64),
+ * D * 64*ceil(N*Ho*Wo/64) and C*kh*kw * 64*ceil(D/64) (FQT_E_SHAPE otherwise). */
 typedef struct {
   int32_t kind;                       /* fqt_layer_kind                                  */
   int32_t dy_dtype, x_dtype, w_dtype, dx_dtype;
@@ -103,9 +105,13 @@ typedef struct {
  *                                   Rows >= count*P are left untouched.
  *   pcq_planes  uint64 [b][D][Wr]   PCQ code planes; row j holds the j-th kept channel,
  *                                   packed along (n, ho, wo).  Rows >= count untouched.
- *   psq_codes   uint8 [R][Wd*64]    the same PSQ codes one byte each (the operand of the
- *                                   int8 products), rows as in psq_planes, bytes past D = 0
- *   pcq_codes   uint8 [D][Wr*64]    the PCQ codes one byte each, bytes past R = 0
+ *   psq_codes   uint8 [2*Wd][R][32] the same PSQ codes one byte each (the operand of the
+ *                                   int8 products), chunk-major: code d of row r (rows as
+ *                                   in psq_planes) at ((d/32)*R + r)*32 + d%32; codes past
+ *                                   D are 0.  The 32-byte chunks of consecutive rows are
+ *                                   adjacent, so the product's operand loads coalesce.
+ *   pcq_codes   uint8 [2*Wr][D][32] the PCQ codes one byte each, chunk-major: code r of
+ *                                   row j at ((r/32)*D + j)*32 + r%32; codes past R are 0
  *   psq_kept    int32 [N]           kept sample ids ascending, then pruned ids ascending
  *   psq_count   int32 [1]           number of kept samples
  *   psq_scale   float [N]           S_n = R_n / (B p_n) if kept, else 0
@@ -129,11 +135,13 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
                     int64_t *pcq_code_bytes);
 
 /* Workspace sizes (host call).  which = FQT_WS_QUANTIZE for fqt_agp_scq_quantize,
- * FQT_WS_LAYER for fqt_layer_backward (which holds an fqt_qgrad and the packed signs
+ * FQT_WS_GEMM_DW for fqt_binary_gemm_dw (its split partial sums), FQT_WS_LAYER for
+ * fqt_layer_backward (which holds an fqt_qgrad, the packed signs and the partial sums
  * inside it).  The library carves the workspace; its contents need no initialisation
  * and are garbage after the call. */
 #define FQT_WS_QUANTIZE 0
 #define FQT_WS_LAYER 1
+#define FQT_WS_GEMM_DW 2
 int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
                        size_t *bytes);
 
@@ -175,13 +183,33 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
  *   I[d][k]  = sum_r q_pcq[d][r] * s_X[r][k]   (k over C*kh*kw, r over N*Ho*Wo);
  *   dW[d][k] = S_d * I[d][k] + Z'_d * c_X[k] in float32 for kept channels, 0 for pruned,
  *   with c_X[k] = sum_r s_X[r][k] (the zero-point term).
- * Computed on int8 MFMA from q->pcq_codes and the packed signs (unpacked in registers).
- * xsign: uint64 [C*kh*kw][ceil(N*Ho*Wo/64)] (fqt_pack_bits IM2COL, or ALONG_ROWS of X for
- * a linear layer).  dW: float [D][C*kh*kw].  I_out (optional): int32 [D][C*kh*kw] receives
- * I (0 in pruned rows). */
+ * Computed on int8 MFMA from q->pcq_codes and the packed signs, which are expanded to
+ * +-1 bytes in registers, in slices of N*Ho*Wo whose partial sums meet in the workspace.
+ * xsign: the output of fqt_pack_input_signs for the layer's X.  dW: float [D][C*kh*kw].  I_out (optional): int32 [D][C*kh*kw] receives
+ * I (0 in pruned rows).  ws: >= fqt_workspace_size(FQT_WS_GEMM_DW) bytes, 256-byte
+ * aligned. */
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
                        const fqt_qgrad *q, const uint64_t *xsign, float *dW, int32_t *I_out,
-                       void *hip_stream);
+                       void *ws, size_t ws_bytes, void *hip_stream);
+
+/* sign(X) in the operand form of the dW product (Section 5.1 binarizer; Appendix C Alg. 2
+ * and the Unfolder): the bits of fqt_pack_bits IM2COL for a convolution (ALONG_ROWS of X
+ * [N][C] for a linear layer) stored word-major, dst uint64 [ceil(N*Ho*Wo/64)][C*kh*kw] with
+ * word w of line l at w * C*kh*kw + l, so that the words of consecutive lines are
+ * adjacent.  X has desc->x_dtype. */
+int fqt_pack_input_signs(const fqt_layer_desc *desc, const void *X, uint64_t *dst,
+                         void *hip_stream);
+
+/* sign(W) in the operand form of the int8 dX product (Section 5.1 binarizer; the +-1 form
+ * of Appendix C's {0,1} <-> {+-1} conversion).  W [D][C][kh][kw] of desc->w_dtype is
+ * viewed as [D][C*kh*kw]; with Dp = 64*ceil(D/64), taps = kh*kw, line l = (c, tap):
+ *   dst      int8 [Dp/32][taps][C][32]   byte d of line (c, tap) at
+ *                                 ((d/32 * taps + tap) * C + c) * 32 + d%32: +1 if
+ *                                 W[d][c][tap] > 0, -1 otherwise, for d < D; 0 for
+ *                                 D <= d < Dp.  16-byte aligned.
+ *   linesum  int32 [C*kh*kw]      sum over d < D of dst[l][d] (2 * positives - D). */
+int fqt_pack_weight_signs(const fqt_layer_desc *desc, const void *W, int8_t *dst,
+                          int32_t *linesum, void *hip_stream);
 
 /* Activation-gradient product with PSQ codes (Section 5.3, SCQ; Appendix C Alg. 1, and
  * the Folder for convolutions):
@@ -191,15 +219,16 @@ int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
  *   dX            = S_n * I + Z'_n * c in float32 (rounded to bf16 if dx_dtype is bf16)
  *                   for kept samples, 0 for pruned samples.
  * This is the unfolded product followed by the folder, taken in integers, on int8 MFMA
- * from q->psq_codes.  wsign: uint64 [C*kh*kw][ceil(D/64)] (fqt_pack_bits ALONG_ROWS of W
- * viewed as [D][C*kh*kw]).  kh*kw <= 64.  dX: [N][C][H][W] of dx_dtype.  I_out (optional):
+ * from q->psq_codes.  wsign, wsign_linesum: the outputs of fqt_pack_weight_signs for the
+ * layer's W.  kh*kw <= 64.  dX: [N][C][H][W] of dx_dtype.  I_out (optional):
  * int32 [N][C][H][W]. */
 int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
-                       const fqt_qgrad *q, const uint64_t *wsign, void *dX, int32_t *I_out,
-                       void *hip_stream);
+                       const fqt_qgrad *q, const int8_t *wsign, const int32_t *wsign_linesum,
+                       void *dX, int32_t *I_out, void *hip_stream);
 
 /* Whole layer backward (Appendix C Alg. 1 backward; Section 5.3's final form):
- * quantize dY, pack sign(X) (im2col for conv) and sign(W), then both products.
+ * quantize dY, pack sign(X) (im2col for conv), expand sign(W) to bytes, then both
+ * products.
  * X: x_dtype, W: w_dtype, dY: dy_dtype, dX: dx_dtype, dW: float32.
  * ws: >= fqt_workspace_size(FQT_WS_LAYER) bytes, 256-byte aligned. */
 int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,

@@ -25,7 +25,10 @@ struct Carver {
 struct LayerWs {
   QuantWs qws;
   fqt_qgrad q;
-  uint64_t *xsign, *wsign;
+  uint64_t *xsign;
+  int8_t *wsb;
+  int32_t *wlsum;
+  void *dw_ws;
 };
 
 void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
@@ -56,7 +59,9 @@ size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
   w.q.pcq_offset = c.take<float>(L.D);
   w.q.pcq_prob = c.take<float>(L.D);
   w.xsign = c.take<uint64_t>(size_t(L.K) * L.Wr);
-  w.wsign = c.take<uint64_t>(size_t(L.K) * L.Wd);
+  w.wsb = c.take<int8_t>(size_t(L.K) * L.Wd * 64);
+  w.wlsum = c.take<int32_t>(L.K);
+  w.dw_ws = c.take<char>(gemm_dw_ws_bytes(L));
   if (out) *out = w;
   return c.off;
 }
@@ -124,6 +129,11 @@ int make_layer(const fqt_layer_desc *d, Layer *L) {
   if (l.D * l.K > LIMIT31) return FQT_E_SHAPE;
   l.Wd = (l.D + 63) / 64;
   l.Wr = (l.R + 63) / 64;
+  // Byte sizes of the code arrays and of the weight-sign bytes: the products address
+  // them with 32-bit buffer offsets.
+  if (l.R * l.Wd * 64 > LIMIT31 || l.D * l.Wr * 64 > LIMIT31 || l.K * l.Wd * 64 > LIMIT31 ||
+      l.K * l.Wr * 8 > LIMIT31)
+    return FQT_E_SHAPE;
   *L = l;
   return FQT_OK;
 }
@@ -190,6 +200,7 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
   if (!bytes) return FQT_E_NULL;
   if (which == FQT_WS_QUANTIZE) *bytes = quant_ws_bytes(L);
   else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, cfg->bits, nullptr);
+  else if (which == FQT_WS_GEMM_DW) *bytes = gemm_dw_ws_bytes(L);
   else return FQT_E_INVAL;
   return FQT_OK;
 }
@@ -234,27 +245,57 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
 }
 
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
-                       const uint64_t *xsign, float *dW, int32_t *I_out, void *hip_stream) {
+                       const uint64_t *xsign, float *dW, int32_t *I_out, void *ws,
+                       size_t ws_bytes, void *hip_stream) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
   FQT_TRY(check_qgrad(q, false, true));
-  if (!xsign || !dW) return FQT_E_NULL;
-  if (!aligned(xsign, 8) || !aligned(dW, 4) || (I_out && !aligned(I_out, 4))) return FQT_E_ALIGN;
-  return launch_gemm_dw(L, *cfg, *q, xsign, dW, I_out, static_cast<hipStream_t>(hip_stream));
+  if (!xsign || !dW || !ws) return FQT_E_NULL;
+  if (!aligned(xsign, 8) || !aligned(dW, 4) || (I_out && !aligned(I_out, 4)) ||
+      !aligned(ws, 256))
+    return FQT_E_ALIGN;
+  if (ws_bytes < gemm_dw_ws_bytes(L)) return FQT_E_WORKSPACE;
+  return launch_gemm_dw(L, *cfg, *q, xsign, dW, I_out, ws, static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_pack_input_signs(const fqt_layer_desc *desc, const void *X, uint64_t *dst,
+                         void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  if (!X || !dst) return FQT_E_NULL;
+  if (!aligned(X, dtype_size(L.x_t)) || !aligned(dst, 8)) return FQT_E_ALIGN;
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (L.kind == FQT_LINEAR)
+    return launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, dst, nullptr,
+                            s, true);
+  return launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, dst, nullptr, s, true);
+}
+
+int fqt_pack_weight_signs(const fqt_layer_desc *desc, const void *W, int8_t *dst,
+                          int32_t *linesum, void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  if (!W || !dst || !linesum) return FQT_E_NULL;
+  if (!aligned(W, dtype_size(L.w_t)) || !aligned(dst, 16) || !aligned(linesum, 4))
+    return FQT_E_ALIGN;
+  return launch_pack_w_i8(W, L, dst, linesum, static_cast<hipStream_t>(hip_stream));
 }
 
 int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
-                       const uint64_t *wsign, void *dX, int32_t *I_out, void *hip_stream) {
+                       const int8_t *wsign, const int32_t *wsign_linesum, void *dX,
+                       int32_t *I_out, void *hip_stream) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
   FQT_TRY(check_qgrad(q, true, false));
-  if (!wsign || !dX) return FQT_E_NULL;
-  if (!aligned(wsign, 8) || !aligned(dX, dtype_size(L.dx_t)) || (I_out && !aligned(I_out, 4)))
+  if (!wsign || !wsign_linesum || !dX) return FQT_E_NULL;
+  if (!aligned(wsign, 16) || !aligned(wsign_linesum, 4) || !aligned(dX, dtype_size(L.dx_t)) ||
+      (I_out && !aligned(I_out, 4)))
     return FQT_E_ALIGN;
   if (L.kh * L.kw > 64) return FQT_E_SHAPE;
-  return launch_gemm_dx(L, *cfg, *q, wsign, dX, I_out, static_cast<hipStream_t>(hip_stream));
+  return launch_gemm_dx(L, *cfg, *q, wsign, wsign_linesum, dX, I_out,
+                        static_cast<hipStream_t>(hip_stream));
 }
 
 int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
@@ -274,14 +315,13 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   if (L.kh * L.kw > 64) return FQT_E_SHAPE;
   if (L.kind == FQT_LINEAR)
     FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,
-                             nullptr, s));
+                             nullptr, s, true));
   else
-    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s));
-  FQT_TRY(launch_pack_bits(W, L.w_t, L.D, L.K, L.K, FQT_PACK_ALONG_ROWS, nullptr, w.wsign,
-                           nullptr, s));
+    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s, true));
+  FQT_TRY(launch_pack_w_i8(W, L, w.wsb, w.wlsum, s));
   FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
-  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, dW, nullptr, s));
-  return launch_gemm_dx(L, *cfg, w.q, w.wsign, dX, nullptr, s);
+  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, dW, nullptr, w.dw_ws, s));
+  return launch_gemm_dx(L, *cfg, w.q, w.wsb, w.wlsum, dX, nullptr, s);
 }
 
 }  // extern "C"

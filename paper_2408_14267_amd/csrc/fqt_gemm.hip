@@ -2,19 +2,29 @@
 // (Section 5.3, SCQ; Appendix C, Alg. 1 binary products and dequantization, the
 // {0,1} <-> {+-1} conversion and the Folder).
 //
-// Operands: the b-bit codes as bytes (written by the quantizer next to the bit planes)
-// and the packed sign bits, unpacked in registers to {0,1} bytes t.  With s = 2t - 1,
-//     I = sum_j q_j s_j = 2 * sum_j q_j t_j - sum_j q_j,
-// so the MFMA computes sum q t (int32, exact), the row code sums come from v_dot4 on
-// the same bytes, and the line popcounts T = sum t give the zero-point column sums
-// c = 2T - len.  For b = 8 the codes do not fit a signed byte; the MFMA then takes
-// q - 128 and adds 128 T back.  The rescale S * I + Z' * c is one float32 step per
-// output without contraction.
+// Both products contract b-bit codes q (one byte each, written by the quantizer next to
+// the bit planes) with signs s = +-1 held as signed bytes, so one v_mfma_i32_32x32x32_i8
+// chain gives I = sum_j q_j s_j exactly in int32.  For b = 8 the codes do not fit a
+// signed byte: the MFMA takes q - 128 and 128 * (sum of the signs it saw) is added back.
+//   dX: the weight signs arrive expanded to +-1 bytes (fqt_pack_weight_signs), so the
+//       inner loop is two 16-byte buffer loads and one MFMA.  The zero-point term
+//       c = sum over the valid taps of the per-(channel, tap) sign sums is a float32
+//       MFMA over the taps (exact: integers below 2^24).
+//   dW: the X signs stay packed; each 16-bit piece is expanded in registers to +-1
+//       bytes once and feeds up to four MFMAs (128 kept channels).  c = 2 popcount - len.
+// The rescale S * I + Z' * c is one float32 step per output without contraction.
 //
-// MFMA v_mfma_i32_32x32x32_i8: lane l feeds row (src0) / column (src1) l % 32 with 16
-// bytes of the 32-deep contraction chosen by l / 32; both operands use the same
-// (lane group, byte) -> k assignment, so each product pairs equal k.  Lane l then holds
-// output column l % 32 at rows 8 (v / 4) + 4 (l / 32) + (v % 4), v = 0..15.
+// MFMA layouts (32 x 32 outputs, 16 accumulators per lane): lane l feeds row (src0) and
+// column (src1) l % 32; in the i8 form its 16 bytes are contraction positions
+// 16 (l / 32) .. 16 (l / 32) + 15, in the f32 32x32x2 form its one value is position
+// l / 32.  Lane l then holds column l % 32 at rows 8 (v / 4) + 4 (l / 32) + (v % 4).
+//
+// Operands are read through buffer resources: a lane whose row does not exist (padding
+// tap, pruned slot, channel past the end) gets the offset BUF_NONE, past every buffer,
+// and loads zeros without touching memory.  Every operand layout puts the 32-byte
+// contraction chunks of consecutive MFMA rows next to each other (chunk-major codes,
+// word-major X signs, chunk-major weight bytes), so one operand load of a wave reads
+// about 1 KB of contiguous memory instead of one cache line per lane.
 #include <algorithm>
 
 #include "fqt_internal.hpp"
@@ -24,23 +34,41 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
-// 16 sign bits (LSB first) -> 16 bytes of 0/1 (byte m of dword q holds bit 4q + m).
-// A nibble times 0x00204081 places bit m at bit 8m without carries.
-__device__ __forceinline__ v4i spread16(uint32_t bits) {
-  v4i r;
-  r.x = int((bits & 0xFu) * 0x00204081u & 0x01010101u);
-  r.y = int(((bits >> 4) & 0xFu) * 0x00204081u & 0x01010101u);
-  r.z = int(((bits >> 8) & 0xFu) * 0x00204081u & 0x01010101u);
-  r.w = int(((bits >> 12) & 0xFu) * 0x00204081u & 0x01010101u);
-  return r;
+constexpr uint32_t BUF_NONE = 0x80000000u;   // every buffer here is shorter than 2^31 bytes
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, uint32_t bytes) {
+  // Raw buffer (stride 0) of `bytes` bytes; 0x00020000 is the gfx9 32-bit data format.
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
 }
 
-__device__ __forceinline__ uint32_t byte_sum16(v4i a) {
-  uint32_t s = __builtin_amdgcn_udot4(uint32_t(a.x), 0x01010101u, 0u, false);
-  s = __builtin_amdgcn_udot4(uint32_t(a.y), 0x01010101u, s, false);
-  s = __builtin_amdgcn_udot4(uint32_t(a.z), 0x01010101u, s, false);
-  return __builtin_amdgcn_udot4(uint32_t(a.w), 0x01010101u, s, false);
+// 16 bytes at byte offset voff + soff of buffer r (soff wave-uniform: it rides in an SGPR).
+__device__ __forceinline__ v4i load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint64_t load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+
+// The wave index as a scalar, so that per-wave loop bounds and strides stay in SGPRs.
+__device__ __forceinline__ uint32_t wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+// 16 sign bits (LSB first) -> 16 signed bytes, +1 for a set bit and -1 for a clear one
+// (byte m of dword k holds bit 4k + m).  A nibble times 0x00408102 puts bit m at bit
+// 8m + 1 without carries; per byte 2t + 0x7F is 0x7F or 0x81, and flipping bit 7 gives
+// 0xFF (-1) or 0x01 (+1).
+__device__ __forceinline__ v4i signs16(uint32_t bits) {
+  v4i r;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t t2 = (((bits >> (4 * k)) & 0xFu) * 0x00408102u) & 0x02020202u;
+    r[k] = int((t2 + 0x7F7F7F7Fu) ^ 0x80808080u);
+  }
+  return r;
 }
 
 __device__ __forceinline__ v4i bias128(v4i a) {
@@ -48,13 +76,16 @@ __device__ __forceinline__ v4i bias128(v4i a) {
   return v4i{a.x ^ m, a.y ^ m, a.z ^ m, a.w ^ m};
 }
 
-__device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
+__device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
   return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float rescale(float S, int I, float Zp, int c) {
-  return __fadd_rn(__fmul_rn(S, float(I)), __fmul_rn(Zp, float(c)));
+__device__ __forceinline__ float rescale(float S, int I, float Zp, float c) {
+  return __fadd_rn(__fmul_rn(S, float(I)), __fmul_rn(Zp, c));
 }
+
+// Output row (0..31) of accumulator v of a lane in half-wave g.
+__device__ __forceinline__ int acc_row(int v, int g) { return 8 * (v >> 2) + 4 * g + (v & 3); }
 
 // Zero `count` elements of `esize` bytes starting at element `first` of `base`, by the
 // `nthr` threads of a block: 16-byte stores where the run is 16-byte aligned, bytes of
@@ -82,156 +113,196 @@ __device__ void zero_run(void *base, size_t first, size_t count, int esize, int 
 // ----------------------------------------------------------------------------- dW
 
 struct DwArgs {
-  const uint8_t *codes;          // PCQ codes [D][Wr*64]
+  const uint8_t *codes;          // PCQ codes [2*Wr][D][32], chunk-major
   const int32_t *kept, *count;   // [D], [1]
   const float *scale, *offset;   // [D]
-  const uint64_t *xsign;         // [K][Wr]
+  const uint64_t *xsign;         // [Wr][K], word-major
   float *dW;                     // [D][K]
   int32_t *I_out;                // [D][K] or null
-  uint32_t D, K, R, Wr, ktiles;
-  int bits8;
+  int32_t *part;                 // [S][D][K] partial sums of each split (slots < count)
+  int32_t *partT;                // [S][K] set bits of each split of each sign line
+  uint32_t D, K, R, Rp, Wr, ktiles, codes_bytes, xsign_bytes, S, wps;
+  FastDiv divS, divKt, divK;
 };
 
-constexpr int DW_WAVES = 16;
+constexpr int DW_RT = 4;                    // 32-row tiles of kept channels per block
+constexpr int DW_WAVES = 4;
 constexpr int DW_THREADS = DW_WAVES * 64;
-constexpr int DW_BATCH = 4;        // 64-bit words of the contraction loaded per batch
+constexpr int DW_PREF = 2;                  // 64-bit words of the contraction loaded per batch
 
-// Grid: one block per 32x32 tile of (kept-channel slot, column of C*kh*kw) over the slot
-// capacity D, plus a pool of extra blocks.  Blocks of the first ceil(count/32) slot tiles
-// compute; all later blocks zero the dW rows of the pruned channels, each a contiguous
-// run of K floats.
-// A computing block is one 32x32 MFMA tile; sixteen waves split the contraction over
-// N*Ho*Wo word by word (wave w takes words w, w+16, ...) and sum in LDS.
-__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw(DwArgs a) {
-  __shared__ int32_t red[16][64];
-  __shared__ int32_t qred[32];
+// Split-R partial products.  Grid: S splits x ceil(D/128) slot groups x ceil(K/32) column
+// tiles over the slot capacity, the split index fastest (consecutive blocks land on
+// different XCDs, so each XCD reads its own slices of the codes and of the signs).  A block
+// of a live group (slot group below ceil(count/128)) holds up to four 32x32 MFMA tiles,
+// the live slot tiles of its group over 32 columns, for the words [s*wps, (s+1)*wps) of
+// the contraction over N*Ho*Wo; its four waves take every fourth word, expand each 16-bit
+// piece of their column's word once and feed it to every tile.  The four partial tiles
+// meet in LDS; the block writes its sum and its set-bit counts to the split's slice.
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
+  __shared__ int32_t red[DW_WAVES - 1][DW_RT][16][64];
   __shared__ int32_t tred[32];
-  __shared__ int32_t rowd[32];
-  __shared__ float rows_s[32], rows_z[32];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
-  const uint32_t live_blocks = uint32_t((count + 31) / 32) * a.ktiles;
+  const uint32_t rest = fdiv(blockIdx.x, a.divS);
+  const uint32_t sp = blockIdx.x - rest * a.S;
+  const uint32_t grp = fdiv(rest, a.divKt);
+  const uint32_t j0 = grp * (DW_RT * 32), k0 = (rest - grp * a.ktiles) * 32;
+  if (int(j0) >= count) return;               // slot group past the kept channels
+  const int nrt = min(DW_RT, (count - int(j0) + 31) / 32);   // live slot tiles, >= 1
+  if (t < 32) tred[t] = 0;
 
-  if (blockIdx.x >= live_blocks) {      // zero the rows of pruned channels, one row per block
-    const uint32_t nz = gridDim.x - live_blocks;
-    for (uint32_t row = blockIdx.x - live_blocks; row < a.D - uint32_t(count); row += nz) {
-      const size_t d = size_t(a.kept[uint32_t(count) + row]);
-      zero_run(a.dW, d * a.K, a.K, 4, t, DW_THREADS);
-      if (a.I_out) zero_run(a.I_out, d * a.K, a.K, 4, t, DW_THREADS);
-    }
-    return;
-  }
-  const uint32_t j0 = (blockIdx.x / a.ktiles) * 32, k0 = (blockIdx.x % a.ktiles) * 32;
-
-  (&red[0][0])[t] = 0;
-  if (t < 32) {
-    qred[t] = 0;
-    tred[t] = 0;
-    const uint32_t j = j0 + t;
-    const int d = (int(j) < count) ? a.kept[j] : -1;
-    rowd[t] = d;
-    rows_s[t] = d >= 0 ? a.scale[d] : 0.0f;
-    rows_z[t] = d >= 0 ? a.offset[d] : 0.0f;
-  }
-  __syncthreads();
-
-  v16i acc = {0};
-  uint32_t qpart = 0, tpart = 0;
-  const uint32_t jr = j0 + i, kc = k0 + i;
-  const bool a_ok = int(jr) < count, b_ok = kc < a.K;
-  const uint8_t *arow = a.codes + size_t(a_ok ? jr : 0) * a.Wr * 64 + 16 * g;
-  const uint64_t *brow = a.xsign + size_t(b_ok ? kc : 0) * a.Wr;
-  for (uint32_t c0 = wave; c0 < a.Wr; c0 += DW_WAVES * DW_BATCH) {
-    v4i av[DW_BATCH][2];
-    uint64_t wb[DW_BATCH];
+  const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
+  const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
+  uint32_t aoff[DW_RT];
 #pragma unroll
-    for (int u = 0; u < DW_BATCH; ++u) {
-      const uint32_t c = c0 + u * DW_WAVES;
-      const bool live = c < a.Wr;
-      av[u][0] = (live && a_ok) ? *reinterpret_cast<const v4i *>(arow + size_t(c) * 64)
-                                : v4i{0, 0, 0, 0};
-      av[u][1] = (live && a_ok) ? *reinterpret_cast<const v4i *>(arow + size_t(c) * 64 + 32)
-                                : v4i{0, 0, 0, 0};
-      wb[u] = (live && b_ok) ? brow[c] : 0ull;
+  for (int rt = 0; rt < DW_RT; ++rt) {
+    const uint32_t j = j0 + 32 * rt + i;
+    aoff[rt] = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
+  }
+  const uint32_t kc = k0 + i;
+  const bool b_ok = kc < a.K;
+  const uint32_t boff = b_ok ? kc * 8 : BUF_NONE;
+  const uint32_t w_end = min(a.Wr, (sp + 1) * a.wps);
+  const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
+
+  v16i acc[DW_RT];
+#pragma unroll
+  for (int rt = 0; rt < DW_RT; ++rt) acc[rt] = v16i{0};
+  uint32_t tpart = 0;
+  for (uint32_t c0 = sp * a.wps + wave; c0 < w_end; c0 += DW_WAVES * DW_PREF) {
+    uint64_t word[DW_PREF];
+    v4i A[DW_PREF][2][DW_RT];
+#pragma unroll
+    for (int u = 0; u < DW_PREF; ++u) {
+      // Past the split's last word the loads read word c0 again (in bounds); the products
+      // of those words are skipped below.
+      const uint32_t c = c0 + u * DW_WAVES < w_end ? c0 + u * DW_WAVES : c0;
+      word[u] = load8(xrs, boff, c * a.K * 8);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int rt = 0; rt < DW_RT; ++rt)
+          A[u][h][rt] = rt < nrt ? load16(crs, aoff[rt], (2 * c + h) * chunk_bytes)
+                                 : v4i{0, 0, 0, 0};
     }
 #pragma unroll
-    for (int u = 0; u < DW_BATCH; ++u) {
+    for (int u = 0; u < DW_PREF; ++u) {
+      if (c0 + u * DW_WAVES >= w_end) break;
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        v4i A = av[u][s];
-        qpart += byte_sum16(A);
-        if (a.bits8) A = bias128(A);
-        const uint32_t bb = uint32_t(wb[u] >> (32 * s + 16 * g)) & 0xFFFFu;
-        tpart += __popc(bb);
-        acc = mfma(A, spread16(bb), acc);
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t bits = uint32_t(word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
+        tpart += __popc(bits);
+        const v4i B = signs16(bits);
+#pragma unroll
+        for (int rt = 0; rt < DW_RT; ++rt)
+          if (rt < nrt) acc[rt] = mfma_i8(B8 ? bias128(A[u][h][rt]) : A[u][h][rt], B, acc[rt]);
       }
     }
   }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) atomicAdd(&red[v][lane], acc[v]);
-  atomicAdd(&qred[i], int(qpart));
+  __syncthreads();                      // tred is initialised
   atomicAdd(&tred[i], int(tpart));
+  if (wave > 0) {
+#pragma unroll
+    for (int rt = 0; rt < DW_RT; ++rt) {
+      if (rt >= nrt) break;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) red[wave - 1][rt][v][lane] = acc[rt][v];
+    }
+  }
   __syncthreads();
+  if (wave != 0 || !b_ok) return;
+  if (g == 0) a.partT[size_t(sp) * a.K + kc] = tred[i];
+#pragma unroll
+  for (int rt = 0; rt < DW_RT; ++rt) {
+    if (rt >= nrt) break;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = 32 * rt + acc_row(v, g);
+      if (int(j0) + row >= count) continue;
+      int s = acc[rt][v];
+#pragma unroll
+      for (int w = 0; w < DW_WAVES - 1; ++w) s += red[w][rt][v][lane];
+      a.part[(size_t(sp) * a.D + j0 + row) * a.K + kc] = s;
+    }
+  }
+}
 
-  const int row = t >> 5, col = t & 31;
-  const int d = rowd[row];
-  const uint32_t k = k0 + col;
-  if (d < 0 || k >= a.K) return;          // rows past the count belong to the zero blocks
-  const int T = tred[col];
-  int Ip = red[4 * (row >> 3) + (row & 3)][col + 32 * ((row >> 2) & 1)];
-  if (a.bits8) Ip += 128 * T;
-  const int I = 2 * Ip - qred[row];
-  const size_t idx = size_t(d) * a.K + k;
-  a.dW[idx] = rescale(rows_s[row], I, rows_z[row], 2 * T - int(a.R));
+// dW from the split partials: one thread per element (slot, k) of the slot capacity.  A
+// kept slot sums its S partials, I = sum (+ 128 (2T - Rp) for b = 8, whose codes entered
+// as q - 128 against every sign including the zero tail of the last word) and writes
+// S_d * I + Z'_d * (2T - N*Ho*Wo) to row d = kept[slot]; a pruned slot zeroes its row.
+template <bool B8>
+__global__ __launch_bounds__(256) void k_dw_finish(DwArgs a) {
+  const uint32_t e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= a.D * a.K) return;
+  const uint32_t slot = fdiv(e, a.divK), k = e - slot * a.K;
+  const int count = *a.count;
+  const size_t d = size_t(a.kept[slot]);
+  const size_t idx = d * a.K + k;
+  if (int(slot) >= count) {
+    a.dW[idx] = 0.0f;
+    if (a.I_out) a.I_out[idx] = 0;
+    return;
+  }
+  int I = 0, T = 0;
+  for (uint32_t s = 0; s < a.S; ++s) {
+    I += a.part[(size_t(s) * a.D + slot) * a.K + k];
+    T += a.partT[size_t(s) * a.K + k];
+  }
+  if (B8) I += 128 * (2 * T - int(a.Rp));
+  a.dW[idx] = rescale(a.scale[d], I, a.offset[d], float(2 * T - int(a.R)));
   if (a.I_out) a.I_out[idx] = I;
 }
 
 // ----------------------------------------------------------------------------- dX
 
 struct DxArgs {
-  const uint8_t *codes;          // PSQ codes [N*Ho*Wo][Wd*64]
+  const uint8_t *codes;          // PSQ codes [Dp/32][N*Ho*Wo][32], chunk-major
   const int32_t *kept, *count;   // [N], [1]
   const float *scale, *offset;   // [N]
-  const uint64_t *wsign;         // [C*kh*kw][Wd]
+  const int8_t *wsb;             // sign(W) bytes [Dp/32][kh*kw][C][32]: +-1, 0 past D
+  const int32_t *wlsum;          // [C*kh*kw] sum over d of the signs of each line
   void *dX;                      // [N][C][H][W]
   int32_t *I_out;
   int dx_t;
-  uint32_t N, C, H, W, HW, Ho, Wo, P, D, Wd, ctiles, CHW;
+  uint32_t N, C, H, W, HW, Ho, Wo, P, R, Dp, ctiles, CHW, taps, nch;   // nch = Dp / 32
+  uint32_t codes_bytes, wsb_bytes;
   int kh, kw, sh, sw, ph, pw;
-  FastDiv divHW, divW, divWd;
-  int bits8;
+  FastDiv divHW, divW, divKw, divNch, divCt;
 };
 
 constexpr int DX_MAX_TAPS = 64;
-constexpr int DX_WAVES = 8;
+constexpr int DX_WAVES = 4;
 constexpr int DX_THREADS = DX_WAVES * 64;
-constexpr int DX_BATCH = 4;        // contraction steps (tap, 64-bit word of D) per batch
 
-// Grid: one block per 32x32 tile of (row m = (kept slot, h, w), channel) over the capacity
+// NB: contraction steps (tap, 32 bytes of D) a wave loads at once, sized on the host so
+// that the common shapes take one batch: the loads of a wave then cost one memory latency.
+// Grid: one block per 32x32 tile of (channel, row m = (kept slot, h, w)) over the capacity
 // N*H*W rows, plus a pool of extra blocks.  Blocks of the first ceil(count*H*W/32) row
 // tiles compute; all later blocks zero the pruned samples of dX, each a contiguous run of
 // C*H*W elements.
 // A computing block is one 32x32 MFMA tile with the sign operand as src0 (rows =
-// channels) so output lanes run along pixels.  Eight waves split the contraction steps
-// (tap, word of D).  For tap (i, j) a pixel (h, w) reads the code row of the output pixel
-// (ho, wo) with ho*sh - ph + i = h and wo*sw - pw + j = w, or nothing; the row of every
-// (pixel, tap) is tabulated once per block.
+// channels) so output lanes run along pixels.  Its four waves take every fourth
+// contraction step (tap, 32 bytes of D).  For tap (i, j) a pixel (h, w) reads the code row
+// of the output pixel (ho, wo) with ho*sh - ph + i = h and wo*sw - pw + j = w, or nothing;
+// the byte offset of every (tap, pixel) row is tabulated once per block.
+template <bool B8, int NB>
 __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
-  // Rows padded to DX_MAX_TAPS + 1 words: lanes reading column `tap` of 32 rows hit 32 banks.
-  __shared__ int32_t rowtab[32][DX_MAX_TAPS + 1];   // code row of (pixel, tap), -1 if none
-  __shared__ uint64_t vmask[32];                    // taps that reach each pixel
-  __shared__ int32_t Tt[32][DX_MAX_TAPS + 1];       // popcount of sign(W) line (channel, tap)
-  __shared__ int32_t red[16][64];
-  __shared__ int32_t qred[32];                  // code sums of each pixel's rows
-  __shared__ int32_t pix_out[32];               // NCHW offset of (sample, pixel) minus channel
+  __shared__ uint32_t rowoff[DX_MAX_TAPS][32];     // 32 * code row, BUF_NONE if none
+  __shared__ int32_t redi[DX_WAVES - 1][16][64];
+  __shared__ float redf[DX_WAVES - 1][16][64];
+  __shared__ int32_t pix_out[32];                  // NCHW offset of (sample, pixel) minus channel
   __shared__ float pix_s[32], pix_z[32];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  __shared__ int32_t ltot[32];                     // b = 8: sum of every sign of the channel
+  const int t = threadIdx.x, lane = t & 63;
+  const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
   const uint32_t live_rows = uint32_t(count) * a.HW;
   const uint32_t live_blocks = ((live_rows + 31) / 32) * a.ctiles;
-  const int taps = a.kh * a.kw;
 
   if (blockIdx.x >= live_blocks) {      // zero the pruned samples, one sample per block
     const uint32_t nz = gridDim.x - live_blocks;
@@ -242,29 +313,28 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
     }
     return;
   }
-  const uint32_t m0 = (blockIdx.x / a.ctiles) * 32, c0 = (blockIdx.x % a.ctiles) * 32;
+  const uint32_t mt = fdiv(blockIdx.x, a.divCt);
+  const uint32_t m0 = mt * 32, c0 = (blockIdx.x - mt * a.ctiles) * 32;
+  const int taps = int(a.taps);
 
   for (int e = t; e < 32 * taps; e += DX_THREADS) {
-    const int p = e / taps, tap = e - p * taps;
-    const int ti = tap / a.kw, tj = tap - ti * a.kw;
+    const int p = e & 31, tap = e >> 5;
+    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
     const uint32_t m = m0 + p;
-    int row = -1;
+    uint32_t off = BUF_NONE;
     if (m < live_rows) {
       const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
       const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
-      const int th = int(h) + a.ph - ti, tw = int(w) + a.pw - tj;
+      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
       if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
         const int ho = th / a.sh, wo = tw / a.sw;
-        if (ho < int(a.Ho) && wo < int(a.Wo)) row = int(slot * a.P + ho * a.Wo + wo);
+        if (ho < int(a.Ho) && wo < int(a.Wo))
+          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
       }
     }
-    rowtab[p][tap] = row;
-    Tt[p][tap] = 0;
+    rowoff[tap][p] = off;
   }
-  (&red[0][0])[t] = 0;
-  (&red[0][0])[t + DX_THREADS] = 0;
   if (t < 32) {
-    qred[t] = 0;
     const uint32_t m = m0 + t;
     int off = -1;
     float sc = 0.0f, zo = 0.0f;
@@ -278,77 +348,78 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
     pix_out[t] = off;
     pix_s[t] = sc;
     pix_z[t] = zo;
+  } else if (B8 && t < 64) {
+    const uint32_t ch = c0 + uint32_t(t - 32);
+    int s = 0;
+    if (ch < a.C)
+      for (int tap = 0; tap < taps; ++tap) s += a.wlsum[ch * a.taps + tap];
+    ltot[t - 32] = s;
   }
   __syncthreads();
-  if (t < 32) {
-    uint64_t mk = 0;
-    for (int tap = 0; tap < taps; ++tap) mk |= uint64_t(rowtab[t][tap] >= 0) << tap;
-    vmask[t] = mk;
-  }
 
   // This lane: A row = channel c0 + i, B column = pixel m0 + i.
   const uint32_t ch = c0 + i;
-  const bool ch_ok = ch < a.C;
-  const uint64_t *wbase = a.wsign + size_t(ch_ok ? ch : 0) * taps * a.Wd;
-  const uint8_t *cbase = a.codes + 16 * g;
-  const uint32_t steps = uint32_t(taps) * a.Wd;
+  const uint32_t abase = ch < a.C ? ch * 32 + 16 * g : BUF_NONE;
+  const __amdgpu_buffer_rsrc_t ars = buffer_of(a.wsb, a.wsb_bytes);
+  const __amdgpu_buffer_rsrc_t brs = buffer_of(a.codes, a.codes_bytes);
+  const uint32_t steps = a.taps * a.nch;
   v16i acc = {0};
-  uint32_t qpart = 0;
-  for (uint32_t s0 = wave; s0 < steps; s0 += DX_WAVES * DX_BATCH) {
-    v4i bv[DX_BATCH][2];
-    uint64_t sw[DX_BATCH];
-    int tapu[DX_BATCH];
+  for (uint32_t s0 = wave; s0 < steps; s0 += DX_WAVES * NB) {
+    v4i A[NB], B[NB];
 #pragma unroll
-    for (int u = 0; u < DX_BATCH; ++u) {
-      const uint32_t st = s0 + u * DX_WAVES;
-      const bool live = st < steps;
-      const uint32_t tap = live ? fdiv(st, a.divWd) : 0;
-      const uint32_t dc = st - tap * a.Wd;
-      const int row = live ? rowtab[i][tap] : -1;
-      const uint8_t *p = cbase + (size_t(row < 0 ? 0 : row) * a.Wd + dc) * 64;
-      bv[u][0] = row >= 0 ? *reinterpret_cast<const v4i *>(p) : v4i{0, 0, 0, 0};
-      bv[u][1] = row >= 0 ? *reinterpret_cast<const v4i *>(p + 32) : v4i{0, 0, 0, 0};
-      sw[u] = (live && ch_ok) ? wbase[st] : 0ull;
-      tapu[u] = live ? int(tap) | (row >= 0 ? 0x10000 : 0) : -1;
+    for (int u = 0; u < NB; ++u) {
+      // Steps past the end load step 0 again (in bounds); their products are skipped.
+      const uint32_t st = s0 + u * DX_WAVES < steps ? s0 + u * DX_WAVES : 0;
+      const uint32_t tap = fdiv(st, a.divNch);
+      const uint32_t kc = st - tap * a.nch;
+      A[u] = load16(ars, abase, (kc * a.taps + tap) * a.C * 32);
+      B[u] = load16(brs, rowoff[tap][i] + 16 * g, kc * a.R * 32);
     }
 #pragma unroll
-    for (int u = 0; u < DX_BATCH; ++u) {
-      uint32_t tp = 0;
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        v4i B = bv[u][s];
-        qpart += byte_sum16(B);
-        if (a.bits8 && (tapu[u] & 0x10000)) B = bias128(B);
-        const uint32_t bits = uint32_t(sw[u] >> (32 * s + 16 * g)) & 0xFFFFu;
-        tp += __popc(bits);
-        acc = mfma(spread16(bits), B, acc);
-      }
-      if (tapu[u] >= 0) atomicAdd(&Tt[i][tapu[u] & 0xFFFF], int(tp));
+    for (int u = 0; u < NB; ++u) {
+      if (s0 + u * DX_WAVES >= steps) break;
+      acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
     }
   }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) atomicAdd(&red[v][lane], acc[v]);
-  atomicAdd(&qred[i], int(qpart));
-  __syncthreads();
 
-  // Epilogue: element e -> (channel row crow, pixel column pc).
-  for (int e = t; e < 32 * 32; e += DX_THREADS) {
-    const int pc = e & 31, crow = e >> 5;
-    const uint32_t cc = c0 + crow;
-    const int off = pix_out[pc];
-    if (off < 0 || cc >= a.C) continue;   // rows past the count belong to the zero blocks
-    uint64_t mk = vmask[pc];
-    int T_valid = 0;
-    const int nvalid = __popcll(mk);
-    while (mk) {
-      const int tap = __ffsll(static_cast<unsigned long long>(mk)) - 1;
-      mk &= mk - 1;
-      T_valid += Tt[crow][tap];
+  // Zero-point term over this wave's taps: c[ch][pixel] = sum of wlsum[ch][tap] over the
+  // taps that reach the pixel, as a float32 MFMA taking two taps per step.
+  v16f cacc = {0.0f};
+  for (int tp = 2 * int(wave); tp < taps; tp += 2 * DX_WAVES) {
+    const int tap = tp + g;
+    const bool tv = tap < taps;
+    const float av = (tv && ch < a.C) ? float(a.wlsum[ch * a.taps + tap]) : 0.0f;
+    const float bv = (tv && rowoff[tv ? tap : 0][i] != BUF_NONE) ? 1.0f : 0.0f;
+    cacc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, cacc, 0, 0, 0);
+  }
+
+  if (wave > 0) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      redi[wave - 1][v][lane] = acc[v];
+      redf[wave - 1][v][lane] = cacc[v];
     }
-    int Ip = red[4 * (crow >> 3) + (crow & 3)][pc + 32 * ((crow >> 2) & 1)];
-    if (a.bits8) Ip += 128 * T_valid;
-    const int I = 2 * Ip - qred[pc];
-    const float out = rescale(pix_s[pc], I, pix_z[pc], 2 * T_valid - nvalid * int(a.D));
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 0; w < DX_WAVES - 1; ++w)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      acc[v] += redi[w][v][lane];
+      cacc[v] += redf[w][v][lane];
+    }
+
+  const int off = pix_out[i];
+  if (off < 0) return;                    // rows past the count belong to the zero blocks
+  const float S = pix_s[i], Z = pix_z[i];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int crow = acc_row(v, g);
+    const uint32_t cc = c0 + crow;
+    if (cc >= a.C) continue;
+    const int I = acc[v] + (B8 ? 128 * ltot[crow] : 0);
+    const float out = rescale(S, I, Z, cacc[v]);
     const size_t o = size_t(off) + size_t(cc) * a.HW;
     if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
     else static_cast<float *>(a.dX)[o] = out;
@@ -358,39 +429,75 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
 
 }  // namespace
 
+int gemm_dw_splits(const Layer &L) { return int(L.Wr < 8 ? L.Wr : 8); }
+
+size_t gemm_dw_ws_bytes(const Layer &L) {
+  const size_t S = size_t(gemm_dw_splits(L));
+  return align256(S * size_t(L.D) * L.K * 4) + align256(S * size_t(L.K) * 4);
+}
+
 int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *xsign, float *dW, int32_t *I_out, hipStream_t s) {
+                   const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s) {
   const uint32_t ktiles = uint32_t((L.K + 31) / 32);
-  DwArgs a{q.pcq_codes, q.pcq_kept, q.pcq_count, q.pcq_scale, q.pcq_offset, xsign, dW, I_out,
-           uint32_t(L.D), uint32_t(L.K), uint32_t(L.R), uint32_t(L.Wr), ktiles,
-           cfg.bits == 8 ? 1 : 0};
-  // Capacity tiles plus a pool of blocks that only zero pruned rows: whatever the device-side
-  // count, at least `zb` blocks are left for the zeroing.
-  const int64_t zb = std::min<int64_t>(256, L.D);
-  const dim3 grid(unsigned(ktiles * ((L.D + 31) / 32) + zb));
-  hipLaunchKernelGGL(k_mfma_dw, grid, dim3(DW_THREADS), 0, s, a);
+  const uint32_t S = uint32_t(gemm_dw_splits(L));
+  DwArgs a;
+  a.codes = q.pcq_codes; a.kept = q.pcq_kept; a.count = q.pcq_count;
+  a.scale = q.pcq_scale; a.offset = q.pcq_offset; a.xsign = xsign;
+  a.dW = dW; a.I_out = I_out;
+  a.part = static_cast<int32_t *>(ws);
+  a.partT = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
+                                        align256(size_t(S) * L.D * L.K * 4));
+  a.D = uint32_t(L.D); a.K = uint32_t(L.K); a.R = uint32_t(L.R);
+  a.Rp = uint32_t(L.Wr * 64); a.Wr = uint32_t(L.Wr); a.ktiles = ktiles;
+  a.codes_bytes = uint32_t(L.D * L.Wr * 64);
+  a.xsign_bytes = uint32_t(L.Wr * L.K * 8);
+  a.S = S; a.wps = uint32_t((L.Wr + S - 1) / S);
+  a.divS = make_fastdiv(S); a.divKt = make_fastdiv(ktiles); a.divK = make_fastdiv(uint32_t(L.K));
+  const int64_t groups = (L.D + DW_RT * 32 - 1) / (DW_RT * 32);
+  const dim3 grid(unsigned(int64_t(S) * groups * ktiles));
+  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
+  if (cfg.bits == 8) {
+    hipLaunchKernelGGL(k_mfma_dw_part<true>, grid, dim3(DW_THREADS), 0, s, a);
+    hipLaunchKernelGGL(k_dw_finish<true>, fgrid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(k_mfma_dw_part<false>, grid, dim3(DW_THREADS), 0, s, a);
+    hipLaunchKernelGGL(k_dw_finish<false>, fgrid, dim3(256), 0, s, a);
+  }
   return last_launch_status();
 }
 
 int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *wsign, void *dX, int32_t *I_out, hipStream_t s) {
+                   const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
+                   hipStream_t s) {
   if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
   DxArgs a;
   a.codes = q.psq_codes; a.kept = q.psq_kept; a.count = q.psq_count;
-  a.scale = q.psq_scale; a.offset = q.psq_offset; a.wsign = wsign;
+  a.scale = q.psq_scale; a.offset = q.psq_offset; a.wsb = wsb; a.wlsum = wlsum;
   a.dX = dX; a.I_out = I_out; a.dx_t = L.dx_t;
   a.N = uint32_t(L.N); a.C = uint32_t(L.C); a.H = uint32_t(L.H); a.W = uint32_t(L.W);
   a.HW = uint32_t(L.HW); a.Ho = uint32_t(L.Ho); a.Wo = uint32_t(L.Wo); a.P = uint32_t(L.P);
-  a.D = uint32_t(L.D); a.Wd = uint32_t(L.Wd);
+  a.R = uint32_t(L.R); a.Dp = uint32_t(L.Wd * 64);
   a.ctiles = uint32_t((L.C + 31) / 32);
   a.CHW = uint32_t(L.C * L.HW);
+  a.taps = uint32_t(L.kh * L.kw);
+  a.nch = a.Dp / 32;
+  a.codes_bytes = uint32_t(L.R * L.Wd * 64);
+  a.wsb_bytes = uint32_t(L.K * L.Wd * 64);
   a.kh = L.kh; a.kw = L.kw; a.sh = L.sh; a.sw = L.sw; a.ph = L.ph; a.pw = L.pw;
   a.divHW = make_fastdiv(uint32_t(L.HW)); a.divW = make_fastdiv(uint32_t(L.W));
-  a.divWd = make_fastdiv(uint32_t(L.Wd));
-  a.bits8 = cfg.bits == 8 ? 1 : 0;
+  a.divKw = make_fastdiv(uint32_t(L.kw)); a.divNch = make_fastdiv(a.nch);
+  a.divCt = make_fastdiv(a.ctiles);
   const int64_t zb = std::min<int64_t>(256, L.N);
   const dim3 grid(unsigned(((L.N * L.HW + 31) / 32) * a.ctiles + zb));
-  hipLaunchKernelGGL(k_mfma_dx, grid, dim3(DX_THREADS), 0, s, a);
+  const uint32_t per_wave = (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
+  auto go = [&]<bool B8>() {
+    if (per_wave <= 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (per_wave <= 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (per_wave <= 12) hipLaunchKernelGGL((k_mfma_dx<B8, 12>), grid, dim3(DX_THREADS), 0, s, a);
+    else hipLaunchKernelGGL((k_mfma_dx<B8, 20>), grid, dim3(DX_THREADS), 0, s, a);
+  };
+  if (cfg.bits == 8) go.template operator()<true>();
+  else go.template operator()<false>();
   return last_launch_status();
 }
 

@@ -78,11 +78,15 @@ inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
                     const QuantWs &w, hipStream_t s);
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
-                     const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s);
+                     const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s,
+                     bool word_major = false);
+size_t gemm_dw_ws_bytes(const Layer &L);
 int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *xsign, float *dW, int32_t *I_out, hipStream_t s);
+                   const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s);
+int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, hipStream_t s);
 int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *wsign, void *dX, int32_t *I_out, hipStream_t s);
+                   const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
+                   hipStream_t s);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }

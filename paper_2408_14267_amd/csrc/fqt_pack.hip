@@ -27,8 +27,9 @@ __global__ __launch_bounds__(THREADS) void k_pack_along_cols(const void *__restr
   if (lane == 0) dst[i * nw + w] = m;
 }
 
-// Down the rows (transposing): 64x64 tile staged in LDS, read back column-wise.
-template <int DT>
+// Down the rows (transposing): 64x64 tile staged in LDS, read back column-wise.  WM: the
+// output is word-major, word w of line c at w * cols + c (the layout the dW product reads).
+template <int DT, bool WM>
 __global__ __launch_bounds__(THREADS) void k_pack_along_rows(const void *__restrict__ src,
                                                              int64_t rows,
                                                              int64_t cols, int64_t ld,
@@ -54,7 +55,7 @@ __global__ __launch_bounds__(THREADS) void k_pack_along_rows(const void *__restr
     const int64_t c = c0 + cc;
     if (c >= cols) break;
     const uint64_t m = __ballot(bits[lane][cc] != 0);
-    if (lane == 0) dst[c * nw + (r0 >> 6)] = m;
+    if (lane == 0) dst[WM ? (r0 >> 6) * cols + c : c * nw + (r0 >> 6)] = m;
   }
 }
 
@@ -71,8 +72,9 @@ constexpr int IM2COL_CPW = 4;   // channels per wave sharing one index decomposi
 // (n, ho, wo) of IM2COL_CPW channels: one index decomposition per lane serves every
 // channel and kernel tap.  The words of a channel's taps are gathered into lanes
 // 0..taps-1 and stored by one instruction.  KH, KW > 0 fix the kernel size at compile
-// time (fully unrolled); 0 reads it from the geometry.
-template <int DT, int KH, int KW>
+// time (fully unrolled); 0 reads it from the geometry.  WM: word-major output, word w of
+// line l at w * C*kh*kw + l (the layout the dW product reads).
+template <int DT, int KH, int KW, bool WM>
 __global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict__ x, Im2colGeom g,
                                                          uint64_t *__restrict__ dst) {
   const int lane = threadIdx.x & 63;
@@ -113,7 +115,9 @@ __global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict_
           const uint64_t m = __ballot(ok && v[i * KW + j] > 0.0f);
           if (lane == i * KW + j) mine = m;
         }
-      if (lane < KH * KW) dst[(size_t(c) * (KH * KW) + lane) * g.nw + w] = mine;
+      if (lane < KH * KW)
+        dst[WM ? size_t(w) * g.C * (KH * KW) + size_t(c) * (KH * KW) + lane
+               : (size_t(c) * (KH * KW) + lane) * g.nw + w] = mine;
     } else {
       for (int t0 = 0; t0 < taps; t0 += 16) {
         int ti = t0 / kw, tj = t0 - ti * kw;
@@ -134,7 +138,9 @@ __global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict_
           const uint64_t m = __ballot(((okm >> u) & 1u) && v[u] > 0.0f);
           if (lane == u) mine = m;
         }
-        if (lane < 16 && t0 + lane < taps) dst[(size_t(c) * taps + t0 + lane) * g.nw + w] = mine;
+        if (lane < 16 && t0 + lane < taps)
+          dst[WM ? size_t(w) * g.C * taps + size_t(c) * taps + t0 + lane
+                 : (size_t(c) * taps + t0 + lane) * g.nw + w] = mine;
       }
     }
   }
@@ -155,10 +161,72 @@ __global__ __launch_bounds__(THREADS) void k_linesum(const uint64_t *__restrict_
 
 unsigned blocks_for(int64_t items) { return unsigned((items + WAVES - 1) / WAVES); }
 
+// sign(W) as signed bytes for the int8 dX product (Section 5.1 binarizer; the +-1 form of
+// Appendix C's {0,1} <-> {+-1} conversion).  W is viewed as [D][K] (K = C*kh*kw, line
+// l = (c, tap)); byte d of line l is +1 if W[d][l] > 0 else -1 for d < D, 0 for
+// D <= d < Dp, stored chunk-major at ((d/32 * taps + tap) * C + c) * 32 + d % 32 so that the
+// 32-byte chunks of consecutive channels are adjacent; lsum[l] = sum over d < D of the
+// line.  One block per 64 lines walks D in 64-row tiles, transposed through LDS (pitch 68
+// bytes = 17 dwords: the column writes of a wave spread over the banks).
+constexpr int WB_PITCH = 68;
+template <int DT>
+__global__ __launch_bounds__(THREADS) void k_pack_w_i8(const void *__restrict__ w, uint32_t D,
+                                                       uint32_t K, uint32_t Dp, uint32_t C,
+                                                       uint32_t taps, FastDiv div_taps,
+                                                       int8_t *__restrict__ dst,
+                                                       int32_t *__restrict__ lsum) {
+  __shared__ int8_t tile[64][WB_PITCH];
+  __shared__ int32_t pos[64];
+  const int t = threadIdx.x, line = t & 63, q = t >> 6;
+  const uint32_t l0 = blockIdx.x * 64, l = l0 + line;
+  if (t < 64) pos[t] = 0;
+  int mine = 0;
+  for (uint32_t d0 = 0; d0 < Dp; d0 += 64) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {   // unconditional loads (element 0 outside) issue back to back
+      const uint32_t d = d0 + 4 * k + q;
+      v[k] = load_elem<DT>(w, (d < D && l < K) ? int64_t(d) * K + l : 0);
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const uint32_t d = d0 + 4 * k + q;
+      const bool in = d < D && l < K;
+      const bool pos_sign = in && v[k] > 0.0f;
+      mine += pos_sign ? 1 : 0;
+      tile[line][4 * k + q] = in ? (pos_sign ? int8_t(1) : int8_t(-1)) : int8_t(0);
+    }
+    __syncthreads();
+    const int wl = t >> 2, part = t & 3;
+    if (l0 + wl < K) {
+      const uint32_t lw = l0 + wl, c = fdiv(lw, div_taps), tap = lw - c * taps;
+      const uint32_t chunk = (d0 >> 5) + (part >> 1);
+      const uint32_t *src = reinterpret_cast<const uint32_t *>(&tile[wl][16 * part]);
+      *reinterpret_cast<uint4 *>(dst + ((size_t(chunk) * taps + tap) * C + c) * 32 +
+                                 16 * (part & 1)) = make_uint4(src[0], src[1], src[2], src[3]);
+    }
+    __syncthreads();
+  }
+  atomicAdd(&pos[line], mine);
+  __syncthreads();
+  if (t < 64 && l0 + t < K) lsum[l0 + t] = 2 * pos[t] - int(D);
+}
+
 }  // namespace
 
+int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, hipStream_t s) {
+  const uint32_t D = uint32_t(L.D), K = uint32_t(L.K), Dp = uint32_t(L.Wd * 64);
+  const uint32_t taps = uint32_t(L.kh * L.kw);
+  dispatch_dtype(L.w_t, [&]<int DT>() {
+    hipLaunchKernelGGL(k_pack_w_i8<DT>, dim3(unsigned((L.K + 63) / 64)), dim3(THREADS), 0, s, W,
+                       D, K, Dp, uint32_t(L.C), taps, make_fastdiv(taps), dst, lsum);
+  });
+  return last_launch_status();
+}
+
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
-                     const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s) {
+                     const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s,
+                     bool word_major) {
   int64_t lines, nw, len;
   if (axis == FQT_PACK_ALONG_COLS) {
     nw = (cols + 63) / 64;
@@ -173,8 +241,13 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     lines = cols;
     len = rows;
     dispatch_dtype(dtype, [&]<int DT>() {
-      hipLaunchKernelGGL(k_pack_along_rows<DT>, dim3(unsigned((cols + 63) / 64), unsigned(nw)),
-                         dim3(THREADS), 0, s, src, rows, cols, ld, dst);
+      const dim3 grid(unsigned((cols + 63) / 64), unsigned(nw));
+      if (word_major)
+        hipLaunchKernelGGL((k_pack_along_rows<DT, true>), grid, dim3(THREADS), 0, s, src, rows,
+                           cols, ld, dst);
+      else
+        hipLaunchKernelGGL((k_pack_along_rows<DT, false>), grid, dim3(THREADS), 0, s, src, rows,
+                           cols, ld, dst);
     });
   } else {
     const Layer &L = *conv;
@@ -187,19 +260,23 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     lines = L.K;
     len = L.R;
     const dim3 grid(blocks_for(int64_t(cgroups) * L.Wr));
-    dispatch_dtype(dtype, [&]<int DT>() {
+    auto go = [&]<int DT, bool WM>() {
       if (L.kh == 1 && L.kw == 1)
-        hipLaunchKernelGGL((k_pack_im2col<DT, 1, 1>), grid, dim3(THREADS), 0, s, src, g, dst);
+        hipLaunchKernelGGL((k_pack_im2col<DT, 1, 1, WM>), grid, dim3(THREADS), 0, s, src, g, dst);
       else if (L.kh == 3 && L.kw == 3)
-        hipLaunchKernelGGL((k_pack_im2col<DT, 3, 3>), grid, dim3(THREADS), 0, s, src, g, dst);
+        hipLaunchKernelGGL((k_pack_im2col<DT, 3, 3, WM>), grid, dim3(THREADS), 0, s, src, g, dst);
       else if (L.kh == 7 && L.kw == 7)
-        hipLaunchKernelGGL((k_pack_im2col<DT, 7, 7>), grid, dim3(THREADS), 0, s, src, g, dst);
+        hipLaunchKernelGGL((k_pack_im2col<DT, 7, 7, WM>), grid, dim3(THREADS), 0, s, src, g, dst);
       else
-        hipLaunchKernelGGL((k_pack_im2col<DT, 0, 0>), grid, dim3(THREADS), 0, s, src, g, dst);
+        hipLaunchKernelGGL((k_pack_im2col<DT, 0, 0, WM>), grid, dim3(THREADS), 0, s, src, g, dst);
+    };
+    dispatch_dtype(dtype, [&]<int DT>() {
+      if (word_major) go.template operator()<DT, true>();
+      else go.template operator()<DT, false>();
     });
   }
   if (last_launch_status() != FQT_OK) return FQT_E_HIP;
-  if (linesum) {
+  if (linesum && !word_major) {
     hipLaunchKernelGGL(k_linesum, dim3(blocks_for(lines)), dim3(THREADS), 0, s, dst, lines, nw,
                        len, linesum);
     return last_launch_status();

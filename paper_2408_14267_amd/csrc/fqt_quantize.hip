@@ -459,8 +459,8 @@ struct QPackArgs {
   const GroupParam *cp;
   uint64_t *psq;        // [bits][R][Wd]
   uint64_t *pcq;        // [bits][D][Wr]
-  uint8_t *psq_codes;   // [R][Wd*64]
-  uint8_t *pcq_codes;   // [D][Wr*64]
+  uint8_t *psq_codes;   // [2*Wd][R][32]  chunk-major: byte d of row r at ((d/32)*R + r)*32 + d%32
+  uint8_t *pcq_codes;   // [2*Wr][D][32]  byte r of kept channel j at ((r/32)*D + j)*32 + r%32
   uint32_t Wd, Wr;
   int bits;
   uint64_t seed;
@@ -575,8 +575,9 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
       const uint64_t m = __ballot((code >> p) & 1u);
       if (lane == p) a.pcq[(size_t(p) * g.D + rank) * a.Wr + (r0 >> 6)] = m;
     }
-    if (lane < 16)
-      reinterpret_cast<uint32_t *>(a.pcq_codes + size_t(rank) * a.Wr * 64 + r0)[lane] =
+    if (lane < 16)        // lanes 0-7 fill 32-byte chunk r0/32, lanes 8-15 the next one
+      *reinterpret_cast<uint32_t *>(
+          a.pcq_codes + ((size_t(r0 >> 5) + (lane >> 3)) * g.D + rank) * 32 + 4 * (lane & 7)) =
           reinterpret_cast<const uint32_t *>(&cc[dd][0])[lane];
   }
   // PSQ: row rr of the tile, lanes along d (row encoder) and its 64 code bytes.
@@ -590,7 +591,8 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
       if (lane == p) a.psq[(size_t(p) * g.R + row) * a.Wd + (d0 >> 6)] = m;
     }
     if (lane < 16)
-      reinterpret_cast<uint32_t *>(a.psq_codes + size_t(row) * a.Wd * 64 + d0)[lane] =
+      *reinterpret_cast<uint32_t *>(
+          a.psq_codes + ((size_t(d0 >> 5) + (lane >> 3)) * g.R + row) * 32 + 4 * (lane & 7)) =
           reinterpret_cast<const uint32_t *>(&cs[rr][0])[lane];
   }
 }

@@ -21,11 +21,13 @@ FQT_F32, FQT_BF16 = 0, 1
 FQT_LINEAR, FQT_CONV2D = 0, 1
 FQT_AGP_BERNOULLI, FQT_AGP_TOPK, FQT_AGP_OFF = 0, 1, 2
 FQT_PACK_ALONG_ROWS, FQT_PACK_ALONG_COLS, FQT_PACK_IM2COL = 0, 1, 2
-FQT_WS_QUANTIZE, FQT_WS_LAYER = 0, 1
+FQT_WS_QUANTIZE, FQT_WS_LAYER, FQT_WS_GEMM_DW = 0, 1, 2
 FQT_MAX_BITS = 8
 FQT_MAX_AGP_GROUPS = 16384
 EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_agp_scq_quantize",
-            "fqt_pack_bits", "fqt_binary_gemm_dw", "fqt_binary_gemm_dx", "fqt_layer_backward")
+            "fqt_pack_bits", "fqt_pack_input_signs", "fqt_binary_gemm_dw", "fqt_pack_weight_signs",
+            "fqt_binary_gemm_dx",
+            "fqt_layer_backward")
 
 
 class FqtError(RuntimeError):
@@ -70,8 +72,12 @@ def _load():
         "fqt_agp_scq_quantize": (c_int, [D, Q, c_void_p, G, c_void_p, c_size_t, c_void_p]),
         "fqt_pack_bits": (c_int, [c_void_p, c_int32, c_int64, c_int64, c_int64, c_int32, D,
                                   c_void_p, c_void_p, c_void_p]),
-        "fqt_binary_gemm_dw": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p]),
-        "fqt_binary_gemm_dx": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dw": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                       c_void_p]),
+        "fqt_pack_input_signs": (c_int, [D, c_void_p, c_void_p, c_void_p]),
+        "fqt_pack_weight_signs": (c_int, [D, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "fqt_binary_gemm_dx": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p,
+                                       c_void_p]),
         "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
     }
@@ -153,14 +159,26 @@ def fqt_pack_bits(src, dtype, rows, cols, ld, axis, conv, dst, linesum=None, str
                               _ptr(dst), _ptr(linesum), _stream(stream)), "fqt_pack_bits")
 
 
-def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, I_out=None, stream=None):
+def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, ws, I_out=None, stream=None):
     _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign), _ptr(dW),
-                                   _ptr(I_out), _stream(stream)), "fqt_binary_gemm_dw")
+                                   _ptr(I_out), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream(stream)), "fqt_binary_gemm_dw")
 
 
-def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, dX, I_out=None, stream=None):
-    _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign), _ptr(dX),
-                                   _ptr(I_out), _stream(stream)), "fqt_binary_gemm_dx")
+def fqt_pack_input_signs(desc, X, dst, stream=None):
+    _check(_lib.fqt_pack_input_signs(desc, _ptr(X), _ptr(dst), _stream(stream)),
+           "fqt_pack_input_signs")
+
+
+def fqt_pack_weight_signs(desc, W, dst, linesum, stream=None):
+    _check(_lib.fqt_pack_weight_signs(desc, _ptr(W), _ptr(dst), _ptr(linesum), _stream(stream)),
+           "fqt_pack_weight_signs")
+
+
+def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, wsign_linesum, dX, I_out=None, stream=None):
+    _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign),
+                                   _ptr(wsign_linesum), _ptr(dX), _ptr(I_out), _stream(stream)),
+           "fqt_binary_gemm_dx")
 
 
 def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):

@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 8
+    assert len(names) == 10
     lib = ctypes.CDLL(fqt.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -105,5 +105,10 @@ def test_null_and_small_workspace_rejected_before_launch():
     assert st == fqt.FQT_E_NULL
     q = fqt.fqt_qgrad()
     st = lib.fqt_binary_gemm_dw(ctypes.byref(d), ctypes.byref(c), ctypes.byref(q), fake, fake,
-                                None, None)
+                                None, fake, 1 << 30, None)
     assert st == fqt.FQT_E_NULL
+    st = lib.fqt_pack_weight_signs(ctypes.byref(d), fake, fake, None, None)
+    assert st == fqt.FQT_E_NULL
+    st = lib.fqt_pack_weight_signs(ctypes.byref(d), fake, ctypes.c_void_p((1 << 20) + 8), fake,
+                                   None)
+    assert st == fqt.FQT_E_ALIGN            # the sign bytes must be 16-byte aligned

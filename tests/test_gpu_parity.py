@@ -97,6 +97,11 @@ def _run_case(layer, bits, mode, recipe, dtype, seed=0, step=3, layer_id=5, data
     return fqt, ref, desc, cfg, X, W, dY
 
 
+def _rows_of_chunks(t, rows, chunks):
+    """[chunks][rows][32] bytes on the device -> [rows][32 * chunks] on the host."""
+    return t.cpu().numpy().reshape(chunks, rows, 32).transpose(1, 0, 2).reshape(rows, 32 * chunks)
+
+
 def _check_quantize(fqt, ref, desc, cfg, dY, layer, bits):
     q = fqt.QGrad(desc, cfg)
     ws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE)
@@ -120,8 +125,9 @@ def _check_quantize(fqt, ref, desc, cfg, dY, layer, bits):
     pcq = _u64(q.pcq_planes).reshape(bits, D, Wr)[:, :kc]
     assert np.array_equal(psq, ref.qgrad.psq_planes), "psq planes"
     assert np.array_equal(pcq, ref.qgrad.pcq_planes), "pcq planes"
-    psq_codes = q.psq_codes.cpu().numpy().reshape(R, Wd * 64)[:ks * P]
-    pcq_codes = q.pcq_codes.cpu().numpy().reshape(D, Wr * 64)[:kc]
+    # Code arrays are chunk-major ([32-byte chunk][row][32]); back to rows for the check.
+    psq_codes = _rows_of_chunks(q.psq_codes, R, 2 * Wd)[:ks * P]
+    pcq_codes = _rows_of_chunks(q.pcq_codes, D, 2 * Wr)[:kc]
     assert np.array_equal(psq_codes[:, :D], ref.qgrad.psq_rows), "psq codes"
     assert not psq_codes[:, D:].any(), "psq code padding"
     assert np.array_equal(pcq_codes[:, :R], ref.qgrad.pcq_rows), "pcq codes"
@@ -142,12 +148,28 @@ def _check_signs(fqt, ref, desc, layer, X, W, x_dt):
     else:
         fqt.fqt_pack_bits(X, x_dt, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc, xs, xsum)
     fqt.fqt_pack_bits(W, fqt.FQT_F32, layer.D, K, K, fqt.FQT_PACK_ALONG_ROWS, None, ws_, wsum)
+    wsb = torch.empty(K, 64 * Wd, dtype=torch.int8, device="cuda")
+    wlsum = torch.empty(K, dtype=torch.int32, device="cuda")
+    fqt.fqt_pack_weight_signs(desc, W, wsb, wlsum)
+    xwm = torch.empty(Wr, K, dtype=torch.int64, device="cuda")
+    fqt.fqt_pack_input_signs(desc, X, xwm)
     torch.cuda.synchronize()
+    # The dW operand: the same im2col bits, word-major.
+    assert np.array_equal(_u64(xwm), ofqt.pack_words(ref.xbits).T), "x sign words (word-major)"
     assert np.array_equal(_u64(xs).reshape(K, Wr), ofqt.pack_words(ref.xbits)), "x sign bits"
     assert np.array_equal(_u64(ws_).reshape(K, Wd), ofqt.pack_words(ref.wbits)), "w sign bits"
     assert np.array_equal(xsum.cpu().numpy(), ref.xsign_colsum), "x line sums"
     assert np.array_equal(wsum.cpu().numpy(), ref.wsign_colsum), "w line sums"
-    return xs, xsum, ws_, wsum
+    # The +-1 byte form of sign(W): the oracle's sign bits as +1 / -1, zero past D, stored
+    # [32-byte chunk of D][tap][channel][32].
+    taps = layer.kh * layer.kw
+    want = np.zeros((K, 64 * Wd), dtype=np.int8)
+    want[:, :layer.D] = np.where(ref.wbits, 1, -1)
+    want = want.reshape(layer.C, taps, 2 * Wd, 32).transpose(2, 1, 0, 3)
+    assert np.array_equal(wsb.cpu().numpy().reshape(2 * Wd, taps, layer.C, 32), want), \
+        "w sign bytes"
+    assert np.array_equal(wlsum.cpu().numpy(), ref.wsign_colsum), "w sign-byte line sums"
+    return xwm, xsum, wsb, wlsum
 
 
 @pytest.mark.parametrize("name,layer,bits,mode,recipe,dtype", CASES, ids=[c[0] for c in CASES])
@@ -156,15 +178,15 @@ def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
     fqt, ref, desc, cfg, X, W, dY = _run_case(layer, bits, mode, recipe, dtype)
     x_dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
     q = _check_quantize(fqt, ref, desc, cfg, dY, layer, bits)
-    xs, xsum, ws_, wsum = _check_signs(fqt, ref, desc, layer, X, W, x_dt)
+    xs, xsum, wsb, wlsum = _check_signs(fqt, ref, desc, layer, X, W, x_dt)
 
     D, K = layer.D, layer.C * layer.kh * layer.kw
     dW = torch.empty(D, K, dtype=torch.float32, device="cuda")
     I_dw = torch.empty(D, K, dtype=torch.int32, device="cuda")
-    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, I_dw)
+    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW), I_dw)
     dX = torch.empty(X.shape, dtype=X.dtype, device="cuda")
     I_dx = torch.empty(layer.N, layer.C, layer.H, layer.W, dtype=torch.int32, device="cuda")
-    fqt.fqt_binary_gemm_dx(desc, cfg, q, ws_, dX, I_dx)
+    fqt.fqt_binary_gemm_dx(desc, cfg, q, wsb, wlsum, dX, I_dx)
     torch.cuda.synchronize()
     assert np.array_equal(I_dw.cpu().numpy(), ref.I_dw), "dW integer product"
     assert np.array_equal(I_dx.cpu().numpy(), ref.I_dx), "dX integer product"
