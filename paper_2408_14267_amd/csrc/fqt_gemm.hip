@@ -130,6 +130,48 @@ constexpr int DW_WAVES = 4;
 constexpr int DW_THREADS = DW_WAVES * 64;
 constexpr int DW_PREF = 2;                  // 64-bit words of the contraction loaded per batch
 
+// The contraction of one wave for NRT live slot tiles: words c0, c0 + DW_WAVES, ... below
+// w_end, DW_PREF words per batch.  Every batch issues all its loads before the first
+// product (a sched_barrier keeps the compiler from sinking them), so a batch costs one
+// memory latency; words past w_end are skipped by a uniform test.
+template <int NRT, bool B8>
+__device__ __forceinline__ void dw_accumulate(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
+                                              __amdgpu_buffer_rsrc_t xrs,
+                                              const uint32_t (&aoff)[DW_RT], uint32_t boff,
+                                              uint32_t c_first, uint32_t w_end, int g,
+                                              v16i (&acc)[DW_RT], uint32_t &tpart) {
+  const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
+  for (uint32_t c0 = c_first; c0 < w_end; c0 += DW_WAVES * DW_PREF) {
+    uint64_t word[DW_PREF];
+    v4i A[DW_PREF][2][NRT];
+#pragma unroll
+    for (int u = 0; u < DW_PREF; ++u) {
+      // Past the split's last word the loads read word c0 again (in bounds).
+      const uint32_t c = c0 + u * DW_WAVES < w_end ? c0 + u * DW_WAVES : c0;
+      word[u] = load8(xrs, boff, c * a.K * 8);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt)
+          A[u][h][rt] = load16(crs, aoff[rt], (2 * c + h) * chunk_bytes);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < DW_PREF; ++u) {
+      if (c0 + u * DW_WAVES >= w_end) break;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t bits = uint32_t(word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
+        tpart += __popc(bits);
+        const v4i B = signs16(bits);
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt)
+          acc[rt] = mfma_i8(B8 ? bias128(A[u][h][rt]) : A[u][h][rt], B, acc[rt]);
+      }
+    }
+  }
+}
+
 // Split-R partial products.  Grid: S splits x ceil(D/128) slot groups x ceil(K/32) column
 // tiles over the slot capacity, the split index fastest (consecutive blocks land on
 // different XCDs, so each XCD reads its own slices of the codes and of the signs).  A block
@@ -166,41 +208,17 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
   const bool b_ok = kc < a.K;
   const uint32_t boff = b_ok ? kc * 8 : BUF_NONE;
   const uint32_t w_end = min(a.Wr, (sp + 1) * a.wps);
-  const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
+  const uint32_t c_first = sp * a.wps + wave;
 
   v16i acc[DW_RT];
 #pragma unroll
   for (int rt = 0; rt < DW_RT; ++rt) acc[rt] = v16i{0};
   uint32_t tpart = 0;
-  for (uint32_t c0 = sp * a.wps + wave; c0 < w_end; c0 += DW_WAVES * DW_PREF) {
-    uint64_t word[DW_PREF];
-    v4i A[DW_PREF][2][DW_RT];
-#pragma unroll
-    for (int u = 0; u < DW_PREF; ++u) {
-      // Past the split's last word the loads read word c0 again (in bounds); the products
-      // of those words are skipped below.
-      const uint32_t c = c0 + u * DW_WAVES < w_end ? c0 + u * DW_WAVES : c0;
-      word[u] = load8(xrs, boff, c * a.K * 8);
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int rt = 0; rt < DW_RT; ++rt)
-          A[u][h][rt] = rt < nrt ? load16(crs, aoff[rt], (2 * c + h) * chunk_bytes)
-                                 : v4i{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int u = 0; u < DW_PREF; ++u) {
-      if (c0 + u * DW_WAVES >= w_end) break;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint32_t bits = uint32_t(word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
-        tpart += __popc(bits);
-        const v4i B = signs16(bits);
-#pragma unroll
-        for (int rt = 0; rt < DW_RT; ++rt)
-          if (rt < nrt) acc[rt] = mfma_i8(B8 ? bias128(A[u][h][rt]) : A[u][h][rt], B, acc[rt]);
-      }
-    }
+  switch (nrt) {
+    case 1: dw_accumulate<1, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
+    case 2: dw_accumulate<2, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
+    case 3: dw_accumulate<3, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
+    default: dw_accumulate<4, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
   }
   __syncthreads();                      // tred is initialised
   atomicAdd(&tred[i], int(tpart));
@@ -215,17 +233,20 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
   __syncthreads();
   if (wave != 0 || !b_ok) return;
   if (g == 0) a.partT[size_t(sp) * a.K + kc] = tred[i];
+  int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.K + kc;
 #pragma unroll
   for (int rt = 0; rt < DW_RT; ++rt) {
     if (rt >= nrt) break;
+    // All partial sums first (the LDS reads issue back to back), then the stores.
+#pragma unroll
+    for (int w = 0; w < DW_WAVES - 1; ++w)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[rt][v] += red[w][rt][v][lane];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = 32 * rt + acc_row(v, g);
-      if (int(j0) + row >= count) continue;
-      int s = acc[rt][v];
-#pragma unroll
-      for (int w = 0; w < DW_WAVES - 1; ++w) s += red[w][rt][v][lane];
-      a.part[(size_t(sp) * a.D + j0 + row) * a.K + kc] = s;
+      if (int(j0) + row < count) out[size_t(row) * a.K] = acc[rt][v];
     }
   }
 }
@@ -365,21 +386,22 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
   const uint32_t steps = a.taps * a.nch;
   v16i acc = {0};
   for (uint32_t s0 = wave; s0 < steps; s0 += DX_WAVES * NB) {
+    // All NB steps' loads issue before the first product (one memory latency per batch);
+    // a step past the end reads zeros through its A operand and adds nothing.
     v4i A[NB], B[NB];
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
-      // Steps past the end load step 0 again (in bounds); their products are skipped.
-      const uint32_t st = s0 + u * DX_WAVES < steps ? s0 + u * DX_WAVES : 0;
+      const uint32_t st0 = s0 + u * DX_WAVES;
+      const bool live = st0 < steps;
+      const uint32_t st = live ? st0 : 0;
       const uint32_t tap = fdiv(st, a.divNch);
       const uint32_t kc = st - tap * a.nch;
-      A[u] = load16(ars, abase, (kc * a.taps + tap) * a.C * 32);
+      A[u] = load16(ars, live ? abase : BUF_NONE, (kc * a.taps + tap) * a.C * 32);
       B[u] = load16(brs, rowoff[tap][i] + 16 * g, kc * a.R * 32);
     }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
-      if (s0 + u * DX_WAVES >= steps) break;
-      acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
-    }
+    for (int u = 0; u < NB; ++u) acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
   }
 
   // Zero-point term over this wave's taps: c[ch][pixel] = sum of wlsum[ch][tap] over the
@@ -413,6 +435,7 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
   const int off = pix_out[i];
   if (off < 0) return;                    // rows past the count belong to the zero blocks
   const float S = pix_s[i], Z = pix_z[i];
+  __builtin_amdgcn_sched_barrier(0);      // every LDS read above issues before the stores
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int crow = acc_row(v, g);
@@ -491,10 +514,10 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   const dim3 grid(unsigned(((L.N * L.HW + 31) / 32) * a.ctiles + zb));
   const uint32_t per_wave = (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
   auto go = [&]<bool B8>() {
+    // Batches of at most 10 steps keep the kernel at three resident blocks per CU.
     if (per_wave <= 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4>), grid, dim3(DX_THREADS), 0, s, a);
     else if (per_wave <= 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8>), grid, dim3(DX_THREADS), 0, s, a);
-    else if (per_wave <= 12) hipLaunchKernelGGL((k_mfma_dx<B8, 12>), grid, dim3(DX_THREADS), 0, s, a);
-    else hipLaunchKernelGGL((k_mfma_dx<B8, 20>), grid, dim3(DX_THREADS), 0, s, a);
+    else hipLaunchKernelGGL((k_mfma_dx<B8, 10>), grid, dim3(DX_THREADS), 0, s, a);
   };
   if (cfg.bits == 8) go.template operator()<true>();
   else go.template operator()<false>();

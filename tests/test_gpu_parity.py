@@ -224,6 +224,42 @@ def test_full_vgg_cifar_conv_layer():
     assert 0 < ref.qgrad.samples.count < layer.N and 0 < ref.qgrad.channels.count < layer.D
 
 
+def test_layer_backward_graph_replays_match_eager():
+    """fqt_layer_backward captured in a HIP graph (forked second stream included) and
+    replayed several times, with eager calls on other data and synchronizations between
+    the replays: every replay equals the eager result bit for bit."""
+    wl = WORKLOADS["resnet18_32px"]
+    layer = wl.layers[3]
+    _announce(f"[gpu parity] graph replay {layer}")
+    fqt = _fqt()
+    desc = fqt.layer_desc(layer)
+    cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, 11, 2, 1)
+    X, W, dY = (_to_dev(a, "f32") for a in draw_layer(layer, wl.recipe, 1, "f32"))
+    X2, W2, dY2 = (_to_dev(a, "f32") for a in draw_layer(layer, wl.recipe, 2, "f32"))
+    ws, ws2 = fqt.workspace(desc, cfg), fqt.workspace(desc, cfg)
+    dX_e, dW_e = torch.empty_like(X), torch.empty_like(W)
+    fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX_e, dW_e, ws)
+    torch.cuda.synchronize()
+    dX_g, dW_g = torch.empty_like(X), torch.empty_like(W)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX_g, dW_g, ws, side)
+    torch.cuda.synchronize()
+    dX_o, dW_o = torch.empty_like(X2), torch.empty_like(W2)
+    for r in range(3):
+        dX_g.fill_(7.0)
+        dW_g.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dX_g.view(torch.int32), dX_e.view(torch.int32)), f"replay {r} dX"
+        assert torch.equal(dW_g.view(torch.int32), dW_e.view(torch.int32)), f"replay {r} dW"
+        fqt.fqt_layer_backward(desc, cfg, X2, W2, dY2, dX_o, dW_o, ws2)   # eager work between
+        torch.cuda.synchronize()
+
+
 def test_all_zero_gradient():
     fqt = _fqt()
     layer = LayerShape("c", "conv2d", 4, 8, 16, 6, 6, 3, 3, 1, 1, 1, 1)
