@@ -32,8 +32,8 @@ struct LayerWs {
 };
 
 void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
-  q->part_c = c->take<int2>(size_t(L.D) * L.Wr);
-  q->part_s = c->take<int2>(size_t(L.Wd) * L.R);
+  q->part_c = c->take<int2>(size_t(L.D) * stats_row_blocks(L));
+  q->part_s = c->take<int2>(size_t(L.Wd) * L.Wr * stats_slots(L));
   q->skey = c->take<int2>(L.N);
   q->ckey = c->take<int2>(L.D);
   q->sp = c->take<GroupParam>(L.N);

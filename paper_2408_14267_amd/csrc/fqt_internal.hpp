@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <climits>
 #include <stdint.h>
 
 #include "fqt.h"
@@ -37,8 +38,9 @@ struct GroupParam {
 // Quantize workspace: per-tile partial min/max keys, the reduced keys of both group
 // sets, and the per-group parameters of the quantizer.
 struct QuantWs {
-  int2 *part_c;            // [D][ceil(R/64)]   channel partials of each 64-row tile
-  int2 *part_s;            // [ceil(D/64)][R]   row partials of each 64-channel tile
+  int2 *part_c;            // [stats_row_blocks][D]  channel partials of each row block
+  int2 *part_s;            // [ceil(D/64)][ceil(R/64)][stats_slots]  sample partials of
+                           //   each 64 x 64 tile, one slot per sample the tile meets
   int2 *skey;              // [N] (min, max) ordered-int keys of each sample
   int2 *ckey;              // [D] (min, max) keys of each output channel
   GroupParam *sp;          // [N]
@@ -70,6 +72,8 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
 int make_layer(const fqt_layer_desc *d, Layer *L);
 int check_cfg(const fqt_quant_cfg *c, const Layer &L);
 size_t quant_ws_bytes(const Layer &L);
+uint32_t stats_slots(const Layer &L);       // sample slots of a 64-row tile
+int64_t stats_row_blocks(const Layer &L);   // row blocks of the stats kernel
 void carve_quant_ws(void *ws, const Layer &L, QuantWs *q);
 inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -196,5 +200,76 @@ __host__ void dispatch_dtype(int dt, F &&f) {
 }
 
 __device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }
+
+// ----------------------------------------------------------------------------- cross-lane
+// Wave-level exchanges on the VALU data path (DPP row operations and the gfx950 lane
+// swaps) instead of ds_bpermute, whose LDS round trip dominates short dependency chains.
+// DPP row operations act within rows of 16 lanes: row_shr:n (0x110 + n) reads lane
+// i - n of the row (lanes without a source keep `old`), row_ror:8 (0x128) swaps the row's
+// halves, row_bcast:15 / :31 (0x142 / 0x143, rows 1,3 / 2,3 enabled) read the last lane
+// of the preceding row / of row 1.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ int dpp(int old, int v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROWS, 0xF, false);
+}
+
+// v of lane (lane ^ M), M in {1, 2, 4, 8, 16, 32}.
+template <int M>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
+  const int x = int(v);
+  if constexpr (M == 1) return uint32_t(dpp<0xB1>(0, x));          // quad_perm [1,0,3,2]
+  else if constexpr (M == 2) return uint32_t(dpp<0x4E>(0, x));     // quad_perm [2,3,0,1]
+  else if constexpr (M == 4) return uint32_t(dpp<0x141>(0, dpp<0x1B>(0, x)));  // i^3, then i^7
+  else if constexpr (M == 8) return uint32_t(dpp<0x128>(0, x));    // row_ror:8
+  else if constexpr (M == 16) {
+    // permlane16_swap(v, v): .x holds the even rows twice, .y the odd rows twice.
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return uint32_t((__lane_id() & 16) ? r[0] : r[1]);
+  } else {
+    static_assert(M == 32, "lane_xor: M must be a power of two below 64");
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return uint32_t((__lane_id() & 32) ? r[0] : r[1]);
+  }
+}
+template <int M>
+__device__ __forceinline__ uint64_t lane_xor64(uint64_t v) {
+  return (uint64_t(lane_xor<M>(uint32_t(v >> 32))) << 32) | lane_xor<M>(uint32_t(v));
+}
+
+// Inclusive scan of v over the wave's lanes under `op` with identity `id` (lane 63 ends
+// with the whole wave's result).
+template <typename Op>
+__device__ __forceinline__ int wave_scan_i32(int v, int id, Op op) {
+  v = op(v, dpp<0x111>(id, v));
+  v = op(v, dpp<0x112>(id, v));
+  v = op(v, dpp<0x114>(id, v));
+  v = op(v, dpp<0x118>(id, v));
+  v = op(v, dpp<0x142, 0xA>(id, v));
+  v = op(v, dpp<0x143, 0xC>(id, v));
+  return v;
+}
+__device__ __forceinline__ int wave_min_all(int v) {
+  return __builtin_amdgcn_readlane(wave_scan_i32(v, INT_MAX, [](int a, int b) { return min(a, b); }), 63);
+}
+__device__ __forceinline__ int wave_max_all(int v) {
+  return __builtin_amdgcn_readlane(wave_scan_i32(v, INT_MIN, [](int a, int b) { return max(a, b); }), 63);
+}
+// Inclusive prefix sum over the wave for 64-bit values (carries through the high word).
+__device__ __forceinline__ uint64_t wave_scan_add_u64(uint64_t v) {
+#define FQT_DPP_ADD64(CTRL, ROWS)                                                    \
+  do {                                                                               \
+    const uint32_t lo = uint32_t(dpp<CTRL, ROWS>(0, int(uint32_t(v))));              \
+    const uint32_t hi = uint32_t(dpp<CTRL, ROWS>(0, int(uint32_t(v >> 32))));        \
+    v += (uint64_t(hi) << 32) | lo;                                                  \
+  } while (0)
+  FQT_DPP_ADD64(0x111, 0xF);
+  FQT_DPP_ADD64(0x112, 0xF);
+  FQT_DPP_ADD64(0x114, 0xF);
+  FQT_DPP_ADD64(0x118, 0xF);
+  FQT_DPP_ADD64(0x142, 0xA);
+  FQT_DPP_ADD64(0x143, 0xC);
+#undef FQT_DPP_ADD64
+  return v;
+}
 
 }  // namespace fqt

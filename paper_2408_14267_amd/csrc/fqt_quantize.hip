@@ -4,10 +4,12 @@
 //                   tiles: per-tile min/max of every channel row and every r column,
 //                   written as partials (no atomics: same-address atomics from the
 //                   eight XCDs serialise at the memory side)
-//   k_stats_reduce  one workgroup per group: min/max of its partials
-//                   (Section 3.2 range and zero point; Section 5.2 / 5.3 groups)
-//   k_select        one workgroup per group set: AGP keep probabilities, Bernoulli
-//                   masks, kept-id compaction, scale/offset (Section 5.2, AGP)
+//   k_select_fused  (N, D <= 1024) one workgroup per group set: min/max of each group's
+//                   partials (Section 3.2 range and zero point; Section 5.2 / 5.3
+//                   groups), then AGP keep probabilities, Bernoulli masks, kept-id
+//                   compaction, scale/offset (Section 5.2, AGP)
+//   k_stats_reduce  (larger sets) one workgroup per group: min/max of its partials,
+//   k_select        then one workgroup per group set for the AGP steps
 //   k_qpack         second pass over dY: stochastic rounding of every element of a
 //                   kept sample / kept channel, bit-plane split and packing, and the
 //                   byte codes the MFMA products read
@@ -60,111 +62,167 @@ __device__ __forceinline__ uint32_t elem_index(const TileGeom &g, uint32_t d, ui
   return (n * g.D + d) * g.P + (r - n * g.P);
 }
 
-__device__ __forceinline__ int wave_min(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_max(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
-  return v;
-}
+__device__ __forceinline__ int wave_min(int v) { return wave_min_all(v); }
+__device__ __forceinline__ int wave_max(int v) { return wave_max_all(v); }
 
 // ----------------------------------------------------------------------------- stats
 
+// Partial layouts.  Channel partials: part_c[rb][d] for row blocks rb of rs * 64 rows
+// (rs = stats_rows_per_block: enough blocks to cover the chip, few partials).  Sample partials: part_s[(dt * nrt + rt) * SL + k] for the 64-row tile rt and
+// 64-channel tile dt, slot k holding sample n_first(rt) + k, n_first(rt) = rt * 64 / P, and
+// SL = min(64, ceil(63 / P) + 1) slots (a 64-row tile meets at most that many samples).
+struct StatsGeom {
+  TileGeom g;
+  uint32_t nrt, SL, rs;
+};
+
+// Load the quads of tile rows [r0, r0 + 64) x channels [d0, d0 + 64) into x (element 0 of
+// dY outside the layer, so the loads issue back to back).
 template <int MODE, int DT>
-__global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy,
-                                                   TileGeom g, uint32_t nrt,
+__device__ __forceinline__ void stats_load(const void *dy, const TileGeom &g, uint32_t r0,
+                                           uint32_t d0, int t, float (&x)[QUADS][4],
+                                           bool (&ok)[QUADS]) {
+  for (int q = 0; q < QUADS; ++q) {
+    int dd, rr;
+    quad_coord<MODE>(t, q, 0, dd, rr);
+    ok[q] = d0 + dd < g.D && r0 + rr < g.R;      // quads are all-valid or all-invalid
+    load_quad<DT>(dy, ok[q] ? elem_index(g, d0 + dd, r0 + rr) : 0, x[q]);
+  }
+}
+
+// One block per (rs row tiles, 64 channels).  Each 64 x 64 tile goes through LDS as
+// order-preserving integer keys; channel rows are reduced over the rows (kept across the
+// block's row tiles), row columns over the channels and then over the rows of each sample
+// in the tile.
+template <int MODE, int DT>
+__global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, StatsGeom sg,
                                                    int2 *__restrict__ part_c,
                                                    int2 *__restrict__ part_s) {
   __shared__ int32_t key[TILE][TILE + 1];
   __shared__ int32_t pmin[WAVES][TILE], pmax[WAVES][TILE];
+  __shared__ int2 cpart[TILE];
+  const TileGeom &g = sg.g;
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
-  const uint32_t r0 = blockIdx.x * TILE, d0 = blockIdx.y * TILE;
+  const uint32_t d0 = blockIdx.y * TILE;
+  const uint32_t rt0 = blockIdx.x * sg.rs;
+  int clo[TILE / WAVES], chi[TILE / WAVES];      // channel rows wave + WAVES * i
+#pragma unroll
+  for (int i = 0; i < TILE / WAVES; ++i) {
+    clo[i] = INT_MAX;
+    chi[i] = INT_MIN;
+  }
+  float x[QUADS][4];
+  bool ok[QUADS];
+  if (MODE != TILE_SCALAR) stats_load<MODE, DT>(dy, g, rt0 * TILE, d0, t, x, ok);
 
-  if (MODE != TILE_SCALAR) {
-    float x[QUADS][4];
-    bool ok[QUADS];
-    for (int q = 0; q < QUADS; ++q) {
-      int dd, rr;
-      quad_coord<MODE>(t, q, 0, dd, rr);
-      ok[q] = d0 + dd < g.D && r0 + rr < g.R;      // quads are all-valid or all-invalid
-      // Unconditional (element 0 outside the layer) so the loads issue back to back.
-      load_quad<DT>(dy, ok[q] ? elem_index(g, d0 + dd, r0 + rr) : 0, x[q]);
-    }
-    for (int q = 0; q < QUADS; ++q) {
-      if (!ok[q]) continue;
-      for (int k = 0; k < 4; ++k) {
-        int dk, rk;
-        quad_coord<MODE>(t, q, k, dk, rk);
-        key[dk][rk] = f2key(x[q][k] + 0.0f);
+  for (uint32_t s = 0; s < sg.rs; ++s) {
+    const uint32_t rt = rt0 + s;
+    if (rt >= sg.nrt) break;
+    const uint32_t r0 = rt * TILE;
+    if (MODE != TILE_SCALAR) {
+      for (int q = 0; q < QUADS; ++q) {
+        if (!ok[q]) continue;
+        for (int k = 0; k < 4; ++k) {
+          int dk, rk;
+          quad_coord<MODE>(t, q, k, dk, rk);
+          key[dk][rk] = f2key(x[q][k] + 0.0f);
+        }
+      }
+      // The next row tile's loads fly while this one is reduced.
+      if (s + 1 < sg.rs && rt + 1 < sg.nrt)
+        stats_load<MODE, DT>(dy, g, r0 + TILE, d0, t, x, ok);
+    } else {
+      for (int q = 0; q < 4 * QUADS; ++q) {
+        int dd, rr;
+        quad_coord<MODE>(t, q >> 2, q & 3, dd, rr);
+        if (d0 + dd < g.D && r0 + rr < g.R)
+          key[dd][rr] = f2key(load_elem<DT>(dy, elem_index(g, d0 + dd, r0 + rr)) + 0.0f);
       }
     }
-  } else {
-    for (int q = 0; q < 4 * QUADS; ++q) {
-      int dd, rr;
-      quad_coord<MODE>(t, q >> 2, q & 3, dd, rr);
-      if (d0 + dd < g.D && r0 + rr < g.R)
-        key[dd][rr] = f2key(load_elem<DT>(dy, elem_index(g, d0 + dd, r0 + rr)) + 0.0f);
-    }
-  }
-  __syncthreads();
+    __syncthreads();
 
-  const bool row_ok = r0 + lane < g.R;
-  // Channel rows of the tile: reduce over the tile's 64 rows r.
-  for (int i = 0; i < TILE / WAVES; ++i) {
-    const int dd = wave + WAVES * i;
-    const uint32_t d = d0 + dd;
-    if (d >= g.D) break;
-    const int k = key[dd][lane];
-    const int lo = wave_min(row_ok ? k : INT_MAX);
-    const int hi = wave_max(row_ok ? k : INT_MIN);
-    if (lane == 0) part_c[size_t(d) * nrt + blockIdx.x] = make_int2(lo, hi);
-  }
-  // Columns r of the tile: reduce over the tile's channels.
-  int lo = INT_MAX, hi = INT_MIN;
-  for (int i = 0; i < TILE / WAVES; ++i) {
-    const int dd = (TILE / WAVES) * wave + i;
-    if (d0 + dd >= g.D) break;
-    const int k = key[dd][lane];
-    lo = min(lo, k);
-    hi = max(hi, k);
-  }
-  pmin[wave][lane] = lo;
-  pmax[wave][lane] = hi;
-  __syncthreads();
-  if (wave == 0 && row_ok) {
-    for (int v = 1; v < WAVES; ++v) {
-      lo = min(lo, pmin[v][lane]);
-      hi = max(hi, pmax[v][lane]);
+    const bool row_ok = r0 + lane < g.R;
+    // Channel rows of the tile: reduce over the tile's 64 rows r.
+#pragma unroll
+    for (int i = 0; i < TILE / WAVES; ++i) {
+      const int dd = wave + WAVES * i;
+      const int k = key[dd][lane];
+      clo[i] = min(clo[i], wave_min(row_ok ? k : INT_MAX));
+      chi[i] = max(chi[i], wave_max(row_ok ? k : INT_MIN));
     }
-    part_s[size_t(blockIdx.y) * g.R + r0 + lane] = make_int2(lo, hi);
+    // Columns r of the tile: reduce over the tile's channels.
+    int lo = INT_MAX, hi = INT_MIN;
+    for (int i = 0; i < TILE / WAVES; ++i) {
+      const int dd = (TILE / WAVES) * wave + i;
+      if (d0 + dd >= g.D) break;
+      const int k = key[dd][lane];
+      lo = min(lo, k);
+      hi = max(hi, k);
+    }
+    pmin[wave][lane] = lo;
+    pmax[wave][lane] = hi;
+    __syncthreads();
+    if (wave == 0) {
+      for (int v = 1; v < WAVES; ++v) {
+        lo = min(lo, pmin[v][lane]);
+        hi = max(hi, pmax[v][lane]);
+      }
+      // Rows of one sample are adjacent lanes: slot k of this tile reduces the rows of
+      // sample n_first + k.
+      const uint32_t n_first = fdiv(r0, g.divP);
+      const uint32_t slot = row_ok ? fdiv(r0 + lane, g.divP) - n_first : 0xFFFFFFFFu;
+      int2 *ps = part_s + (size_t(blockIdx.y) * sg.nrt + rt) * sg.SL;
+      if (g.P == 1) {
+        ps[lane] = row_ok ? make_int2(lo, hi) : make_int2(INT_MAX, INT_MIN);
+      } else {
+        for (uint32_t k = 0; k < sg.SL; ++k) {
+          const int l = wave_min(slot == k ? lo : INT_MAX);
+          const int h = wave_max(slot == k ? hi : INT_MIN);
+          if (lane == 0) ps[k] = make_int2(l, h);
+        }
+      }
+    }
+    // (The next tile's key stores wait for every read of this one.)
+    __syncthreads();
   }
+  // Channel partials of this row block, [row block][D]: one coalesced store.
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < TILE / WAVES; ++i) cpart[wave + WAVES * i] = make_int2(clo[i], chi[i]);
+  }
+  __syncthreads();
+  if (wave == 1 && d0 + lane < g.D) part_c[size_t(blockIdx.x) * g.D + d0 + lane] = cpart[lane];
 }
 
-// Block b < N reduces sample b over part_s[*][b*P .. b*P+P); block N + d reduces
-// channel d over part_c[d][*].
+// Large group sets: block b < N reduces sample b over its slots, block N + d channel d
+// over its row-block partials.
 constexpr int RED_THREADS = 256;
 __global__ __launch_bounds__(RED_THREADS) void k_stats_reduce(const int2 *__restrict__ part_c,
                                                           const int2 *__restrict__ part_s,
-                                                          uint32_t N, uint32_t P, uint32_t R,
-                                                          uint32_t nrt, uint32_t ndt,
+                                                          StatsGeom sg, uint32_t nrb,
+                                                          uint32_t ndt,
                                                           int2 *__restrict__ skey,
                                                           int2 *__restrict__ ckey) {
   __shared__ int32_t smn[RED_THREADS / 64], smx[RED_THREADS / 64];
+  const TileGeom &g = sg.g;
   const uint32_t b = blockIdx.x;
+  const uint32_t N = g.R / g.P;
   int lo = INT_MAX, hi = INT_MIN;
   if (b < N) {
-    for (uint32_t dt = 0; dt < ndt; ++dt)
-      for (uint32_t p = threadIdx.x; p < P; p += RED_THREADS) {
-        const int2 v = part_s[size_t(dt) * R + b * P + p];
-        lo = min(lo, v.x);
-        hi = max(hi, v.y);
-      }
+    const uint32_t rt_lo = (b * g.P) / TILE, rt_hi = min(sg.nrt - 1, (b * g.P + g.P - 1) / TILE);
+    const uint32_t cnt = rt_hi - rt_lo + 1;
+    for (uint32_t i = threadIdx.x; i < ndt * cnt; i += RED_THREADS) {
+      const uint32_t dt = i / cnt, rt = rt_lo + i % cnt;
+      const uint32_t k = b - fdiv(rt * TILE, g.divP);
+      const int2 v = part_s[(size_t(dt) * sg.nrt + rt) * sg.SL + k];
+      lo = min(lo, v.x);
+      hi = max(hi, v.y);
+    }
   } else {
     const uint32_t d = b - N;
-    for (uint32_t i = threadIdx.x; i < nrt; i += RED_THREADS) {
-      const int2 v = part_c[size_t(d) * nrt + i];
+    for (uint32_t i = threadIdx.x; i < nrb; i += RED_THREADS) {
+      const int2 v = part_c[size_t(i) * g.D + d];
       lo = min(lo, v.x);
       hi = max(hi, v.y);
     }
@@ -190,7 +248,13 @@ __global__ __launch_bounds__(RED_THREADS) void k_stats_reduce(const int2 *__rest
 // ----------------------------------------------------------------------------- select
 
 struct SetArgs {
-  const int2 *key;     // [G] (min, max) keys
+  const int2 *key;     // [G] (min, max) keys (k_select)
+  const int2 *part;    // partials (k_select_fused)
+  uint32_t slots;      // 0: group g reduces part[u * ld + g], u < U (channels)
+                       // 1: sample slots of part_s (P, nrt, SL, ndt)
+  uint32_t U, ld;
+  uint32_t P, nrt, SL, ndt;
+  FastDiv divP;
   int32_t G;
   uint32_t stream;
   int32_t *kept;
@@ -440,6 +504,245 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
 #undef GROUP_KEY
 }
 
+// Select for group sets of at most GP <= 1024 groups, one 1024-thread workgroup per set,
+// with the partial reduction folded in.  One sort key per thread: the bitonic stages
+// whose partner lies in the same wave exchange through shuffles, the others through a
+// double-buffered LDS array (one barrier per stage); the water-filling scan, the
+// saturation count and the kept-id ranks are wave scans plus one LDS combine each.
+constexpr int SEL_NT = 1024;
+constexpr int SEL_NW = SEL_NT / 64;
+
+// v of lane (lane ^ j) for a wave-internal bitonic partner distance j < 64.
+__device__ __forceinline__ uint64_t xor_partner(uint64_t v, int j) {
+  switch (j) {
+    case 32: return lane_xor64<32>(v);
+    case 16: return lane_xor64<16>(v);
+    case 8: return lane_xor64<8>(v);
+    case 4: return lane_xor64<4>(v);
+    case 2: return lane_xor64<2>(v);
+    default: return lane_xor64<1>(v);
+  }
+}
+
+// Inclusive prefix sum of v over the block's thread order, and the block total.
+template <typename T>
+__device__ T block_incl_scan(T v, T *scr, T &total, int lane, int wave) {
+  if constexpr (sizeof(T) == 8) v = wave_scan_add_u64(v);
+  else v = wave_scan_i32(v, 0, [](int a, int b) { return a + b; });
+  if (lane == 63) scr[wave] = v;
+  __syncthreads();
+  T off = 0, tot = 0;
+  for (int w = 0; w < SEL_NW; ++w) {
+    const T x = scr[w];
+    off += w < wave ? x : T(0);
+    tot += x;
+  }
+  __syncthreads();
+  total = tot;
+  return off + v;
+}
+
+template <int GP>
+__global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
+  static_assert(GP <= SEL_NT && GP % 64 == 0, "one sort key per thread");
+  __shared__ int2 gk[GP];
+  __shared__ int2 tmpk[SEL_NT];
+  __shared__ uint64_t sbuf[2][GP];
+  __shared__ uint64_t scr_u[SEL_NW];
+  __shared__ int32_t scr_i[SEL_NW];
+  __shared__ float scr_f[SEL_NW];
+  __shared__ uint64_t sat_w[2];          // W(s_sat), w at s_sat - 1
+  const SetArgs S = blockIdx.x ? a.set[1] : a.set[0];
+  const int G = S.G;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int b = a.bits;
+  const int B = (1 << b) - 1;
+
+  // Group keys: min over the minima, max over the maxima of the group's partials.  Loads
+  // are issued in batches of 16 per thread so that a group set costs a few memory
+  // latencies.
+  // SEL_NT / GP threads per group: thread t takes group t % GP and every (SEL_NT / GP)-th
+  // of its partials from t / GP; the shares meet in LDS.
+  {
+    constexpr int SPLIT = SEL_NT / GP;
+    const int g = t % GP, r0 = t / GP;
+    int lo = INT_MAX, hi = INT_MIN;
+    if (g < G && !S.slots) {            // channels: row-block partials, adjacent per row
+      for (uint32_t u0 = r0; u0 < S.U; u0 += 16 * SPLIT) {
+        int2 v[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const uint32_t u = u0 + k * SPLIT;
+          v[k] = u < S.U ? S.part[size_t(u) * S.ld + g] : make_int2(INT_MAX, INT_MIN);
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          lo = min(lo, v[k].x);
+          hi = max(hi, v[k].y);
+        }
+      }
+    } else if (g < G) {                 // samples: the slots of the 64-row tiles they meet
+      const uint32_t first = uint32_t(g) * S.P;
+      const uint32_t rt_lo = first / TILE, rt_hi = min(S.nrt - 1, (first + S.P - 1) / TILE);
+      for (uint32_t dt = r0; dt < S.ndt; dt += SPLIT) {
+#pragma unroll 4
+        for (uint32_t rt = rt_lo; rt <= rt_hi; ++rt) {
+          const uint32_t k = uint32_t(g) - fdiv(rt * TILE, S.divP);
+          const int2 v = S.part[(size_t(dt) * S.nrt + rt) * S.SL + k];
+          lo = min(lo, v.x);
+          hi = max(hi, v.y);
+        }
+      }
+    }
+    tmpk[t] = make_int2(lo, hi);
+    __syncthreads();
+    if (t < G) {
+      int2 k = tmpk[t];
+#pragma unroll
+      for (int s2 = 1; s2 < SPLIT; ++s2) {
+        const int2 o = tmpk[t + s2 * GP];
+        k.x = min(k.x, o.x);
+        k.y = max(k.y, o.y);
+      }
+      gk[t] = k;
+    }
+  }
+  __syncthreads();
+
+  // Largest range: ranges are non-negative, so their float bits order like ints.
+  float rmax = 0.0f;
+  for (int i = t; i < G; i += SEL_NT) rmax = fmaxf(rmax, group_range(gk[i]));
+  {
+    const int m = wave_max_all(__float_as_int(rmax));
+    if (lane == 0) scr_f[wave] = __int_as_float(m);
+    __syncthreads();
+    rmax = 0.0f;
+    for (int w = 0; w < SEL_NW; ++w) rmax = fmaxf(rmax, scr_f[w]);
+  }
+  const int2 own = t < G ? gk[t] : make_int2(0, 0);
+  const float own_R = group_range(own);
+  const uint64_t own_w = t < G ? agp_weight(own_R, rmax) : 0;
+
+  int64_t s_sat = 0;           // number of saturated groups (p capped at 1)
+  uint64_t w_thr = 0;          // weight of the last saturated group
+  uint64_t w_rem = 0;          // weight of the unsaturated groups
+  uint64_t key_thr = 0;        // TOPK: smallest kept sort key
+  if (a.mode != FQT_AGP_OFF) {
+    // Bitonic sort of one key per thread, descending.
+    uint64_t x = t < G ? sort_key(own_w, t) : 0ull;
+    int buf = 0;
+    // Only the GP / 64 waves holding keys work; the others just meet the LDS stages'
+    // barriers (they would otherwise take VALU issue slots from the sorting waves).
+    const bool sorter = wave < GP / 64;
+    // Fully unrolled (GP is a compile-time constant): every stage is straight-line code
+    // with its exchange pattern fixed.
+#pragma unroll
+    for (int k = 2; k <= GP; k <<= 1) {
+#pragma unroll
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        uint64_t y = 0;
+        if (j >= 64) {
+          if (sorter) sbuf[buf][t] = x;
+          __syncthreads();
+          if (sorter) y = sbuf[buf][t ^ j];
+          buf ^= 1;
+        } else if (sorter) {
+          y = xor_partner(x, j);
+        }
+        if (sorter) {
+          const bool lower = (t & j) == 0, desc = (t & k) == 0;
+          x = (lower == desc) ? (x > y ? x : y) : (x < y ? x : y);
+        }
+      }
+    }
+    if (a.mode == FQT_AGP_TOPK) {
+      if (t < GP) sbuf[buf][t] = x;
+      __syncthreads();
+      key_thr = sbuf[buf][max(1, G / b) - 1];
+    } else {
+      // Position p = t of the descending order saturates iff (G - b p) w_(p) >= b W(p),
+      // W(p) = weight at positions >= p; the test holds on a prefix, so its pass count
+      // is s_sat.
+      const uint64_t w = t < G ? (x >> ID_BITS) : 0ull;
+      uint64_t total;
+      const uint64_t incl = block_incl_scan<uint64_t>(w, scr_u, total, lane, wave);
+      const uint64_t Wp = total - incl + w;
+      const bool pass = t < G && w > 0 &&
+                        (int64_t(G) - int64_t(b) * t) * int64_t(w) >= int64_t(b) * int64_t(Wp);
+      int32_t cnt_total;
+      block_incl_scan<int32_t>(pass ? 1 : 0, scr_i, cnt_total, lane, wave);
+      s_sat = cnt_total;
+      if (t == s_sat) sat_w[0] = Wp;
+      if (t == s_sat - 1) sat_w[1] = w;
+      __syncthreads();
+      w_rem = s_sat < G ? sat_w[0] : 0;
+      w_thr = s_sat > 0 ? sat_w[1] : 0;
+    }
+  }
+
+  // Mask of group i = t, then the stable partition kept-ascending | pruned-ascending.
+  const int64_t A = int64_t(G) - int64_t(b) * s_sat;
+  bool keep = false;
+  if (t < G) {
+    if (a.mode == FQT_AGP_OFF) {
+      keep = true;
+    } else if (a.mode == FQT_AGP_TOPK) {
+      keep = sort_key(own_w, t) >= key_thr;
+    } else if (s_sat > 0 && own_w > 0 && own_w >= w_thr) {
+      keep = true;
+    } else if (A > 0 && w_rem > 0 && own_w > 0) {
+      const Ctr4 u = philox_block(uint64_t(t) >> 2, S.stream, a.seed, a.step, a.layer);
+      const uint32_t u32 = ctr_word(u, uint32_t(t) & 3u);
+      uint64_t lh, ll;
+      mul_32x64(u32, uint64_t(b) * w_rem, lh, ll);
+      const uint64_t aw = uint64_t(A) * own_w;     // < 2^55
+      const uint64_t rh = aw >> 32, rl = aw << 32;
+      keep = lh < rh || (lh == rh && ll < rl);
+    }
+  }
+  int32_t count;
+  const int32_t rank = block_incl_scan<int32_t>(keep ? 1 : 0, scr_i, count, lane, wave) -
+                       (keep ? 1 : 0);
+  if (t == 0) *S.count = count;
+  if (t >= G) return;
+  const float R = own_R;
+  const float Z = key2f(own.x);
+  float Sc = 0.0f, Zp = 0.0f, p = 0.0f;
+  const bool unit_p = a.mode != FQT_AGP_BERNOULLI || (s_sat > 0 && own_w > 0 && own_w >= w_thr);
+  if (a.mode == FQT_AGP_OFF) {
+    p = 1.0f;
+  } else if (a.mode == FQT_AGP_TOPK) {
+    p = keep ? 1.0f : 0.0f;
+  } else if (unit_p) {
+    p = 1.0f;
+  } else if (w_rem > 0 && A > 0) {
+    p = static_cast<float>(static_cast<double>(uint64_t(A) * own_w) /
+                           static_cast<double>(uint64_t(b) * w_rem));
+  }
+  if (keep) {
+    if (unit_p) {
+      Sc = static_cast<float>(static_cast<double>(R) / static_cast<double>(B));
+      Zp = Z;
+    } else {
+      const double bw = static_cast<double>(uint64_t(b) * w_rem);
+      const double aw = static_cast<double>(uint64_t(A) * own_w);
+      Sc = static_cast<float>((static_cast<double>(R) * bw) / (static_cast<double>(B) * aw));
+      Zp = static_cast<float>((static_cast<double>(Z) * bw) / aw);
+    }
+  }
+  S.prob[t] = p;
+  S.scale[t] = Sc;
+  S.offset[t] = Zp + 0.0f;
+  GroupParam gp;
+  gp.z = Z;
+  gp.inv = R > 0.0f ? __fdiv_rn(float(B), R) : 0.0f;
+  gp.rank = keep ? rank : -1;
+  gp.pad = 0;
+  S.gp[t] = gp;
+  S.kept[keep ? rank : count + (t - rank)] = t;
+}
+
 // ----------------------------------------------------------------------------- quantize + pack
 
 // b-bit stochastic rounding code of x (Section 3.2): v = clamp((x - Z) * inv, 0, B),
@@ -616,44 +919,69 @@ int launch_select(const SelectArgs &sa, hipStream_t s) {
 
 }  // namespace
 
+uint32_t stats_slots(const Layer &L) {
+  const int64_t per = (63 + L.P - 1) / L.P + 1;
+  return uint32_t(per < 64 ? per : 64);
+}
+// Row tiles per stats block: one while that still gives 512 blocks, else up to 8.
+uint32_t stats_rows_per_block(const Layer &L) {
+  int64_t rs = 1;
+  while (rs < 8 && L.Wr * L.Wd / (rs * 2) >= 512) rs *= 2;
+  return uint32_t(rs);
+}
+int64_t stats_row_blocks(const Layer &L) {
+  const int64_t rs = stats_rows_per_block(L);
+  return (L.Wr + rs - 1) / rs;
+}
+
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
                     const QuantWs &w, hipStream_t s) {
   TileGeom g{uint32_t(L.D), uint32_t(L.P), uint32_t(L.R), make_fastdiv(uint32_t(L.P))};
   const uint32_t nrt = uint32_t(L.Wr), ndt = uint32_t(L.Wd);
-  const dim3 grid(nrt, ndt);
+  const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L)};
+  const uint32_t nrb = uint32_t(stats_row_blocks(L));
+  const dim3 grid(nrb, ndt);
   const int mode = (L.P % 4 == 0) ? TILE_PIX : (L.P == 1 && L.D % 4 == 0) ? TILE_CHAN : TILE_SCALAR;
   dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
-      hipLaunchKernelGGL((k_stats<TILE_PIX, DT>), grid, dim3(THREADS), 0, s, dY, g, nrt, w.part_c,
+      hipLaunchKernelGGL((k_stats<TILE_PIX, DT>), grid, dim3(THREADS), 0, s, dY, sg, w.part_c,
                          w.part_s);
     else if (mode == TILE_CHAN)
-      hipLaunchKernelGGL((k_stats<TILE_CHAN, DT>), grid, dim3(THREADS), 0, s, dY, g, nrt,
-                         w.part_c, w.part_s);
+      hipLaunchKernelGGL((k_stats<TILE_CHAN, DT>), grid, dim3(THREADS), 0, s, dY, sg, w.part_c,
+                         w.part_s);
     else
-      hipLaunchKernelGGL((k_stats<TILE_SCALAR, DT>), grid, dim3(THREADS), 0, s, dY, g, nrt,
+      hipLaunchKernelGGL((k_stats<TILE_SCALAR, DT>), grid, dim3(THREADS), 0, s, dY, sg,
                          w.part_c, w.part_s);
   });
   if (last_launch_status() != FQT_OK) return FQT_E_HIP;
-  hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s, w.part_c,
-                     w.part_s, uint32_t(L.N), uint32_t(L.P), uint32_t(L.R), nrt, ndt, w.skey,
-                     w.ckey);
-  if (last_launch_status() != FQT_OK) return FQT_E_HIP;
 
   SelectArgs sa;
-  sa.set[0] = SetArgs{w.skey, int32_t(L.N), STREAM_SAMPLE, q.psq_kept, q.psq_count, q.psq_scale,
-                      q.psq_offset, q.psq_prob, w.sp};
-  sa.set[1] = SetArgs{w.ckey, int32_t(L.D), STREAM_CHANNEL, q.pcq_kept, q.pcq_count, q.pcq_scale,
-                      q.pcq_offset, q.pcq_prob, w.cp};
+  sa.set[0] = SetArgs{w.skey, w.part_s, 1u, 0u, 0u, uint32_t(L.P), nrt, sg.SL, ndt,
+                      make_fastdiv(uint32_t(L.P)), int32_t(L.N), STREAM_SAMPLE, q.psq_kept,
+                      q.psq_count, q.psq_scale, q.psq_offset, q.psq_prob, w.sp};
+  sa.set[1] = SetArgs{w.ckey, w.part_c, 0u, nrb, uint32_t(L.D), 0u, 0u, 0u, 0u,
+                      make_fastdiv(1u), int32_t(L.D), STREAM_CHANNEL, q.pcq_kept, q.pcq_count,
+                      q.pcq_scale, q.pcq_offset, q.pcq_prob, w.cp};
   sa.bits = cfg.bits; sa.mode = cfg.agp_mode; sa.seed = cfg.seed; sa.step = cfg.step;
   sa.layer = cfg.layer_id;
   const int64_t gmax = L.N > L.D ? L.N : L.D;
   int st;
-  if (gmax <= 256) st = launch_select<256, 256>(sa, s);
-  else if (gmax <= 1024) st = launch_select<1024, 1024>(sa, s);
-  else if (gmax <= 4096) st = launch_select<4096, 1024>(sa, s);
-  else st = launch_select<16384, 1024>(sa, s);
+  if (gmax <= 256) {
+    hipLaunchKernelGGL(k_select_fused<256>, dim3(2), dim3(SEL_NT), 0, s, sa);
+    st = last_launch_status();
+  } else if (gmax <= 1024) {
+    hipLaunchKernelGGL(k_select_fused<1024>, dim3(2), dim3(SEL_NT), 0, s, sa);
+    st = last_launch_status();
+  } else {
+    hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,
+                       w.part_c, w.part_s, sg, nrb, ndt, w.skey, w.ckey);
+    if (last_launch_status() != FQT_OK) return FQT_E_HIP;
+    if (gmax <= 4096) st = launch_select<4096, 1024>(sa, s);
+    else st = launch_select<16384, 1024>(sa, s);
+  }
   if (st != FQT_OK) return st;
 
+  const dim3 qgrid(nrt, ndt);            // one block per 64 x 64 tile
   QPackArgs qa;
   qa.dy = dY; qa.g = g; qa.sp = w.sp; qa.cp = w.cp;
   qa.psq = q.psq_planes; qa.pcq = q.pcq_planes;
@@ -662,11 +990,11 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   qa.bits = cfg.bits; qa.seed = cfg.seed; qa.step = cfg.step; qa.layer = cfg.layer_id;
   dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
-      hipLaunchKernelGGL((k_qpack<TILE_PIX, DT>), grid, dim3(THREADS), 0, s, qa);
+      hipLaunchKernelGGL((k_qpack<TILE_PIX, DT>), qgrid, dim3(THREADS), 0, s, qa);
     else if (mode == TILE_CHAN)
-      hipLaunchKernelGGL((k_qpack<TILE_CHAN, DT>), grid, dim3(THREADS), 0, s, qa);
+      hipLaunchKernelGGL((k_qpack<TILE_CHAN, DT>), qgrid, dim3(THREADS), 0, s, qa);
     else
-      hipLaunchKernelGGL((k_qpack<TILE_SCALAR, DT>), grid, dim3(THREADS), 0, s, qa);
+      hipLaunchKernelGGL((k_qpack<TILE_SCALAR, DT>), qgrid, dim3(THREADS), 0, s, qa);
   });
   return last_launch_status();
 }
