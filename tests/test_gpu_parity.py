@@ -56,6 +56,11 @@ CASES = [
      Recipe("sample_lognormal", sigma=1.0), "f32"),
     ("conv2x3_mixed_stride_b3", LayerShape("c", "conv2d", 2, 5, 9, 6, 7, 2, 3, 1, 2, 0, 1), 3, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # 64 | Ho*Wo: the staged-band im2col path (ragged channel group, stride 2, bf16 input).
+    ("conv_s2_p256_bf16_b4", LayerShape("c", "conv2d", 2, 20, 48, 32, 32, 3, 3, 2, 2, 1, 1), 4,
+     0, Recipe("sample_lognormal", sigma=1.0), "bf16"),
+    ("conv_p64_ragged_b2", LayerShape("c", "conv2d", 3, 33, 40, 8, 8, 3, 3, 1, 1, 1, 1), 2, 0,
+     Recipe("channel_lognormal", sigma=1.0), "f32"),
 ]
 
 
