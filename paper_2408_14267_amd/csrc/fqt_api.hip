@@ -320,8 +320,7 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
     FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s, true));
   FQT_TRY(launch_pack_w_i8(W, L, w.wsb, w.wlsum, s));
   FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
-  FQT_TRY(launch_gemm_dw(L, *cfg, w.q, w.xsign, dW, nullptr, w.dw_ws, s));
-  return launch_gemm_dx(L, *cfg, w.q, w.wsb, w.wlsum, dX, nullptr, s);
+  return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, s);
 }
 
 }  // extern "C"

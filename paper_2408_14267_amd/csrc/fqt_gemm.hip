@@ -180,21 +180,24 @@ __device__ __forceinline__ void dw_accumulate(const DwArgs &a, __amdgpu_buffer_r
 // the contraction over N*Ho*Wo; its four waves take every fourth word, expand each 16-bit
 // piece of their column's word once and feed it to every tile.  The four partial tiles
 // meet in LDS; the block writes its sum and its set-bit counts to the split's slice.
+struct DwPartLds {
+  int32_t red[DW_WAVES - 1][DW_RT][16][64];
+  int32_t tred[32];
+};
+
 template <bool B8>
-__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
-  __shared__ int32_t red[DW_WAVES - 1][DW_RT][16][64];
-  __shared__ int32_t tred[32];
+__device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid, DwPartLds &sm) {
   const int t = threadIdx.x, lane = t & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
-  const uint32_t rest = fdiv(blockIdx.x, a.divS);
-  const uint32_t sp = blockIdx.x - rest * a.S;
+  const uint32_t rest = fdiv(bid, a.divS);
+  const uint32_t sp = bid - rest * a.S;
   const uint32_t grp = fdiv(rest, a.divKt);
   const uint32_t j0 = grp * (DW_RT * 32), k0 = (rest - grp * a.ktiles) * 32;
   if (int(j0) >= count) return;               // slot group past the kept channels
   const int nrt = min(DW_RT, (count - int(j0) + 31) / 32);   // live slot tiles, >= 1
-  if (t < 32) tred[t] = 0;
+  if (t < 32) sm.tred[t] = 0;
 
   const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
   const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
@@ -221,18 +224,18 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
     default: dw_accumulate<4, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
   }
   __syncthreads();                      // tred is initialised
-  atomicAdd(&tred[i], int(tpart));
+  atomicAdd(&sm.tred[i], int(tpart));
   if (wave > 0) {
 #pragma unroll
     for (int rt = 0; rt < DW_RT; ++rt) {
       if (rt >= nrt) break;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) red[wave - 1][rt][v][lane] = acc[rt][v];
+      for (int v = 0; v < 16; ++v) sm.red[wave - 1][rt][v][lane] = acc[rt][v];
     }
   }
   __syncthreads();
   if (wave != 0 || !b_ok) return;
-  if (g == 0) a.partT[size_t(sp) * a.K + kc] = tred[i];
+  if (g == 0) a.partT[size_t(sp) * a.K + kc] = sm.tred[i];
   int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.K + kc;
 #pragma unroll
   for (int rt = 0; rt < DW_RT; ++rt) {
@@ -241,7 +244,7 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
 #pragma unroll
     for (int w = 0; w < DW_WAVES - 1; ++w)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[rt][v] += red[w][rt][v][lane];
+      for (int v = 0; v < 16; ++v) acc[rt][v] += sm.red[w][rt][v][lane];
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -249,6 +252,12 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
       if (int(j0) + row < count) out[size_t(row) * a.K] = acc[rt][v];
     }
   }
+}
+
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
+  __shared__ DwPartLds sm;
+  dw_part_body<B8>(a, blockIdx.x, sm);
 }
 
 // dW from the split partials: one thread per element (slot, k) of the slot capacity.  A
@@ -293,6 +302,7 @@ struct DxArgs {
   uint32_t codes_bytes, wsb_bytes;
   int kh, kw, sh, sw, ph, pw;
   FastDiv divHW, divW, divKw, divNch, divCt;
+  uint32_t nblocks;              // blocks of the dX grid (compute tiles + zero pool)
 };
 
 constexpr int DX_MAX_TAPS = 64;
@@ -310,14 +320,17 @@ constexpr int DX_THREADS = DX_WAVES * 64;
 // contraction step (tap, 32 bytes of D).  For tap (i, j) a pixel (h, w) reads the code row
 // of the output pixel (ho, wo) with ho*sh - ph + i = h and wo*sw - pw + j = w, or nothing;
 // the byte offset of every (tap, pixel) row is tabulated once per block.
+struct DxLds {
+  uint32_t rowoff[DX_MAX_TAPS][32];     // 32 * code row, BUF_NONE if none
+  int32_t redi[DX_WAVES - 1][16][64];
+  float redf[DX_WAVES - 1][16][64];
+  int32_t pix_out[32];                  // NCHW offset of (sample, pixel) minus channel
+  float pix_s[32], pix_z[32];
+  int32_t ltot[32];                     // b = 8: sum of every sign of the channel
+};
+
 template <bool B8, int NB>
-__global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
-  __shared__ uint32_t rowoff[DX_MAX_TAPS][32];     // 32 * code row, BUF_NONE if none
-  __shared__ int32_t redi[DX_WAVES - 1][16][64];
-  __shared__ float redf[DX_WAVES - 1][16][64];
-  __shared__ int32_t pix_out[32];                  // NCHW offset of (sample, pixel) minus channel
-  __shared__ float pix_s[32], pix_z[32];
-  __shared__ int32_t ltot[32];                     // b = 8: sum of every sign of the channel
+__device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm) {
   const int t = threadIdx.x, lane = t & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
@@ -325,17 +338,17 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
   const uint32_t live_rows = uint32_t(count) * a.HW;
   const uint32_t live_blocks = ((live_rows + 31) / 32) * a.ctiles;
 
-  if (blockIdx.x >= live_blocks) {      // zero the pruned samples, one sample per block
-    const uint32_t nz = gridDim.x - live_blocks;
-    for (uint32_t slot = blockIdx.x - live_blocks; slot < a.N - uint32_t(count); slot += nz) {
+  if (bid >= live_blocks) {      // zero the pruned samples, one sample per block
+    const uint32_t nz = a.nblocks - live_blocks;
+    for (uint32_t slot = bid - live_blocks; slot < a.N - uint32_t(count); slot += nz) {
       const size_t n = size_t(a.kept[uint32_t(count) + slot]);
       zero_run(a.dX, n * a.CHW, a.CHW, a.dx_t == FQT_BF16 ? 2 : 4, t, DX_THREADS);
       if (a.I_out) zero_run(a.I_out, n * a.CHW, a.CHW, 4, t, DX_THREADS);
     }
     return;
   }
-  const uint32_t mt = fdiv(blockIdx.x, a.divCt);
-  const uint32_t m0 = mt * 32, c0 = (blockIdx.x - mt * a.ctiles) * 32;
+  const uint32_t mt = fdiv(bid, a.divCt);
+  const uint32_t m0 = mt * 32, c0 = (bid - mt * a.ctiles) * 32;
   const int taps = int(a.taps);
 
   for (int e = t; e < 32 * taps; e += DX_THREADS) {
@@ -353,7 +366,7 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
           off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
       }
     }
-    rowoff[tap][p] = off;
+    sm.rowoff[tap][p] = off;
   }
   if (t < 32) {
     const uint32_t m = m0 + t;
@@ -366,15 +379,15 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
       sc = a.scale[n];
       zo = a.offset[n];
     }
-    pix_out[t] = off;
-    pix_s[t] = sc;
-    pix_z[t] = zo;
+    sm.pix_out[t] = off;
+    sm.pix_s[t] = sc;
+    sm.pix_z[t] = zo;
   } else if (B8 && t < 64) {
     const uint32_t ch = c0 + uint32_t(t - 32);
     int s = 0;
     if (ch < a.C)
       for (int tap = 0; tap < taps; ++tap) s += a.wlsum[ch * a.taps + tap];
-    ltot[t - 32] = s;
+    sm.ltot[t - 32] = s;
   }
   __syncthreads();
 
@@ -397,7 +410,7 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
       const uint32_t tap = fdiv(st, a.divNch);
       const uint32_t kc = st - tap * a.nch;
       A[u] = load16(ars, live ? abase : BUF_NONE, (kc * a.taps + tap) * a.C * 32);
-      B[u] = load16(brs, rowoff[tap][i] + 16 * g, kc * a.R * 32);
+      B[u] = load16(brs, sm.rowoff[tap][i] + 16 * g, kc * a.R * 32);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -411,15 +424,15 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
     const int tap = tp + g;
     const bool tv = tap < taps;
     const float av = (tv && ch < a.C) ? float(a.wlsum[ch * a.taps + tap]) : 0.0f;
-    const float bv = (tv && rowoff[tv ? tap : 0][i] != BUF_NONE) ? 1.0f : 0.0f;
+    const float bv = (tv && sm.rowoff[tv ? tap : 0][i] != BUF_NONE) ? 1.0f : 0.0f;
     cacc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, cacc, 0, 0, 0);
   }
 
   if (wave > 0) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      redi[wave - 1][v][lane] = acc[v];
-      redf[wave - 1][v][lane] = cacc[v];
+      sm.redi[wave - 1][v][lane] = acc[v];
+      sm.redf[wave - 1][v][lane] = cacc[v];
     }
   }
   __syncthreads();
@@ -428,26 +441,45 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
   for (int w = 0; w < DX_WAVES - 1; ++w)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      acc[v] += redi[w][v][lane];
-      cacc[v] += redf[w][v][lane];
+      acc[v] += sm.redi[w][v][lane];
+      cacc[v] += sm.redf[w][v][lane];
     }
 
-  const int off = pix_out[i];
+  const int off = sm.pix_out[i];
   if (off < 0) return;                    // rows past the count belong to the zero blocks
-  const float S = pix_s[i], Z = pix_z[i];
+  const float S = sm.pix_s[i], Z = sm.pix_z[i];
   __builtin_amdgcn_sched_barrier(0);      // every LDS read above issues before the stores
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int crow = acc_row(v, g);
     const uint32_t cc = c0 + crow;
     if (cc >= a.C) continue;
-    const int I = acc[v] + (B8 ? 128 * ltot[crow] : 0);
+    const int I = acc[v] + (B8 ? 128 * sm.ltot[crow] : 0);
     const float out = rescale(S, I, Z, cacc[v]);
     const size_t o = size_t(off) + size_t(cc) * a.HW;
     if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
     else static_cast<float *>(a.dX)[o] = out;
     if (a.I_out) a.I_out[o] = I;
   }
+}
+
+template <bool B8, int NB>
+__global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
+  __shared__ DxLds sm;
+  dx_body<B8, NB>(a, blockIdx.x, sm);
+}
+
+// Both products in one launch (the layer backward): blocks [0, ndw) are dW split-R
+// partial blocks, the rest dX blocks; the two share the LDS allocation.
+union ProductsLds {
+  DxLds dx;
+  DwPartLds dw;
+};
+template <bool B8, int NB>
+__global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
+  __shared__ ProductsLds sm;
+  if (blockIdx.x < ndw) dw_part_body<B8>(dwa, blockIdx.x, sm.dw);
+  else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
 }
 
 }  // namespace
@@ -459,8 +491,10 @@ size_t gemm_dw_ws_bytes(const Layer &L) {
   return align256(S * size_t(L.D) * L.K * 4) + align256(S * size_t(L.K) * 4);
 }
 
-int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s) {
+namespace {
+
+DwArgs make_dw_args(const Layer &L, const fqt_qgrad &q, const uint64_t *xsign, float *dW,
+                    int32_t *I_out, void *ws) {
   const uint32_t ktiles = uint32_t((L.K + 31) / 32);
   const uint32_t S = uint32_t(gemm_dw_splits(L));
   DwArgs a;
@@ -476,23 +510,15 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   a.xsign_bytes = uint32_t(L.Wr * L.K * 8);
   a.S = S; a.wps = uint32_t((L.Wr + S - 1) / S);
   a.divS = make_fastdiv(S); a.divKt = make_fastdiv(ktiles); a.divK = make_fastdiv(uint32_t(L.K));
-  const int64_t groups = (L.D + DW_RT * 32 - 1) / (DW_RT * 32);
-  const dim3 grid(unsigned(int64_t(S) * groups * ktiles));
-  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
-  if (cfg.bits == 8) {
-    hipLaunchKernelGGL(k_mfma_dw_part<true>, grid, dim3(DW_THREADS), 0, s, a);
-    hipLaunchKernelGGL(k_dw_finish<true>, fgrid, dim3(256), 0, s, a);
-  } else {
-    hipLaunchKernelGGL(k_mfma_dw_part<false>, grid, dim3(DW_THREADS), 0, s, a);
-    hipLaunchKernelGGL(k_dw_finish<false>, fgrid, dim3(256), 0, s, a);
-  }
-  return last_launch_status();
+  return a;
+}
+// Split-R partial blocks over the slot capacity: S x ceil(D/128) x ceil(K/32).
+uint32_t dw_part_blocks(const Layer &L, const DwArgs &a) {
+  return a.S * uint32_t((L.D + DW_RT * 32 - 1) / (DW_RT * 32)) * a.ktiles;
 }
 
-int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
-                   const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
-                   hipStream_t s) {
-  if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
+DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
+                    const int32_t *wlsum, void *dX, int32_t *I_out) {
   DxArgs a;
   a.codes = q.psq_codes; a.kept = q.psq_kept; a.count = q.psq_count;
   a.scale = q.psq_scale; a.offset = q.psq_offset; a.wsb = wsb; a.wlsum = wlsum;
@@ -510,14 +536,67 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   a.divHW = make_fastdiv(uint32_t(L.HW)); a.divW = make_fastdiv(uint32_t(L.W));
   a.divKw = make_fastdiv(uint32_t(L.kw)); a.divNch = make_fastdiv(a.nch);
   a.divCt = make_fastdiv(a.ctiles);
-  const int64_t zb = std::min<int64_t>(256, L.N);
-  const dim3 grid(unsigned(((L.N * L.HW + 31) / 32) * a.ctiles + zb));
+  // Capacity tiles plus a pool of blocks that only zero pruned samples: whatever the
+  // device-side count, at least min(256, N) blocks are left for the zeroing.
+  a.nblocks = uint32_t(((L.N * L.HW + 31) / 32) * a.ctiles + std::min<int64_t>(256, L.N));
+  return a;
+}
+// Contraction steps of one dX wave, rounded to the instantiated batch depths (at most
+// 10 steps per batch keeps three resident blocks per CU).
+int dx_batch(const DxArgs &a) {
   const uint32_t per_wave = (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
+  return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;
+}
+
+}  // namespace
+
+int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                   const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s) {
+  const DwArgs a = make_dw_args(L, q, xsign, dW, I_out, ws);
+  const dim3 grid(dw_part_blocks(L, a));
+  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
+  if (cfg.bits == 8) {
+    hipLaunchKernelGGL(k_mfma_dw_part<true>, grid, dim3(DW_THREADS), 0, s, a);
+    hipLaunchKernelGGL(k_dw_finish<true>, fgrid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(k_mfma_dw_part<false>, grid, dim3(DW_THREADS), 0, s, a);
+    hipLaunchKernelGGL(k_dw_finish<false>, fgrid, dim3(256), 0, s, a);
+  }
+  return last_launch_status();
+}
+
+int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                   const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
+                   hipStream_t s) {
+  if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
+  const DxArgs a = make_dx_args(L, q, wsb, wlsum, dX, I_out);
+  const dim3 grid(a.nblocks);
+  const int nb = dx_batch(a);
   auto go = [&]<bool B8>() {
-    // Batches of at most 10 steps keep the kernel at three resident blocks per CU.
-    if (per_wave <= 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4>), grid, dim3(DX_THREADS), 0, s, a);
-    else if (per_wave <= 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8>), grid, dim3(DX_THREADS), 0, s, a);
+    if (nb == 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (nb == 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8>), grid, dim3(DX_THREADS), 0, s, a);
     else hipLaunchKernelGGL((k_mfma_dx<B8, 10>), grid, dim3(DX_THREADS), 0, s, a);
+  };
+  if (cfg.bits == 8) go.template operator()<true>();
+  else go.template operator()<false>();
+  return last_launch_status();
+}
+
+int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                    const uint64_t *xsign, const int8_t *wsb, const int32_t *wlsum, void *dX,
+                    float *dW, void *dw_ws, hipStream_t s) {
+  if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
+  const DwArgs dwa = make_dw_args(L, q, xsign, dW, nullptr, dw_ws);
+  const DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
+  const uint32_t ndw = dw_part_blocks(L, dwa);
+  const dim3 grid(ndw + dxa.nblocks);
+  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
+  const int nb = dx_batch(dxa);
+  auto go = [&]<bool B8>() {
+    if (nb == 4) hipLaunchKernelGGL((k_products<B8, 4>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    else if (nb == 8) hipLaunchKernelGGL((k_products<B8, 8>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    else hipLaunchKernelGGL((k_products<B8, 10>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    hipLaunchKernelGGL(k_dw_finish<B8>, fgrid, dim3(256), 0, s, dwa);
   };
   if (cfg.bits == 8) go.template operator()<true>();
   else go.template operator()<false>();

@@ -91,6 +91,10 @@ int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, 
 int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                    const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
                    hipStream_t s);
+// Both products of the layer backward in one launch, then the dW finish pass.
+int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                    const uint64_t *xsign, const int8_t *wsb, const int32_t *wlsum, void *dX,
+                    float *dW, void *dw_ws, hipStream_t s);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }
