@@ -121,143 +121,98 @@ struct DwArgs {
   int32_t *I_out;                // [D][K] or null
   int32_t *part;                 // [S][D][K] partial sums of each split (slots < count)
   int32_t *partT;                // [S][K] set bits of each split of each sign line
-  uint32_t D, K, R, Rp, Wr, ktiles, codes_bytes, xsign_bytes, S, wps;
-  FastDiv divS, divKt, divK;
+  uint32_t D, K, R, Rp, Wr, ktiles, kgroups, codes_bytes, xsign_bytes, S, wps;
+  FastDiv divS, divKg, divK;
 };
 
-constexpr int DW_RT = 4;                    // 32-row tiles of kept channels per block
-constexpr int DW_WAVES = 4;
+constexpr int DW_WAVES = 4;                 // column tiles per block, one per wave
 constexpr int DW_THREADS = DW_WAVES * 64;
-constexpr int DW_PREF = 2;                  // 64-bit words of the contraction loaded per batch
+constexpr int DW_PREF = 8;                  // 64-bit words of the contraction loaded per batch
 
-// The contraction of one wave for NRT live slot tiles: words c0, c0 + DW_WAVES, ... below
-// w_end, DW_PREF words per batch.  Every batch issues all its loads before the first
-// product (a sched_barrier keeps the compiler from sinking them), so a batch costs one
-// memory latency; words past w_end are skipped by a uniform test.
-template <int NRT, bool B8>
+// The contraction of one wave's 32x32 tile over the words [c_first, w_end) of its split,
+// DW_PREF words per batch.  Every batch issues all its loads before the first product (a
+// sched_barrier keeps the compiler from sinking them), so a batch costs one memory
+// latency; past w_end the loads read word c0 again (in bounds) and a uniform test skips
+// the products.
+template <bool B8>
 __device__ __forceinline__ void dw_accumulate(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
-                                              __amdgpu_buffer_rsrc_t xrs,
-                                              const uint32_t (&aoff)[DW_RT], uint32_t boff,
-                                              uint32_t c_first, uint32_t w_end, int g,
-                                              v16i (&acc)[DW_RT], uint32_t &tpart) {
+                                              __amdgpu_buffer_rsrc_t xrs, uint32_t aoff,
+                                              uint32_t boff, uint32_t c_first, uint32_t w_end,
+                                              int g, v16i &acc, uint32_t &tpart) {
   const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
-  for (uint32_t c0 = c_first; c0 < w_end; c0 += DW_WAVES * DW_PREF) {
+  for (uint32_t c0 = c_first; c0 < w_end; c0 += DW_PREF) {
     uint64_t word[DW_PREF];
-    v4i A[DW_PREF][2][NRT];
+    v4i A[DW_PREF][2];
 #pragma unroll
     for (int u = 0; u < DW_PREF; ++u) {
-      // Past the split's last word the loads read word c0 again (in bounds).
-      const uint32_t c = c0 + u * DW_WAVES < w_end ? c0 + u * DW_WAVES : c0;
+      const uint32_t c = c0 + u < w_end ? c0 + u : c0;
       word[u] = load8(xrs, boff, c * a.K * 8);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt)
-          A[u][h][rt] = load16(crs, aoff[rt], (2 * c + h) * chunk_bytes);
+      for (int h = 0; h < 2; ++h) A[u][h] = load16(crs, aoff, (2 * c + h) * chunk_bytes);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < DW_PREF; ++u) {
-      if (c0 + u * DW_WAVES >= w_end) break;
+      if (c0 + u >= w_end) break;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const uint32_t bits = uint32_t(word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
         tpart += __popc(bits);
-        const v4i B = signs16(bits);
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt)
-          acc[rt] = mfma_i8(B8 ? bias128(A[u][h][rt]) : A[u][h][rt], B, acc[rt]);
+        acc = mfma_i8(B8 ? bias128(A[u][h]) : A[u][h], signs16(bits), acc);
       }
     }
   }
 }
 
-// Split-R partial products.  Grid: S splits x ceil(D/128) slot groups x ceil(K/32) column
-// tiles over the slot capacity, the split index fastest (consecutive blocks land on
-// different XCDs, so each XCD reads its own slices of the codes and of the signs).  A block
-// of a live group (slot group below ceil(count/128)) holds up to four 32x32 MFMA tiles,
-// the live slot tiles of its group over 32 columns, for the words [s*wps, (s+1)*wps) of
-// the contraction over N*Ho*Wo; its four waves take every fourth word, expand each 16-bit
-// piece of their column's word once and feed it to every tile.  The four partial tiles
-// meet in LDS; the block writes its sum and its set-bit counts to the split's slice.
-struct DwPartLds {
-  int32_t red[DW_WAVES - 1][DW_RT][16][64];
-  int32_t tred[32];
-};
-
+// Split-R partial products.  Grid: S splits x ceil(ceil(K/32) / 4) column groups x
+// ceil(D/32) slot tiles over the slot capacity, the split index fastest (consecutive
+// blocks land on different XCDs, so each XCD reads its own slices of the codes and of the
+// signs) and the slot tile slowest (blocks past the kept channels exit at once).  Wave w
+// of a block computes the 32x32 MFMA tile (slot tile, column tile 4 * group + w) over the
+// words [s * wps, (s + 1) * wps) of the contraction over N*Ho*Wo: the four waves read the
+// same code rows (one fetch from L2) and their own sign columns, and each writes its tile
+// and the set-bit counts of its columns to the split's slice.  No LDS, no barrier.
 template <bool B8>
-__device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid, DwPartLds &sm) {
-  const int t = threadIdx.x, lane = t & 63;
+__device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
+  const int lane = threadIdx.x & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
   const uint32_t rest = fdiv(bid, a.divS);
   const uint32_t sp = bid - rest * a.S;
-  const uint32_t grp = fdiv(rest, a.divKt);
-  const uint32_t j0 = grp * (DW_RT * 32), k0 = (rest - grp * a.ktiles) * 32;
-  if (int(j0) >= count) return;               // slot group past the kept channels
-  const int nrt = min(DW_RT, (count - int(j0) + 31) / 32);   // live slot tiles, >= 1
-  if (t < 32) sm.tred[t] = 0;
+  const uint32_t rt = fdiv(rest, a.divKg);
+  const uint32_t kt = (rest - rt * a.kgroups) * DW_WAVES + wave;
+  const uint32_t j0 = rt * 32;
+  if (int(j0) >= count || kt >= a.ktiles) return;   // past the kept channels or the columns
 
   const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
   const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
-  uint32_t aoff[DW_RT];
-#pragma unroll
-  for (int rt = 0; rt < DW_RT; ++rt) {
-    const uint32_t j = j0 + 32 * rt + i;
-    aoff[rt] = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
-  }
-  const uint32_t kc = k0 + i;
+  const uint32_t j = j0 + i;
+  const uint32_t aoff = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
+  const uint32_t kc = kt * 32 + i;
   const bool b_ok = kc < a.K;
   const uint32_t boff = b_ok ? kc * 8 : BUF_NONE;
   const uint32_t w_end = min(a.Wr, (sp + 1) * a.wps);
-  const uint32_t c_first = sp * a.wps + wave;
-
-  v16i acc[DW_RT];
-#pragma unroll
-  for (int rt = 0; rt < DW_RT; ++rt) acc[rt] = v16i{0};
+  v16i acc = v16i{0};
   uint32_t tpart = 0;
-  switch (nrt) {
-    case 1: dw_accumulate<1, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
-    case 2: dw_accumulate<2, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
-    case 3: dw_accumulate<3, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
-    default: dw_accumulate<4, B8>(a, crs, xrs, aoff, boff, c_first, w_end, g, acc, tpart); break;
-  }
-  __syncthreads();                      // tred is initialised
-  atomicAdd(&sm.tred[i], int(tpart));
-  if (wave > 0) {
-#pragma unroll
-    for (int rt = 0; rt < DW_RT; ++rt) {
-      if (rt >= nrt) break;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sm.red[wave - 1][rt][v][lane] = acc[rt][v];
-    }
-  }
-  __syncthreads();
-  if (wave != 0 || !b_ok) return;
-  if (g == 0) a.partT[size_t(sp) * a.K + kc] = sm.tred[i];
+  dw_accumulate<B8>(a, crs, xrs, aoff, boff, sp * a.wps, w_end, g, acc, tpart);
+
+  // Set bits of column kc in this split: lanes i and i + 32 counted the two halves of
+  // every 32-bit piece.
+  const uint32_t T = tpart + lane_xor<32>(tpart);
+  if (!b_ok) return;
+  if (rt == 0 && g == 0) a.partT[size_t(sp) * a.K + kc] = int32_t(T);
   int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.K + kc;
 #pragma unroll
-  for (int rt = 0; rt < DW_RT; ++rt) {
-    if (rt >= nrt) break;
-    // All partial sums first (the LDS reads issue back to back), then the stores.
-#pragma unroll
-    for (int w = 0; w < DW_WAVES - 1; ++w)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[rt][v] += sm.red[w][rt][v][lane];
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = 32 * rt + acc_row(v, g);
-      if (int(j0) + row < count) out[size_t(row) * a.K] = acc[rt][v];
-    }
+  for (int v = 0; v < 16; ++v) {
+    const int row = acc_row(v, g);
+    if (int(j0) + row < count) out[size_t(row) * a.K] = acc[v];
   }
 }
 
 template <bool B8>
 __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
-  __shared__ DwPartLds sm;
-  dw_part_body<B8>(a, blockIdx.x, sm);
+  dw_part_body<B8>(a, blockIdx.x);
 }
 
 // dW from the split partials: one thread per element (slot, k) of the slot capacity.  A
@@ -319,14 +274,17 @@ constexpr int DX_THREADS = DX_WAVES * 64;
 // channels) so output lanes run along pixels.  Its four waves take every fourth
 // contraction step (tap, 32 bytes of D).  For tap (i, j) a pixel (h, w) reads the code row
 // of the output pixel (ho, wo) with ho*sh - ph + i = h and wo*sw - pw + j = w, or nothing;
-// the byte offset of every (tap, pixel) row is tabulated once per block.
-struct DxLds {
+// the byte offset of every (tap, pixel) row is tabulated once per block, next to the sign
+// sums of the block's channels per tap.  The four partial tiles meet in LDS and wave w
+// finishes accumulator registers 4w .. 4w + 3 (channel rows 8w + 4g + u): their integer
+// sums, the zero-point term c = sum of the channel's sign sums over the taps that reach
+// the pixel (exact integers), the rescale and the stores.
+struct alignas(16) DxLds {
   uint32_t rowoff[DX_MAX_TAPS][32];     // 32 * code row, BUF_NONE if none
-  int32_t redi[DX_WAVES - 1][16][64];
-  float redf[DX_WAVES - 1][16][64];
+  int32_t wl[DX_MAX_TAPS][32];          // sign sum of line (channel c0 + k, tap), 0 past C
+  int32_t red[DX_WAVES][16][64];        // partial tiles of the four waves
   int32_t pix_out[32];                  // NCHW offset of (sample, pixel) minus channel
   float pix_s[32], pix_z[32];
-  int32_t ltot[32];                     // b = 8: sum of every sign of the channel
 };
 
 template <bool B8, int NB>
@@ -351,23 +309,6 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   const uint32_t m0 = mt * 32, c0 = (bid - mt * a.ctiles) * 32;
   const int taps = int(a.taps);
 
-  for (int e = t; e < 32 * taps; e += DX_THREADS) {
-    const int p = e & 31, tap = e >> 5;
-    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
-    const uint32_t m = m0 + p;
-    uint32_t off = BUF_NONE;
-    if (m < live_rows) {
-      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
-      const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
-      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
-      if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
-        const int ho = th / a.sh, wo = tw / a.sw;
-        if (ho < int(a.Ho) && wo < int(a.Wo))
-          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
-      }
-    }
-    sm.rowoff[tap][p] = off;
-  }
   if (t < 32) {
     const uint32_t m = m0 + t;
     int off = -1;
@@ -382,12 +323,25 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
     sm.pix_out[t] = off;
     sm.pix_s[t] = sc;
     sm.pix_z[t] = zo;
-  } else if (B8 && t < 64) {
-    const uint32_t ch = c0 + uint32_t(t - 32);
-    int s = 0;
-    if (ch < a.C)
-      for (int tap = 0; tap < taps; ++tap) s += a.wlsum[ch * a.taps + tap];
-    sm.ltot[t - 32] = s;
+  }
+  for (int e = t; e < 32 * taps; e += DX_THREADS) {
+    const int p = e & 31, tap = e >> 5;
+    const uint32_t ch = c0 + uint32_t(p);
+    sm.wl[tap][p] = ch < a.C ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
+    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
+    const uint32_t m = m0 + p;
+    uint32_t off = BUF_NONE;
+    if (m < live_rows) {
+      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
+      const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
+      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
+      if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
+        const int ho = th / a.sh, wo = tw / a.sw;
+        if (ho < int(a.Ho) && wo < int(a.Wo))
+          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
+      }
+    }
+    sm.rowoff[tap][p] = off;
   }
   __syncthreads();
 
@@ -417,49 +371,36 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
     for (int u = 0; u < NB; ++u) acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
   }
 
-  // Zero-point term over this wave's taps: c[ch][pixel] = sum of wlsum[ch][tap] over the
-  // taps that reach the pixel, as a float32 MFMA taking two taps per step.
-  v16f cacc = {0.0f};
-  for (int tp = 2 * int(wave); tp < taps; tp += 2 * DX_WAVES) {
-    const int tap = tp + g;
-    const bool tv = tap < taps;
-    const float av = (tv && ch < a.C) ? float(a.wlsum[ch * a.taps + tap]) : 0.0f;
-    const float bv = (tv && sm.rowoff[tv ? tap : 0][i] != BUF_NONE) ? 1.0f : 0.0f;
-    cacc = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, cacc, 0, 0, 0);
-  }
-
-  if (wave > 0) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      sm.redi[wave - 1][v][lane] = acc[v];
-      sm.redf[wave - 1][v][lane] = cacc[v];
-    }
-  }
+  for (int v = 0; v < 16; ++v) sm.red[wave][v][lane] = acc[v];
   __syncthreads();
-  if (wave != 0) return;
-#pragma unroll
-  for (int w = 0; w < DX_WAVES - 1; ++w)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      acc[v] += sm.redi[w][v][lane];
-      cacc[v] += sm.redf[w][v][lane];
-    }
-
   const int off = sm.pix_out[i];
   if (off < 0) return;                    // rows past the count belong to the zero blocks
   const float S = sm.pix_s[i], Z = sm.pix_z[i];
-  __builtin_amdgcn_sched_barrier(0);      // every LDS read above issues before the stores
+  const int r0 = 8 * int(wave) + 4 * g;   // channel rows r0 .. r0 + 3 of this lane
+  int I[4], c[4] = {0, 0, 0, 0}, lt[4] = {0, 0, 0, 0};
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int crow = acc_row(v, g);
-    const uint32_t cc = c0 + crow;
+  for (int u = 0; u < 4; ++u) {
+    const int v = 4 * int(wave) + u;
+    I[u] = sm.red[0][v][lane] + sm.red[1][v][lane] + sm.red[2][v][lane] + sm.red[3][v][lane];
+  }
+  for (int tap = 0; tap < taps; ++tap) {
+    const bool reach = sm.rowoff[tap][i] != BUF_NONE;
+    const int4 w4 = *reinterpret_cast<const int4 *>(&sm.wl[tap][r0]);
+    c[0] += reach ? w4.x : 0; c[1] += reach ? w4.y : 0;
+    c[2] += reach ? w4.z : 0; c[3] += reach ? w4.w : 0;
+    if (B8) { lt[0] += w4.x; lt[1] += w4.y; lt[2] += w4.z; lt[3] += w4.w; }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t cc = c0 + uint32_t(r0 + u);
     if (cc >= a.C) continue;
-    const int I = acc[v] + (B8 ? 128 * sm.ltot[crow] : 0);
-    const float out = rescale(S, I, Z, cacc[v]);
+    const int Iu = I[u] + (B8 ? 128 * lt[u] : 0);
+    const float out = rescale(S, Iu, Z, float(c[u]));
     const size_t o = size_t(off) + size_t(cc) * a.HW;
     if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
     else static_cast<float *>(a.dX)[o] = out;
-    if (a.I_out) a.I_out[o] = I;
+    if (a.I_out) a.I_out[o] = Iu;
   }
 }
 
@@ -471,15 +412,11 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
 
 // Both products in one launch (the layer backward): blocks [0, ndw) are dW split-R
 // partial blocks, the rest dX blocks; the two share the LDS allocation.
-union ProductsLds {
-  DxLds dx;
-  DwPartLds dw;
-};
 template <bool B8, int NB>
 __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
-  __shared__ ProductsLds sm;
-  if (blockIdx.x < ndw) dw_part_body<B8>(dwa, blockIdx.x, sm.dw);
-  else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
+  __shared__ DxLds sm;
+  if (blockIdx.x < ndw) dw_part_body<B8>(dwa, blockIdx.x);
+  else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm);
 }
 
 }  // namespace
@@ -508,13 +445,14 @@ DwArgs make_dw_args(const Layer &L, const fqt_qgrad &q, const uint64_t *xsign, f
   a.Rp = uint32_t(L.Wr * 64); a.Wr = uint32_t(L.Wr); a.ktiles = ktiles;
   a.codes_bytes = uint32_t(L.D * L.Wr * 64);
   a.xsign_bytes = uint32_t(L.Wr * L.K * 8);
+  a.kgroups = (ktiles + DW_WAVES - 1) / DW_WAVES;
   a.S = S; a.wps = uint32_t((L.Wr + S - 1) / S);
-  a.divS = make_fastdiv(S); a.divKt = make_fastdiv(ktiles); a.divK = make_fastdiv(uint32_t(L.K));
+  a.divS = make_fastdiv(S); a.divKg = make_fastdiv(a.kgroups); a.divK = make_fastdiv(uint32_t(L.K));
   return a;
 }
-// Split-R partial blocks over the slot capacity: S x ceil(D/128) x ceil(K/32).
+// Split-R partial blocks over the slot capacity: S x ceil(ceil(K/32) / 4) x ceil(D/32).
 uint32_t dw_part_blocks(const Layer &L, const DwArgs &a) {
-  return a.S * uint32_t((L.D + DW_RT * 32 - 1) / (DW_RT * 32)) * a.ktiles;
+  return a.S * a.kgroups * uint32_t((L.D + 31) / 32);
 }
 
 DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
@@ -541,8 +479,8 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
   a.nblocks = uint32_t(((L.N * L.HW + 31) / 32) * a.ctiles + std::min<int64_t>(256, L.N));
   return a;
 }
-// Contraction steps of one dX wave, rounded to the instantiated batch depths (at most
-// 10 steps per batch keeps three resident blocks per CU).
+// Contraction steps of one dX wave, rounded to the instantiated batch depths (10 steps
+// per batch still leaves four resident blocks per CU).
 int dx_batch(const DxArgs &a) {
   const uint32_t per_wave = (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
   return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;

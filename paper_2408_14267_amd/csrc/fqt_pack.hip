@@ -276,39 +276,45 @@ unsigned blocks_for(int64_t items) { return unsigned((items + WAVES - 1) / WAVES
 // l = (c, tap)); byte d of line l is +1 if W[d][l] > 0 else -1 for d < D, 0 for
 // D <= d < Dp, stored chunk-major at ((d/32 * taps + tap) * C + c) * 32 + d % 32 so that the
 // 32-byte chunks of consecutive channels are adjacent; lsum[l] = sum over d < D of the
-// line.  One block per 64 lines walks D in 64-row tiles, transposed through LDS (pitch 68
-// bytes = 17 dwords: the column writes of a wave spread over the banks).
-constexpr int WB_PITCH = 68;
+// line.  One block of 1024 threads per 64 lines walks D in passes of 256 rows (one pass
+// for D <= 256): each thread loads 16 rows of its line back to back, the pass is
+// transposed through LDS (pitch 260 bytes = 65 dwords: the column writes of a wave spread
+// over the banks) and written as 16-byte pieces of the 32-byte chunks.
+constexpr int WB_THREADS = 1024;
+constexpr int WB_ROWS = 256;                  // rows of D per pass: 16 per thread
+constexpr int WB_PITCH = WB_ROWS + 4;
 template <int DT>
-__global__ __launch_bounds__(THREADS) void k_pack_w_i8(const void *__restrict__ w, uint32_t D,
-                                                       uint32_t K, uint32_t Dp, uint32_t C,
-                                                       uint32_t taps, FastDiv div_taps,
-                                                       int8_t *__restrict__ dst,
-                                                       int32_t *__restrict__ lsum) {
-  __shared__ int8_t tile[64][WB_PITCH];
+__global__ __launch_bounds__(WB_THREADS) void k_pack_w_i8(const void *__restrict__ w, uint32_t D,
+                                                          uint32_t K, uint32_t Dp, uint32_t C,
+                                                          uint32_t taps, FastDiv div_taps,
+                                                          int8_t *__restrict__ dst,
+                                                          int32_t *__restrict__ lsum) {
+  constexpr int Q = WB_THREADS / 64;          // row phases per pass
+  __shared__ __align__(16) int8_t tile[64][WB_PITCH];
   __shared__ int32_t pos[64];
   const int t = threadIdx.x, line = t & 63, q = t >> 6;
   const uint32_t l0 = blockIdx.x * 64, l = l0 + line;
   if (t < 64) pos[t] = 0;
   int mine = 0;
-  for (uint32_t d0 = 0; d0 < Dp; d0 += 64) {
-    float v[16];
+  for (uint32_t d0 = 0; d0 < Dp; d0 += WB_ROWS) {
+    float v[WB_ROWS / Q];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {   // unconditional loads (element 0 outside) issue back to back
-      const uint32_t d = d0 + 4 * k + q;
+    for (int k = 0; k < WB_ROWS / Q; ++k) {   // unconditional loads (element 0 outside) issue back to back
+      const uint32_t d = d0 + Q * k + q;
       v[k] = load_elem<DT>(w, (d < D && l < K) ? int64_t(d) * K + l : 0);
     }
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const uint32_t d = d0 + 4 * k + q;
+    for (int k = 0; k < WB_ROWS / Q; ++k) {
+      const uint32_t d = d0 + Q * k + q;
       const bool in = d < D && l < K;
       const bool pos_sign = in && v[k] > 0.0f;
       mine += pos_sign ? 1 : 0;
-      tile[line][4 * k + q] = in ? (pos_sign ? int8_t(1) : int8_t(-1)) : int8_t(0);
+      tile[line][Q * k + q] = in ? (pos_sign ? int8_t(1) : int8_t(-1)) : int8_t(0);
     }
     __syncthreads();
-    const int wl = t >> 2, part = t & 3;
-    if (l0 + wl < K) {
+    // 64 lines x 16 pieces of 16 bytes; pieces past Dp (last pass of a short D) are not stored.
+    const int wl = t >> 4, part = t & 15;
+    if (l0 + wl < K && d0 + 16 * part < Dp) {
       const uint32_t lw = l0 + wl, c = fdiv(lw, div_taps), tap = lw - c * taps;
       const uint32_t chunk = (d0 >> 5) + (part >> 1);
       const uint32_t *src = reinterpret_cast<const uint32_t *>(&tile[wl][16 * part]);
@@ -328,7 +334,7 @@ int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, 
   const uint32_t D = uint32_t(L.D), K = uint32_t(L.K), Dp = uint32_t(L.Wd * 64);
   const uint32_t taps = uint32_t(L.kh * L.kw);
   dispatch_dtype(L.w_t, [&]<int DT>() {
-    hipLaunchKernelGGL(k_pack_w_i8<DT>, dim3(unsigned((L.K + 63) / 64)), dim3(THREADS), 0, s, W,
+    hipLaunchKernelGGL(k_pack_w_i8<DT>, dim3(unsigned((L.K + 63) / 64)), dim3(WB_THREADS), 0, s, W,
                        D, K, Dp, uint32_t(L.C), taps, make_fastdiv(taps), dst, lsum);
   });
   return last_launch_status();

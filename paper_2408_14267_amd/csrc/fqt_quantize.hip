@@ -28,6 +28,7 @@ constexpr int TILE = 64;
 constexpr int THREADS = 512;                 // tile kernels: 8 elements (2 quads) per thread
 constexpr int WAVES = THREADS / 64;
 constexpr int QUADS = TILE * TILE / (4 * THREADS);
+static_assert(TILE / WAVES == 8, "qpack stores 8 lines x 8 planes (or 8-byte code pieces) per wave");
 constexpr int PITCH = TILE + 4;   // bytes per LDS code row; 68 keeps transposed reads conflict-free
 
 // How a thread walks its 8 tile elements (2 quads of 4).
@@ -772,8 +773,8 @@ struct QPackArgs {
 
 template <int MODE, int DT>
 __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
-  __shared__ uint8_t cs[TILE][PITCH];   // PSQ codes, [rr][dd]
-  __shared__ uint8_t cc[TILE][PITCH];   // PCQ codes, [dd][rr]
+  __shared__ __align__(16) uint8_t cs[TILE][PITCH];   // PSQ codes, [rr][dd]
+  __shared__ __align__(16) uint8_t cc[TILE][PITCH];   // PCQ codes, [dd][rr]
   __shared__ GroupParam spar[TILE];     // sample params of each column rr
   __shared__ GroupParam cpar[TILE];     // channel params of each row dd
   __shared__ int32_t prow[TILE];        // PSQ row of column rr, -1 if pruned/outside
@@ -867,36 +868,55 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   }
   __syncthreads();
 
-  // PCQ: channel row dd of the tile, lanes along r (column encoder) and its 64 code bytes.
-  for (int i = 0; i < TILE / WAVES; ++i) {
+  // Each wave stores its 8 lines of each encoding (line i = wave + WAVES * i).  Lane
+  // 8 i + p keeps the ballot of plane p of line i, and lane 8 i + j then stores bytes
+  // 8 j .. 8 j + 7 of the line's 64 codes, so the planes and the codes of the 8 lines take
+  // one store instruction each.
+  // PCQ: channel rows dd, lanes along r (column encoder).
+  {
+    uint64_t pw = 0;
+#pragma unroll
+    for (int i = 0; i < TILE / WAVES; ++i) {
+      const uint32_t code = cc[wave + WAVES * i][lane];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        if (p >= a.bits) break;
+        const uint64_t m = __ballot((code >> p) & 1u);
+        pw = lane == 8 * i + p ? m : pw;
+      }
+    }
+    const int i = lane >> 3, j = lane & 7;
     const int dd = wave + WAVES * i;
-    if (d0 + dd >= g.D) break;
-    const int rank = cpar[dd].rank;
-    if (rank < 0) continue;
-    const uint32_t code = cc[dd][lane];
-    for (int p = 0; p < a.bits; ++p) {
-      const uint64_t m = __ballot((code >> p) & 1u);
-      if (lane == p) a.pcq[(size_t(p) * g.D + rank) * a.Wr + (r0 >> 6)] = m;
+    const int rank = cpar[dd].rank;             // -1 for pruned channels and past D
+    if (rank >= 0) {
+      if (j < a.bits) a.pcq[(size_t(j) * g.D + rank) * a.Wr + (r0 >> 6)] = pw;
+      const uint32_t *src = reinterpret_cast<const uint32_t *>(&cc[dd][8 * j]);
+      *reinterpret_cast<uint2 *>(a.pcq_codes + ((size_t(r0 >> 5) + (j >> 2)) * g.D + rank) * 32 +
+                                 8 * (j & 3)) = make_uint2(src[0], src[1]);
     }
-    if (lane < 16)        // lanes 0-7 fill 32-byte chunk r0/32, lanes 8-15 the next one
-      *reinterpret_cast<uint32_t *>(
-          a.pcq_codes + ((size_t(r0 >> 5) + (lane >> 3)) * g.D + rank) * 32 + 4 * (lane & 7)) =
-          reinterpret_cast<const uint32_t *>(&cc[dd][0])[lane];
   }
-  // PSQ: row rr of the tile, lanes along d (row encoder) and its 64 code bytes.
-  for (int i = 0; i < TILE / WAVES; ++i) {
-    const int rr = wave + WAVES * i;
-    const int row = prow[rr];
-    if (row < 0) continue;
-    const uint32_t code = cs[rr][lane];
-    for (int p = 0; p < a.bits; ++p) {
-      const uint64_t m = __ballot((code >> p) & 1u);
-      if (lane == p) a.psq[(size_t(p) * g.R + row) * a.Wd + (d0 >> 6)] = m;
+  // PSQ: sample rows rr, lanes along d (row encoder).
+  {
+    uint64_t pw = 0;
+#pragma unroll
+    for (int i = 0; i < TILE / WAVES; ++i) {
+      const uint32_t code = cs[wave + WAVES * i][lane];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        if (p >= a.bits) break;
+        const uint64_t m = __ballot((code >> p) & 1u);
+        pw = lane == 8 * i + p ? m : pw;
+      }
     }
-    if (lane < 16)
-      *reinterpret_cast<uint32_t *>(
-          a.psq_codes + ((size_t(d0 >> 5) + (lane >> 3)) * g.R + row) * 32 + 4 * (lane & 7)) =
-          reinterpret_cast<const uint32_t *>(&cs[rr][0])[lane];
+    const int i = lane >> 3, j = lane & 7;
+    const int rr = wave + WAVES * i;
+    const int row = prow[rr];                   // -1 for pruned samples and past R
+    if (row >= 0) {
+      if (j < a.bits) a.psq[(size_t(j) * g.R + row) * a.Wd + (d0 >> 6)] = pw;
+      const uint32_t *src = reinterpret_cast<const uint32_t *>(&cs[rr][8 * j]);
+      *reinterpret_cast<uint2 *>(a.psq_codes + ((size_t(d0 >> 5) + (j >> 2)) * g.R + row) * 32 +
+                                 8 * (j & 3)) = make_uint2(src[0], src[1]);
+    }
   }
 }
 
