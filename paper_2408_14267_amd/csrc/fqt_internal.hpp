@@ -240,6 +240,25 @@ __device__ __forceinline__ uint64_t lane_xor64(uint64_t v) {
   return (uint64_t(lane_xor<M>(uint32_t(v >> 32))) << 32) | lane_xor<M>(uint32_t(v));
 }
 
+// Write the wave-uniform value v into lane `l` of `old` (v_writelane_b32; the LLVM
+// intrinsic has no clang builtin here).
+extern "C" __device__ int fqt_llvm_writelane(int v, int l, int old) __asm("llvm.amdgcn.writelane.i32");
+__device__ __forceinline__ uint32_t writelane(uint32_t v, int l, uint32_t old) {
+  return uint32_t(fqt_llvm_writelane(int(v), l, int(old)));
+}
+
+// 8 x 8 bit-matrix transpose of x, byte k = row k, LSB first: byte p of the result holds
+// bit p of every byte k of x at bit k (three delta swaps).
+__device__ __forceinline__ uint64_t bit_transpose8(uint64_t x) {
+  uint64_t t = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
+  x ^= t ^ (t << 7);
+  t = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
+  x ^= t ^ (t << 14);
+  t = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
+  x ^= t ^ (t << 28);
+  return x;
+}
+
 // Inclusive scan of v over the wave's lanes under `op` with identity `id` (lane 63 ends
 // with the whole wave's result).
 template <typename Op>

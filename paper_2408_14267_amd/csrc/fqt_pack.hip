@@ -221,10 +221,8 @@ __global__ __launch_bounds__(THREADS) void k_pack_im2col_band(const void *__rest
   int filled = 0;
   uint64_t *out = dst + size_t(w) * g.K;
   auto put = [&](uint64_t m, uint32_t line_last) {
-    if (lane == filled) {
-      mlo = uint32_t(m);
-      mhi = uint32_t(m >> 32);
-    }
+    mlo = writelane(uint32_t(m), filled, mlo);
+    mhi = writelane(uint32_t(m >> 32), filled, mhi);
     if (++filled == 64) {                        // 64 words of consecutive lines
       out[line_last - 63 + lane] = (uint64_t(mhi) << 32) | mlo;
       filled = 0;

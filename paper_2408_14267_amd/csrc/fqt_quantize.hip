@@ -28,7 +28,7 @@ constexpr int TILE = 64;
 constexpr int THREADS = 512;                 // tile kernels: 8 elements (2 quads) per thread
 constexpr int WAVES = THREADS / 64;
 constexpr int QUADS = TILE * TILE / (4 * THREADS);
-static_assert(TILE / WAVES == 8, "qpack stores 8 lines x 8 planes (or 8-byte code pieces) per wave");
+static_assert(TILE / WAVES == 8, "qpack: a wave stores 8 lines, 8 lanes per line");
 constexpr int PITCH = TILE + 4;   // bytes per LDS code row; 68 keeps transposed reads conflict-free
 
 // How a thread walks its 8 tile elements (2 quads of 4).
@@ -775,6 +775,7 @@ template <int MODE, int DT>
 __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   __shared__ __align__(16) uint8_t cs[TILE][PITCH];   // PSQ codes, [rr][dd]
   __shared__ __align__(16) uint8_t cc[TILE][PITCH];   // PCQ codes, [dd][rr]
+  __shared__ __align__(8) uint8_t pbuf[WAVES][8][8][8];  // per wave: [line][plane][8-code chunk]
   __shared__ GroupParam spar[TILE];     // sample params of each column rr
   __shared__ GroupParam cpar[TILE];     // channel params of each row dd
   __shared__ int32_t prow[TILE];        // PSQ row of column rr, -1 if pruned/outside
@@ -869,53 +870,45 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   __syncthreads();
 
   // Each wave stores its 8 lines of each encoding (line i = wave + WAVES * i).  Lane
-  // 8 i + p keeps the ballot of plane p of line i, and lane 8 i + j then stores bytes
-  // 8 j .. 8 j + 7 of the line's 64 codes, so the planes and the codes of the 8 lines take
-  // one store instruction each.
+  // 8 i + k holds code bytes 8 k .. 8 k + 7 of line i: it stores them, transposes them as
+  // an 8 x 8 bit matrix (byte p = plane p of those 8 codes) and leaves the plane bytes in
+  // LDS, from where lane 8 i + p reads the whole 64-bit word of plane p.
+  const int li = lane >> 3, lk = lane & 7;
   // PCQ: channel rows dd, lanes along r (column encoder).
   {
-    uint64_t pw = 0;
-#pragma unroll
-    for (int i = 0; i < TILE / WAVES; ++i) {
-      const uint32_t code = cc[wave + WAVES * i][lane];
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        if (p >= a.bits) break;
-        const uint64_t m = __ballot((code >> p) & 1u);
-        pw = lane == 8 * i + p ? m : pw;
-      }
-    }
-    const int i = lane >> 3, j = lane & 7;
-    const int dd = wave + WAVES * i;
+    const int dd = wave + WAVES * li;
     const int rank = cpar[dd].rank;             // -1 for pruned channels and past D
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(&cc[dd][8 * lk]);
+    const uint32_t lo = src[0], hi = src[1];
+    const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+      if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
+    __builtin_amdgcn_wave_barrier();            // LDS operations of a wave run in order
+    const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
     if (rank >= 0) {
-      if (j < a.bits) a.pcq[(size_t(j) * g.D + rank) * a.Wr + (r0 >> 6)] = pw;
-      const uint32_t *src = reinterpret_cast<const uint32_t *>(&cc[dd][8 * j]);
-      *reinterpret_cast<uint2 *>(a.pcq_codes + ((size_t(r0 >> 5) + (j >> 2)) * g.D + rank) * 32 +
-                                 8 * (j & 3)) = make_uint2(src[0], src[1]);
+      *reinterpret_cast<uint2 *>(a.pcq_codes + ((size_t(r0 >> 5) + (lk >> 2)) * g.D + rank) * 32 +
+                                 8 * (lk & 3)) = make_uint2(lo, hi);
+      if (lk < a.bits) a.pcq[(size_t(lk) * g.D + rank) * a.Wr + (r0 >> 6)] = pw;
     }
   }
+  __builtin_amdgcn_wave_barrier();
   // PSQ: sample rows rr, lanes along d (row encoder).
   {
-    uint64_t pw = 0;
-#pragma unroll
-    for (int i = 0; i < TILE / WAVES; ++i) {
-      const uint32_t code = cs[wave + WAVES * i][lane];
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        if (p >= a.bits) break;
-        const uint64_t m = __ballot((code >> p) & 1u);
-        pw = lane == 8 * i + p ? m : pw;
-      }
-    }
-    const int i = lane >> 3, j = lane & 7;
-    const int rr = wave + WAVES * i;
+    const int rr = wave + WAVES * li;
     const int row = prow[rr];                   // -1 for pruned samples and past R
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(&cs[rr][8 * lk]);
+    const uint32_t lo = src[0], hi = src[1];
+    const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+      if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
+    __builtin_amdgcn_wave_barrier();
+    const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
     if (row >= 0) {
-      if (j < a.bits) a.psq[(size_t(j) * g.R + row) * a.Wd + (d0 >> 6)] = pw;
-      const uint32_t *src = reinterpret_cast<const uint32_t *>(&cs[rr][8 * j]);
-      *reinterpret_cast<uint2 *>(a.psq_codes + ((size_t(d0 >> 5) + (j >> 2)) * g.R + row) * 32 +
-                                 8 * (j & 3)) = make_uint2(src[0], src[1]);
+      *reinterpret_cast<uint2 *>(a.psq_codes + ((size_t(d0 >> 5) + (lk >> 2)) * g.R + row) * 32 +
+                                 8 * (lk & 3)) = make_uint2(lo, hi);
+      if (lk < a.bits) a.psq[(size_t(lk) * g.R + row) * a.Wd + (d0 >> 6)] = pw;
     }
   }
 }
