@@ -313,13 +313,19 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   carve_layer_ws(ws, L, cfg->bits, &w);
   const hipStream_t s = static_cast<hipStream_t>(hip_stream);
   if (L.kh * L.kw > 64) return FQT_E_SHAPE;
-  if (L.kind == FQT_LINEAR)
-    FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,
-                             nullptr, s, true));
-  else
-    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s, true));
-  FQT_TRY(launch_pack_w_i8(W, L, w.wsb, w.wlsum, s));
-  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s));
+  // Statistics, then the selection (whose launch also packs the sign operands when the
+  // layer allows), the quantizer, both products.
+  SignJob sj{X, W, w.xsign, w.wsb, w.wlsum, false};
+  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s, &sj));
+  if (!sj.done) {
+    if (L.kind == FQT_LINEAR)
+      FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,
+                               nullptr, s, true));
+    else
+      FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, w.xsign, nullptr, s,
+                               true));
+    FQT_TRY(launch_pack_w_i8(W, L, w.wsb, w.wlsum, s));
+  }
   return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, s);
 }
 

@@ -36,22 +36,6 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr uint32_t BUF_NONE = 0x80000000u;   // every buffer here is shorter than 2^31 bytes
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, uint32_t bytes) {
-  // Raw buffer (stride 0) of `bytes` bytes; 0x00020000 is the gfx9 32-bit data format.
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
-                                           static_cast<int>(bytes), 0x00020000);
-}
-
-// 16 bytes at byte offset voff + soff of buffer r (soff wave-uniform: it rides in an SGPR).
-__device__ __forceinline__ v4i load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-__device__ __forceinline__ uint64_t load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
-}
-
 // The wave index as a scalar, so that per-wave loop bounds and strides stay in SGPRs.
 __device__ __forceinline__ uint32_t wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -119,10 +103,10 @@ struct DwArgs {
   const uint64_t *xsign;         // [Wr][K], word-major
   float *dW;                     // [D][K]
   int32_t *I_out;                // [D][K] or null
-  int32_t *part;                 // [S][D][K] partial sums of each split (slots < count)
-  int32_t *partT;                // [S][K] set bits of each split of each sign line
-  uint32_t D, K, R, Rp, Wr, ktiles, kgroups, codes_bytes, xsign_bytes, S, wps;
-  FastDiv divS, divKg, divK;
+  int32_t *part;                 // [S][D][Kp] partial sums of each split (slots < count)
+  int32_t *partT;                // [S][Kp] set bits of each split of each sign line
+  uint32_t D, K, Kp, R, Rp, Wr, ktiles, kgroups, codes_bytes, xsign_bytes, S, wps;
+  FastDiv divS, divKg, divQ;    // divQ: Kp / 4
 };
 
 constexpr int DW_WAVES = 4;                 // column tiles per block, one per wave
@@ -201,12 +185,12 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   // every 32-bit piece.
   const uint32_t T = tpart + lane_xor<32>(tpart);
   if (!b_ok) return;
-  if (rt == 0 && g == 0) a.partT[size_t(sp) * a.K + kc] = int32_t(T);
-  int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.K + kc;
+  if (rt == 0 && g == 0) a.partT[size_t(sp) * a.Kp + kc] = int32_t(T);
+  int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.Kp + kc;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int row = acc_row(v, g);
-    if (int(j0) + row < count) out[size_t(row) * a.K] = acc[v];
+    if (int(j0) + row < count) out[size_t(row) * a.Kp] = acc[v];
   }
 }
 
@@ -215,31 +199,45 @@ __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
   dw_part_body<B8>(a, blockIdx.x);
 }
 
-// dW from the split partials: one thread per element (slot, k) of the slot capacity.  A
-// kept slot sums its S partials, I = sum (+ 128 (2T - Rp) for b = 8, whose codes entered
-// as q - 128 against every sign including the zero tail of the last word) and writes
-// S_d * I + Z'_d * (2T - N*Ho*Wo) to row d = kept[slot]; a pruned slot zeroes its row.
+// dW from the split partials: one thread per 4 columns (slot, k .. k + 3) of the slot
+// capacity, reading 16 bytes of each partial row.  A kept slot sums its S partials,
+// I = sum (+ 128 (2T - Rp) for b = 8, whose codes entered as q - 128 against every sign
+// including the zero tail of the last word) and writes S_d * I + Z'_d * (2T - N*Ho*Wo) to
+// row d = kept[slot]; a pruned slot zeroes its row.
 template <bool B8>
 __global__ __launch_bounds__(256) void k_dw_finish(DwArgs a) {
   const uint32_t e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= a.D * a.K) return;
-  const uint32_t slot = fdiv(e, a.divK), k = e - slot * a.K;
+  const uint32_t qrow = a.Kp / 4;
+  if (e >= a.D * qrow) return;
+  const uint32_t slot = fdiv(e, a.divQ), k = 4 * (e - slot * qrow);
+  if (k >= a.K) return;
   const int count = *a.count;
   const size_t d = size_t(a.kept[slot]);
-  const size_t idx = d * a.K + k;
-  if (int(slot) >= count) {
-    a.dW[idx] = 0.0f;
-    if (a.I_out) a.I_out[idx] = 0;
-    return;
+  int I[4] = {0, 0, 0, 0};
+  float out[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (int(slot) < count) {
+    int4 acc = make_int4(0, 0, 0, 0), T4 = make_int4(0, 0, 0, 0);
+    for (uint32_t s = 0; s < a.S; ++s) {
+      const int4 v = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
+      const int4 t4 = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      T4.x += t4.x; T4.y += t4.y; T4.z += t4.z; T4.w += t4.w;
+    }
+    const int T[4] = {T4.x, T4.y, T4.z, T4.w};
+    I[0] = acc.x; I[1] = acc.y; I[2] = acc.z; I[3] = acc.w;
+    const float Sd = a.scale[d], Zd = a.offset[d];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (B8) I[u] += 128 * (2 * T[u] - int(a.Rp));
+      out[u] = rescale(Sd, I[u], Zd, float(2 * T[u] - int(a.R)));
+    }
   }
-  int I = 0, T = 0;
-  for (uint32_t s = 0; s < a.S; ++s) {
-    I += a.part[(size_t(s) * a.D + slot) * a.K + k];
-    T += a.partT[size_t(s) * a.K + k];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (k + u >= a.K) break;
+    a.dW[d * a.K + k + u] = out[u];
+    if (a.I_out) a.I_out[d * a.K + k + u] = I[u];
   }
-  if (B8) I += 128 * (2 * T - int(a.Rp));
-  a.dW[idx] = rescale(a.scale[d], I, a.offset[d], float(2 * T - int(a.R)));
-  if (a.I_out) a.I_out[idx] = I;
 }
 
 // ----------------------------------------------------------------------------- dX
@@ -423,9 +421,11 @@ __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa,
 
 int gemm_dw_splits(const Layer &L) { return int(L.Wr < 8 ? L.Wr : 8); }
 
+// dW workspace: partials [S][D][Kp] and set-bit counts [S][Kp], Kp = K rounded up to 32.
+static size_t dw_kp(const Layer &L) { return size_t((L.K + 31) / 32) * 32; }
 size_t gemm_dw_ws_bytes(const Layer &L) {
   const size_t S = size_t(gemm_dw_splits(L));
-  return align256(S * size_t(L.D) * L.K * 4) + align256(S * size_t(L.K) * 4);
+  return align256(S * size_t(L.D) * dw_kp(L) * 4) + align256(S * dw_kp(L) * 4);
 }
 
 namespace {
@@ -440,14 +440,14 @@ DwArgs make_dw_args(const Layer &L, const fqt_qgrad &q, const uint64_t *xsign, f
   a.dW = dW; a.I_out = I_out;
   a.part = static_cast<int32_t *>(ws);
   a.partT = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
-                                        align256(size_t(S) * L.D * L.K * 4));
-  a.D = uint32_t(L.D); a.K = uint32_t(L.K); a.R = uint32_t(L.R);
+                                        align256(size_t(S) * L.D * dw_kp(L) * 4));
+  a.D = uint32_t(L.D); a.K = uint32_t(L.K); a.Kp = uint32_t(dw_kp(L)); a.R = uint32_t(L.R);
   a.Rp = uint32_t(L.Wr * 64); a.Wr = uint32_t(L.Wr); a.ktiles = ktiles;
   a.codes_bytes = uint32_t(L.D * L.Wr * 64);
   a.xsign_bytes = uint32_t(L.Wr * L.K * 8);
   a.kgroups = (ktiles + DW_WAVES - 1) / DW_WAVES;
   a.S = S; a.wps = uint32_t((L.Wr + S - 1) / S);
-  a.divS = make_fastdiv(S); a.divKg = make_fastdiv(a.kgroups); a.divK = make_fastdiv(uint32_t(L.K));
+  a.divS = make_fastdiv(S); a.divKg = make_fastdiv(a.kgroups); a.divQ = make_fastdiv(uint32_t(dw_kp(L) / 4));
   return a;
 }
 // Split-R partial blocks over the slot capacity: S x ceil(ceil(K/32) / 4) x ceil(D/32).
@@ -492,7 +492,7 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                    const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s) {
   const DwArgs a = make_dw_args(L, q, xsign, dW, I_out, ws);
   const dim3 grid(dw_part_blocks(L, a));
-  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
+  const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));
   if (cfg.bits == 8) {
     hipLaunchKernelGGL(k_mfma_dw_part<true>, grid, dim3(DW_THREADS), 0, s, a);
     hipLaunchKernelGGL(k_dw_finish<true>, fgrid, dim3(256), 0, s, a);
@@ -528,7 +528,7 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   const DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
   const uint32_t ndw = dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
-  const dim3 fgrid(unsigned((L.D * L.K + 255) / 256));
+  const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));
   const int nb = dx_batch(dxa);
   auto go = [&]<bool B8>() {
     if (nb == 4) hipLaunchKernelGGL((k_products<B8, 4>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);

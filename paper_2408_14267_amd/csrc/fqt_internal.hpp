@@ -79,8 +79,17 @@ inline size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 inline bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 // Launchers (stream-ordered, no synchronisation).  They return an fqt_status.
+// The sign operands of the products, packed in spare blocks of the selection launch when
+// the layer allows it (launch_quantize then sets *done).
+struct SignJob {
+  const void *X, *W;
+  uint64_t *xsign;       // word-major sign(unfold(X))
+  int8_t *wsb;           // sign(W) bytes
+  int32_t *wlsum;
+  bool done;
+};
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
-                    const QuantWs &w, hipStream_t s);
+                    const QuantWs &w, hipStream_t s, SignJob *signs = nullptr);
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                      const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s,
                      bool word_major = false);
@@ -204,6 +213,27 @@ __host__ void dispatch_dtype(int dt, F &&f) {
 }
 
 __device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }
+
+// ----------------------------------------------------------------------------- buffer loads
+// Raw buffer resources: a lane whose offset is BUF_NONE (past every buffer here, all
+// shorter than 2^31 bytes) loads zeros without touching memory.  The bounds check covers
+// the per-lane offset only; the wave-uniform offset (an SGPR) must keep in-bounds lanes in
+// bounds by construction.
+typedef int v4i __attribute__((ext_vector_type(4)));
+constexpr uint32_t BUF_NONE = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, uint32_t bytes) {
+  // Raw buffer (stride 0) of `bytes` bytes; 0x00020000 is the gfx9 32-bit data format.
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+// 16 / 8 bytes at byte offset voff + soff of buffer r (soff wave-uniform).
+__device__ __forceinline__ v4i load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint64_t load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
 
 // ----------------------------------------------------------------------------- cross-lane
 // Wave-level exchanges on the VALU data path (DPP row operations and the gfx950 lane

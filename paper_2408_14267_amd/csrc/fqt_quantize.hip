@@ -20,6 +20,7 @@
 #include <climits>
 
 #include "fqt_internal.hpp"
+#include "fqt_signs.hpp"
 
 namespace fqt {
 namespace {
@@ -544,7 +545,7 @@ __device__ T block_incl_scan(T v, T *scr, T &total, int lane, int wave) {
 }
 
 template <int GP>
-__global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
+__device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) {
   static_assert(GP <= SEL_NT && GP % 64 == 0, "one sort key per thread");
   __shared__ int2 gk[GP];
   __shared__ int2 tmpk[SEL_NT];
@@ -553,7 +554,7 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
   __shared__ int32_t scr_i[SEL_NW];
   __shared__ float scr_f[SEL_NW];
   __shared__ uint64_t sat_w[2];          // W(s_sat), w at s_sat - 1
-  const SetArgs S = blockIdx.x ? a.set[1] : a.set[0];
+  const SetArgs S = set ? a.set[1] : a.set[0];
   const int G = S.G;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -570,17 +571,22 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
     const int g = t % GP, r0 = t / GP;
     int lo = INT_MAX, hi = INT_MIN;
     if (g < G && !S.slots) {            // channels: row-block partials, adjacent per row
+      // One per-lane offset (the group) and a wave-uniform one per row block (r0 is
+      // uniform across each wave).
+      const __amdgpu_buffer_rsrc_t prs = buffer_of(S.part, S.U * S.ld * 8);
+      const uint32_t voff = uint32_t(g) * 8;
       for (uint32_t u0 = r0; u0 < S.U; u0 += 16 * SPLIT) {
-        int2 v[16];
+        uint64_t v[16];
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
           const uint32_t u = u0 + k * SPLIT;
-          v[k] = u < S.U ? S.part[size_t(u) * S.ld + g] : make_int2(INT_MAX, INT_MIN);
+          v[k] = load8(prs, u < S.U ? voff : BUF_NONE, u < S.U ? u * S.ld * 8 : 0);
         }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
-          lo = min(lo, v[k].x);
-          hi = max(hi, v[k].y);
+          if (u0 + k * SPLIT >= S.U) break;
+          lo = min(lo, int(uint32_t(v[k])));
+          hi = max(hi, int(uint32_t(v[k] >> 32)));
         }
       }
     } else if (g < G) {                 // samples: the slots of the 64-row tiles they meet
@@ -742,6 +748,48 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
   gp.pad = 0;
   S.gp[t] = gp;
   S.kept[keep ? rank : count + (t - rank)] = t;
+}
+
+// One workgroup per group set.
+template <int GP>
+__global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
+  select_fused_body<GP>(a, int(blockIdx.x));
+}
+
+// The same two selection workgroups, then spare workgroups that pack the products' sign
+// operands (they do not depend on dY): blocks [2, 2 + npw) the weight bytes, the rest the
+// band im2col of X (word fastest, then 64-channel groups).
+struct SignArgs {
+  const void *x;
+  BandGeom bg;
+  uint64_t *xsign;
+  uint32_t Wr;
+  FastDiv divWr;
+  const void *w;
+  PackWGeom pg;
+  int8_t *wsb;
+  int32_t *wlsum;
+  uint32_t npw;
+};
+template <int GP, int DT, int KH, int KW>
+__global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) void k_select_signs(SelectArgs a,
+                                                                                 SignArgs sg) {
+  extern __shared__ uint32_t band[];
+  __shared__ PackWLds pws;
+  const uint32_t b = blockIdx.x;
+  if (b < 2) {
+    select_fused_body<GP>(a, int(b));
+  } else if (b - 2 < sg.npw) {
+    pack_w_body<DT>(sg.w, sg.pg, sg.wsb, sg.wlsum, b - 2, pws);
+  } else {
+    const uint32_t f = b - 2 - sg.npw;
+    const uint32_t cb = fdiv(f, sg.divWr);
+    band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.Wr, cb, band);
+  }
+}
+// Static LDS of k_select_signs<GP>: the selection's arrays and the weight-byte tile.
+constexpr size_t select_signs_static_lds(int GP) {
+  return size_t(24) * GP + 8 * SEL_NT + 16 * SEL_NW + 16 + sizeof(PackWLds);
 }
 
 // ----------------------------------------------------------------------------- quantize + pack
@@ -936,10 +984,11 @@ uint32_t stats_slots(const Layer &L) {
   const int64_t per = (63 + L.P - 1) / L.P + 1;
   return uint32_t(per < 64 ? per : 64);
 }
-// Row tiles per stats block: one while that still gives 512 blocks, else up to 8.
+// Row tiles per stats block: one while that still gives 256 blocks, else up to 8 (each
+// row block adds a partial per channel that the selection reads from one workgroup).
 uint32_t stats_rows_per_block(const Layer &L) {
   int64_t rs = 1;
-  while (rs < 8 && L.Wr * L.Wd / (rs * 2) >= 512) rs *= 2;
+  while (rs < 8 && L.Wr * L.Wd / (rs * 2) >= 256) rs *= 2;
   return uint32_t(rs);
 }
 int64_t stats_row_blocks(const Layer &L) {
@@ -948,7 +997,7 @@ int64_t stats_row_blocks(const Layer &L) {
 }
 
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
-                    const QuantWs &w, hipStream_t s) {
+                    const QuantWs &w, hipStream_t s, SignJob *signs) {
   TileGeom g{uint32_t(L.D), uint32_t(L.P), uint32_t(L.R), make_fastdiv(uint32_t(L.P))};
   const uint32_t nrt = uint32_t(L.Wr), ndt = uint32_t(L.Wd);
   const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L)};
@@ -979,7 +1028,38 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   sa.layer = cfg.layer_id;
   const int64_t gmax = L.N > L.D ? L.N : L.D;
   int st;
-  if (gmax <= 256) {
+  // Sign operands in the selection launch: a convolution whose X and W share a dtype and
+  // whose band fits the LDS left beside the selection (64 KB per workgroup in all).
+  BandGeom bg;
+  size_t band_lds = 0;
+  const int gp = gmax <= 256 ? 256 : 1024;
+  const bool with_signs =
+      signs && gmax <= 1024 && L.x_t == L.w_t &&
+      band_geom(L, signs->X, L.x_t, SEL_NT, 65536 - 512 - select_signs_static_lds(gp), &bg,
+                &band_lds);
+  if (with_signs) {
+    SignArgs sg;
+    sg.x = signs->X; sg.bg = bg; sg.xsign = signs->xsign;
+    sg.Wr = uint32_t(L.Wr); sg.divWr = make_fastdiv(uint32_t(L.Wr));
+    sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
+    sg.npw = pack_w_blocks(L);
+    const uint32_t cgroups = uint32_t((L.C + BAND_CPW * SEL_NW - 1) / (BAND_CPW * SEL_NW));
+    const dim3 grid(2 + sg.npw + uint32_t(L.Wr) * cgroups);
+    dispatch_dtype(L.x_t, [&]<int DT>() {
+      auto go = [&]<int GPT>() {
+        if (L.kh == 3 && L.kw == 3)
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 3, 3>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+        else if (L.kh == 1 && L.kw == 1)
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 1, 1>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+        else
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 0, 0>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+      };
+      if (gp == 256) go.template operator()<256>();
+      else go.template operator()<1024>();
+    });
+    st = last_launch_status();
+    signs->done = st == FQT_OK;
+  } else if (gmax <= 256) {
     hipLaunchKernelGGL(k_select_fused<256>, dim3(2), dim3(SEL_NT), 0, s, sa);
     st = last_launch_status();
   } else if (gmax <= 1024) {

@@ -1,0 +1,218 @@
+// Device bodies of the two sign packers that feed the MFMA products (Section 5.1
+// binarizer; Appendix C, Alg. 2 encoders, the Unfolder and the {0,1} <-> {+-1}
+// conversion):
+//   band im2col   sign(unfold(X)) as word-major bits, the dW operand;
+//   weight bytes  sign(W) as +-1 bytes with per-line sums, the dX operand.
+// fqt_pack.hip launches them on their own; the layer backward runs them in spare blocks
+// of the AGP selection launch, whose two selection workgroups leave the chip idle.
+#pragma once
+
+#include "fqt_internal.hpp"
+
+namespace fqt {
+
+// ----------------------------------------------------------------------------- band im2col
+// Bit-im2col through LDS, word-major output, for layers whose output positions per sample
+// are a multiple of 64 (every 64-position word lies in one sample) and whose rows are
+// whole 16-byte quads (W % 4 == 0, pw <= 4).  A block takes one word w (output positions
+// p0 .. p0 + 63 of sample n) and BAND_CPW channels per wave: it stages, per channel, the
+// band of input rows those positions read as one byte per pixel (1 = positive), each band
+// row framed by four zero bytes on either side and rows outside the image all zero; a
+// lane loads one 16-byte quad and writes one LDS dword.  Then each (channel, tap) word is
+// one LDS byte per lane and a ballot.  Lane l reads band row (ho - ho_lo) * sh + i, column
+// wo * sw + j - pw + 4 for its position (ho, wo) and tap (i, j); band row 0 is image row
+// ho_lo * sh - ph.
+constexpr int BAND_CPW = 4;            // channels per wave
+struct BandGeom {
+  uint32_t C, H, W, Wo, P, K, taps, BR, WL, plane;   // WL = W + 8, plane = BR * WL
+  uint32_t qrow;                                     // dwords per band row, WL / 4
+  int kw, sh, sw, ph, pw;
+  FastDiv divWo, divP, divQrow, divBR, divKw;
+};
+
+// Geometry of the band im2col for blocks of `nt` threads (BAND_CPW * nt / 64 channels),
+// or false when the layer does not fit it or its band exceeds `lds_max` bytes.
+inline bool band_geom(const Layer &L, const void *x, int dtype, int nt, size_t lds_max,
+                      BandGeom *bg, size_t *lds) {
+  const bool quads_ok = reinterpret_cast<uintptr_t>(x) % (dtype == FQT_BF16 ? 8 : 16) == 0;
+  if (L.kind != FQT_CONV2D || !quads_ok || L.P % 64 != 0 || L.W % 4 != 0 || L.pw > 4 ||
+      L.kh * L.kw > 64)
+    return false;
+  // Band of input rows read by one word: its output rows times the stride plus the kernel
+  // height.
+  const int64_t orows = (64 + L.Wo - 1) / L.Wo + 1;
+  const int64_t BR = (orows - 1) * L.sh + L.kh;
+  const int64_t WL = L.W + 8;
+  const int64_t plane = BR * WL;
+  const size_t bytes = size_t(plane) * BAND_CPW * (nt / 64);
+  if (bytes > lds_max) return false;
+  *bg = BandGeom{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
+                 uint32_t(L.K), uint32_t(L.kh * L.kw), uint32_t(BR), uint32_t(WL),
+                 uint32_t(plane), uint32_t(WL / 4), L.kw, L.sh, L.sw, L.ph, L.pw,
+                 make_fastdiv(uint32_t(L.Wo)), make_fastdiv(uint32_t(L.P)),
+                 make_fastdiv(uint32_t(WL / 4)), make_fastdiv(uint32_t(BR)),
+                 make_fastdiv(uint32_t(L.kw))};
+  *lds = bytes;
+  return true;
+}
+
+// One block of NT threads: word w, channels [cblk * BAND, (cblk + 1) * BAND).  band: the
+// block's LDS, BAND * plane bytes.
+template <int DT, int KH, int KW, int NT>
+__device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, const BandGeom &g,
+                                                 uint64_t *__restrict__ dst, uint32_t w,
+                                                 uint32_t cblk, uint32_t *band) {
+  constexpr int NW = NT / 64, BAND = BAND_CPW * NW;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const uint32_t c0 = cblk * BAND;
+  const uint32_t nch = min(uint32_t(BAND), g.C - c0);
+  const uint32_t r0 = w * 64;
+  const uint32_t n = fdiv(r0, g.divP), p0 = r0 - n * g.P;
+  const uint32_t ho_lo = fdiv(p0, g.divWo);
+  const int h_base = int(ho_lo) * g.sh - g.ph;   // image row of band row 0
+  const size_t xbase = (size_t(n) * g.C + c0) * g.H * g.W;   // element (c0, 0, 0) of sample n
+
+  // Stage: dword q of band row (c, br) holds image columns 4 (q - 1) .. 4 (q - 1) + 3.
+  const uint32_t rows = nch * g.BR;
+  const uint32_t items = rows * g.qrow;
+  constexpr int SB = 4;
+  for (uint32_t e0 = t; e0 < items; e0 += SB * NT) {
+    float v[SB][4];
+    bool in[SB];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const uint32_t e = e0 + k * NT;
+      const uint32_t row = fdiv(e, g.divQrow), q = e - row * g.qrow;
+      const uint32_t c = fdiv(row, g.divBR), br = row - c * g.BR;
+      const int h = h_base + int(br);
+      in[k] = e < items && h >= 0 && h < int(g.H) && q >= 1 && q <= g.W / 4;
+      const uint32_t off = (c * g.H + uint32_t(h)) * g.W + 4 * (q - 1);   // < C*H*W
+      load_quad<DT>(x, in[k] ? int64_t(xbase + off) : 0, v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const uint32_t e = e0 + k * NT;
+      if (e >= items) break;
+      uint32_t b = 0;
+      if (in[k])
+        b = (v[k][0] > 0.0f ? 1u : 0u) | (v[k][1] > 0.0f ? 0x100u : 0u) |
+            (v[k][2] > 0.0f ? 0x10000u : 0u) | (v[k][3] > 0.0f ? 0x1000000u : 0u);
+      band[e] = b;
+    }
+  }
+  __syncthreads();
+
+  // This lane's output position and its band byte offset for tap (0, 0).
+  const uint8_t *bb = reinterpret_cast<const uint8_t *>(band);
+  const uint32_t p = p0 + lane;
+  const uint32_t ho = fdiv(p, g.divWo), wo = p - ho * g.Wo;
+  const uint32_t base = (ho - ho_lo) * g.sh * g.WL + wo * g.sw + 4 - g.pw;
+  const uint32_t cl_lo = wave * BAND_CPW, cl_hi = min(nch, cl_lo + BAND_CPW);
+  uint32_t mlo = 0, mhi = 0;                     // words gather in lanes 0 .. 63
+  int filled = 0;
+  uint64_t *out = dst + size_t(w) * g.K;
+  auto put = [&](uint64_t m, uint32_t line_last) {
+    mlo = writelane(uint32_t(m), filled, mlo);
+    mhi = writelane(uint32_t(m >> 32), filled, mhi);
+    if (++filled == 64) {                        // 64 words of consecutive lines
+      out[line_last - 63 + lane] = (uint64_t(mhi) << 32) | mlo;
+      filled = 0;
+    }
+  };
+  for (uint32_t cl = cl_lo; cl < cl_hi; ++cl) {
+    const uint8_t *pl = bb + cl * g.plane + base;
+    if constexpr (KH > 0) {
+      // Kernel size fixed at compile time: every tap's LDS read issues before the ballots.
+      uint8_t b[KH * KW];
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int j = 0; j < KW; ++j) b[i * KW + j] = pl[i * g.WL + j];
+#pragma unroll
+      for (int tap = 0; tap < KH * KW; ++tap)
+        put(__ballot(b[tap] != 0), (c0 + cl) * (KH * KW) + tap);
+    } else {
+      for (uint32_t tap = 0; tap < g.taps; ++tap) {
+        const uint32_t i = fdiv(tap, g.divKw), j = tap - i * g.kw;
+        put(__ballot(pl[i * g.WL + j] != 0), (c0 + cl) * g.taps + tap);
+      }
+    }
+  }
+  if (filled > 0 && cl_hi > cl_lo) {
+    // The words left end at the wave's last line.
+    const uint32_t l_end = (c0 + cl_hi) * g.taps;
+    if (lane < filled) out[l_end - filled + lane] = (uint64_t(mhi) << 32) | mlo;
+  }
+}
+
+// ----------------------------------------------------------------------------- weight bytes
+// sign(W) as signed bytes for the int8 dX product.  W is viewed as [D][K] (K = C*kh*kw,
+// line l = (c, tap)); byte d of line l is +1 if W[d][l] > 0 else -1 for d < D, 0 for
+// D <= d < Dp, stored chunk-major at ((d/32 * taps + tap) * C + c) * 32 + d % 32 so that the
+// 32-byte chunks of consecutive channels are adjacent; lsum[l] = sum over d < D of the
+// line.  One block of 1024 threads per 64 lines walks D in passes of 256 rows (one pass
+// for D <= 256): each thread loads 16 rows of its line back to back, the pass is
+// transposed through LDS (pitch 260 bytes = 65 dwords: the column writes of a wave spread
+// over the banks) and written as 16-byte pieces of the 32-byte chunks.
+constexpr int WB_THREADS = 1024;
+constexpr int WB_ROWS = 256;                  // rows of D per pass: 16 per thread
+constexpr int WB_PITCH = WB_ROWS + 4;
+struct PackWGeom {
+  uint32_t D, K, Dp, C, taps;
+  FastDiv div_taps;
+};
+struct alignas(16) PackWLds {
+  int8_t tile[64][WB_PITCH];
+  int32_t pos[64];
+};
+
+template <int DT>
+__device__ __forceinline__ void pack_w_body(const void *__restrict__ w, const PackWGeom &g,
+                                            int8_t *__restrict__ dst, int32_t *__restrict__ lsum,
+                                            uint32_t bid, PackWLds &sm) {
+  constexpr int Q = WB_THREADS / 64;          // row phases per pass
+  const int t = threadIdx.x, line = t & 63, q = t >> 6;
+  const uint32_t l0 = bid * 64, l = l0 + line;
+  if (t < 64) sm.pos[t] = 0;
+  int mine = 0;
+  for (uint32_t d0 = 0; d0 < g.Dp; d0 += WB_ROWS) {
+    float v[WB_ROWS / Q];
+#pragma unroll
+    for (int k = 0; k < WB_ROWS / Q; ++k) {   // unconditional loads (element 0 outside) issue back to back
+      const uint32_t d = d0 + Q * k + q;
+      v[k] = load_elem<DT>(w, (d < g.D && l < g.K) ? int64_t(d) * g.K + l : 0);
+    }
+#pragma unroll
+    for (int k = 0; k < WB_ROWS / Q; ++k) {
+      const uint32_t d = d0 + Q * k + q;
+      const bool in = d < g.D && l < g.K;
+      const bool pos_sign = in && v[k] > 0.0f;
+      mine += pos_sign ? 1 : 0;
+      sm.tile[line][Q * k + q] = in ? (pos_sign ? int8_t(1) : int8_t(-1)) : int8_t(0);
+    }
+    __syncthreads();
+    // 64 lines x 16 pieces of 16 bytes; pieces past Dp (last pass of a short D) are not stored.
+    const int wl = t >> 4, part = t & 15;
+    if (l0 + wl < g.K && d0 + 16 * part < g.Dp) {
+      const uint32_t lw = l0 + wl, c = fdiv(lw, g.div_taps), tap = lw - c * g.taps;
+      const uint32_t chunk = (d0 >> 5) + (part >> 1);
+      const uint32_t *src = reinterpret_cast<const uint32_t *>(&sm.tile[wl][16 * part]);
+      *reinterpret_cast<uint4 *>(dst + ((size_t(chunk) * g.taps + tap) * g.C + c) * 32 +
+                                 16 * (part & 1)) = make_uint4(src[0], src[1], src[2], src[3]);
+    }
+    __syncthreads();
+  }
+  atomicAdd(&sm.pos[line], mine);
+  __syncthreads();
+  if (t < 64 && l0 + t < g.K) lsum[l0 + t] = 2 * sm.pos[t] - int(g.D);
+}
+
+inline PackWGeom pack_w_geom(const Layer &L) {
+  const uint32_t taps = uint32_t(L.kh * L.kw);
+  return PackWGeom{uint32_t(L.D), uint32_t(L.K), uint32_t(L.Wd * 64), uint32_t(L.C), taps,
+                   make_fastdiv(taps)};
+}
+inline uint32_t pack_w_blocks(const Layer &L) { return uint32_t((L.K + 63) / 64); }
+
+}  // namespace fqt
