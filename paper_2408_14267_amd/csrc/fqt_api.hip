@@ -38,6 +38,8 @@ void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
   q->ckey = c->take<int2>(L.D);
   q->sp = c->take<GroupParam>(L.N);
   q->cp = c->take<GroupParam>(L.D);
+  q->sslot = c->take<float2>(L.N);
+  q->cslot = c->take<float2>(L.D);
 }
 
 size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
@@ -326,7 +328,8 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
                                true));
     FQT_TRY(launch_pack_w_i8(W, L, w.wsb, w.wlsum, s));
   }
-  return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, s);
+  return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, w.qws.sslot,
+                         w.qws.cslot, s);
 }
 
 }  // extern "C"

@@ -100,6 +100,7 @@ struct DwArgs {
   const uint8_t *codes;          // PCQ codes [2*Wr][D][32], chunk-major
   const int32_t *kept, *count;   // [D], [1]
   const float *scale, *offset;   // [D]
+  const float2 *slot_sz;         // [D] (scale, offset) by kept slot, or null (read via kept)
   const uint64_t *xsign;         // [Wr][K], word-major
   float *dW;                     // [D][K]
   int32_t *I_out;                // [D][K] or null
@@ -225,7 +226,8 @@ __global__ __launch_bounds__(256) void k_dw_finish(DwArgs a) {
     }
     const int T[4] = {T4.x, T4.y, T4.z, T4.w};
     I[0] = acc.x; I[1] = acc.y; I[2] = acc.z; I[3] = acc.w;
-    const float Sd = a.scale[d], Zd = a.offset[d];
+    const float2 sz = a.slot_sz ? a.slot_sz[slot] : make_float2(a.scale[d], a.offset[d]);
+    const float Sd = sz.x, Zd = sz.y;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (B8) I[u] += 128 * (2 * T[u] - int(a.Rp));
@@ -246,6 +248,7 @@ struct DxArgs {
   const uint8_t *codes;          // PSQ codes [Dp/32][N*Ho*Wo][32], chunk-major
   const int32_t *kept, *count;   // [N], [1]
   const float *scale, *offset;   // [N]
+  const float2 *slot_sz;         // [N] (scale, offset) by kept slot, or null (read via kept)
   const int8_t *wsb;             // sign(W) bytes [Dp/32][kh*kw][C][32]: +-1, 0 past D
   const int32_t *wlsum;          // [C*kh*kw] sum over d of the signs of each line
   void *dX;                      // [N][C][H][W]
@@ -291,6 +294,30 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
+  // Loads that do not depend on the count issue with it: the pixel parameters and the
+  // line sign sums this block needs were it a computing block (indices clamped into the
+  // arrays for the zeroing blocks past the capacity tiles).
+  const uint32_t mt = fdiv(bid, a.divCt);
+  const uint32_t m0 = mt * 32, c0 = (bid - mt * a.ctiles) * 32;
+  const int taps = int(a.taps);
+  int kn = 0;
+  float2 sz = make_float2(0.0f, 0.0f);
+  uint32_t pslot = 0, ppix = 0;
+  if (t < 32) {
+    const uint32_t m = min(m0 + uint32_t(t), a.N * a.HW - 1);
+    pslot = fdiv(m, a.divHW);
+    ppix = m - pslot * a.HW;
+    kn = a.kept[pslot];
+    if (a.slot_sz) sz = a.slot_sz[pslot];
+  }
+  constexpr int WLT = DX_MAX_TAPS * 32 / DX_THREADS;   // sign sums per thread, at most
+  int wlv[WLT];
+#pragma unroll
+  for (int k = 0; k < WLT; ++k) {
+    const int e = t + k * DX_THREADS, p = e & 31, tap = e >> 5;
+    const uint32_t ch = c0 + uint32_t(p);
+    wlv[k] = (e < 32 * taps && ch < a.C) ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
+  }
   const uint32_t live_rows = uint32_t(count) * a.HW;
   const uint32_t live_blocks = ((live_rows + 31) / 32) * a.ctiles;
 
@@ -303,29 +330,21 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
     }
     return;
   }
-  const uint32_t mt = fdiv(bid, a.divCt);
-  const uint32_t m0 = mt * 32, c0 = (bid - mt * a.ctiles) * 32;
-  const int taps = int(a.taps);
 
   if (t < 32) {
-    const uint32_t m = m0 + t;
-    int off = -1;
-    float sc = 0.0f, zo = 0.0f;
-    if (m < live_rows) {
-      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
-      const int n = a.kept[slot];
-      off = int(uint32_t(n) * a.CHW + pix);
-      sc = a.scale[n];
-      zo = a.offset[n];
-    }
-    sm.pix_out[t] = off;
-    sm.pix_s[t] = sc;
-    sm.pix_z[t] = zo;
+    const bool live = m0 + uint32_t(t) < live_rows;
+    if (!a.slot_sz && live) sz = make_float2(a.scale[kn], a.offset[kn]);
+    sm.pix_out[t] = live ? int(uint32_t(kn) * a.CHW + ppix) : -1;
+    sm.pix_s[t] = live ? sz.x : 0.0f;
+    sm.pix_z[t] = live ? sz.y : 0.0f;
+  }
+#pragma unroll
+  for (int k = 0; k < WLT; ++k) {
+    const int e = t + k * DX_THREADS;
+    if (e < 32 * taps) sm.wl[e >> 5][e & 31] = wlv[k];
   }
   for (int e = t; e < 32 * taps; e += DX_THREADS) {
     const int p = e & 31, tap = e >> 5;
-    const uint32_t ch = c0 + uint32_t(p);
-    sm.wl[tap][p] = ch < a.C ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
     const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
     const uint32_t m = m0 + p;
     uint32_t off = BUF_NONE;
@@ -436,7 +455,7 @@ DwArgs make_dw_args(const Layer &L, const fqt_qgrad &q, const uint64_t *xsign, f
   const uint32_t S = uint32_t(gemm_dw_splits(L));
   DwArgs a;
   a.codes = q.pcq_codes; a.kept = q.pcq_kept; a.count = q.pcq_count;
-  a.scale = q.pcq_scale; a.offset = q.pcq_offset; a.xsign = xsign;
+  a.scale = q.pcq_scale; a.offset = q.pcq_offset; a.slot_sz = nullptr; a.xsign = xsign;
   a.dW = dW; a.I_out = I_out;
   a.part = static_cast<int32_t *>(ws);
   a.partT = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
@@ -459,7 +478,8 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
                     const int32_t *wlsum, void *dX, int32_t *I_out) {
   DxArgs a;
   a.codes = q.psq_codes; a.kept = q.psq_kept; a.count = q.psq_count;
-  a.scale = q.psq_scale; a.offset = q.psq_offset; a.wsb = wsb; a.wlsum = wlsum;
+  a.scale = q.psq_scale; a.offset = q.psq_offset; a.slot_sz = nullptr; a.wsb = wsb;
+  a.wlsum = wlsum;
   a.dX = dX; a.I_out = I_out; a.dx_t = L.dx_t;
   a.N = uint32_t(L.N); a.C = uint32_t(L.C); a.H = uint32_t(L.H); a.W = uint32_t(L.W);
   a.HW = uint32_t(L.HW); a.Ho = uint32_t(L.Ho); a.Wo = uint32_t(L.Wo); a.P = uint32_t(L.P);
@@ -522,10 +542,13 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
 
 int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                     const uint64_t *xsign, const int8_t *wsb, const int32_t *wlsum, void *dX,
-                    float *dW, void *dw_ws, hipStream_t s) {
+                    float *dW, void *dw_ws, const float2 *sslot, const float2 *cslot,
+                    hipStream_t s) {
   if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
-  const DwArgs dwa = make_dw_args(L, q, xsign, dW, nullptr, dw_ws);
-  const DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
+  DwArgs dwa = make_dw_args(L, q, xsign, dW, nullptr, dw_ws);
+  DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
+  dwa.slot_sz = cslot;
+  dxa.slot_sz = sslot;
   const uint32_t ndw = dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));

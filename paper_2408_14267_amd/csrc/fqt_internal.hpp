@@ -45,6 +45,8 @@ struct QuantWs {
   int2 *ckey;              // [D] (min, max) keys of each output channel
   GroupParam *sp;          // [N]
   GroupParam *cp;          // [D]
+  float2 *sslot;           // [N] (scale, offset) of the kept sample in slot j (j < count)
+  float2 *cslot;           // [D] the same for the kept channels
 };
 
 // Division by a fixed divisor for numerators below 2^31:
@@ -101,9 +103,11 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                    const int8_t *wsb, const int32_t *wlsum, void *dX, int32_t *I_out,
                    hipStream_t s);
 // Both products of the layer backward in one launch, then the dW finish pass.
+// sslot / cslot: the selection's slot-ordered (scale, offset) pairs (QuantWs).
 int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                     const uint64_t *xsign, const int8_t *wsb, const int32_t *wlsum, void *dX,
-                    float *dW, void *dw_ws, hipStream_t s);
+                    float *dW, void *dw_ws, const float2 *sslot, const float2 *cslot,
+                    hipStream_t s);
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }

@@ -263,6 +263,7 @@ struct SetArgs {
   int32_t *count;
   float *scale, *offset, *prob;
   GroupParam *gp;
+  float2 *slot;        // [G] (scale, offset) of the kept group in each slot
 };
 
 struct SelectArgs {
@@ -490,6 +491,7 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
     S.prob[i] = p;
     S.scale[i] = Sc;
     S.offset[i] = Zp + 0.0f;
+    if (keep) S.slot[rank] = make_float2(Sc, Zp + 0.0f);
     GroupParam gp;
     gp.z = Z;
     gp.inv = R > 0.0f ? __fdiv_rn(float(B), R) : 0.0f;
@@ -741,6 +743,7 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
   S.prob[t] = p;
   S.scale[t] = Sc;
   S.offset[t] = Zp + 0.0f;
+  if (keep) S.slot[rank] = make_float2(Sc, Zp + 0.0f);
   GroupParam gp;
   gp.z = Z;
   gp.inv = R > 0.0f ? __fdiv_rn(float(B), R) : 0.0f;
@@ -1020,10 +1023,10 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   SelectArgs sa;
   sa.set[0] = SetArgs{w.skey, w.part_s, 1u, 0u, 0u, uint32_t(L.P), nrt, sg.SL, ndt,
                       make_fastdiv(uint32_t(L.P)), int32_t(L.N), STREAM_SAMPLE, q.psq_kept,
-                      q.psq_count, q.psq_scale, q.psq_offset, q.psq_prob, w.sp};
+                      q.psq_count, q.psq_scale, q.psq_offset, q.psq_prob, w.sp, w.sslot};
   sa.set[1] = SetArgs{w.ckey, w.part_c, 0u, nrb, uint32_t(L.D), 0u, 0u, 0u, 0u,
                       make_fastdiv(1u), int32_t(L.D), STREAM_CHANNEL, q.pcq_kept, q.pcq_count,
-                      q.pcq_scale, q.pcq_offset, q.pcq_prob, w.cp};
+                      q.pcq_scale, q.pcq_offset, q.pcq_prob, w.cp, w.cslot};
   sa.bits = cfg.bits; sa.mode = cfg.agp_mode; sa.seed = cfg.seed; sa.step = cfg.step;
   sa.layer = cfg.layer_id;
   const int64_t gmax = L.N > L.D ? L.N : L.D;
