@@ -42,7 +42,8 @@ void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
   q->cslot = c->take<float2>(L.D);
 }
 
-size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
+size_t carve_layer_ws(void *ws, const Layer &L, const fqt_quant_cfg &cfg, LayerWs *out) {
+  const int bits = cfg.bits;
   Carver c{static_cast<char *>(ws)};
   LayerWs w{};
   carve_quant_ws(&c, L, &w.qws);
@@ -63,7 +64,7 @@ size_t carve_layer_ws(void *ws, const Layer &L, int bits, LayerWs *out) {
   w.xsign = c.take<uint64_t>(size_t(L.K) * L.Wr);
   w.wsb = c.take<int8_t>(size_t(L.K) * L.Wd * 64);
   w.wlsum = c.take<int32_t>(L.K);
-  w.dw_ws = c.take<char>(gemm_dw_ws_bytes(L));
+  w.dw_ws = c.take<char>(gemm_dw_ws_bytes(L, cfg));
   if (out) *out = w;
   return c.off;
 }
@@ -201,8 +202,8 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
   FQT_TRY(check_cfg(cfg, L));
   if (!bytes) return FQT_E_NULL;
   if (which == FQT_WS_QUANTIZE) *bytes = quant_ws_bytes(L);
-  else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, cfg->bits, nullptr);
-  else if (which == FQT_WS_GEMM_DW) *bytes = gemm_dw_ws_bytes(L);
+  else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, *cfg, nullptr);
+  else if (which == FQT_WS_GEMM_DW) *bytes = gemm_dw_ws_bytes(L, *cfg);
   else return FQT_E_INVAL;
   return FQT_OK;
 }
@@ -257,7 +258,7 @@ int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   if (!aligned(xsign, 8) || !aligned(dW, 4) || (I_out && !aligned(I_out, 4)) ||
       !aligned(ws, 256))
     return FQT_E_ALIGN;
-  if (ws_bytes < gemm_dw_ws_bytes(L)) return FQT_E_WORKSPACE;
+  if (ws_bytes < gemm_dw_ws_bytes(L, *cfg)) return FQT_E_WORKSPACE;
   return launch_gemm_dw(L, *cfg, *q, xsign, dW, I_out, ws, static_cast<hipStream_t>(hip_stream));
 }
 
@@ -310,9 +311,9 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   if (!aligned(dY, 16) || !aligned(X, dtype_size(L.x_t)) || !aligned(W, dtype_size(L.w_t)) ||
       !aligned(dX, dtype_size(L.dx_t)) || !aligned(dW, 4) || !aligned(ws, 256))
     return FQT_E_ALIGN;
-  if (ws_bytes < carve_layer_ws(nullptr, L, cfg->bits, nullptr)) return FQT_E_WORKSPACE;
+  if (ws_bytes < carve_layer_ws(nullptr, L, *cfg, nullptr)) return FQT_E_WORKSPACE;
   LayerWs w;
-  carve_layer_ws(ws, L, cfg->bits, &w);
+  carve_layer_ws(ws, L, *cfg, &w);
   const hipStream_t s = static_cast<hipStream_t>(hip_stream);
   if (L.kh * L.kw > 64) return FQT_E_SHAPE;
   // Statistics, then the selection (whose launch also packs the sign operands when the

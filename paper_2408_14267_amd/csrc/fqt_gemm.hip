@@ -112,52 +112,106 @@ struct DwArgs {
 
 constexpr int DW_WAVES = 4;                 // column tiles per block, one per wave
 constexpr int DW_THREADS = DW_WAVES * 64;
-constexpr int DW_PREF = 8;                  // 64-bit words of the contraction loaded per batch
+constexpr int DW_PREF = 4;                  // 64-bit words of the contraction per batch
+
+// One batch of a wave's operands: DW_PREF words of its sign column and the two 32-byte
+// code chunks of each word.
+struct DwBatch {
+  uint64_t word[DW_PREF];
+  v4i A[DW_PREF][2];
+};
+__device__ __forceinline__ void dw_issue(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
+                                         __amdgpu_buffer_rsrc_t xrs, uint32_t aoff,
+                                         uint32_t boff, uint32_t c0, uint32_t w_end,
+                                         DwBatch &b) {
+  const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
+#pragma unroll
+  for (int u = 0; u < DW_PREF; ++u) {
+    const uint32_t c = c0 + u < w_end ? c0 + u : c0;   // past the end: word c0 again
+    b.word[u] = load8(xrs, boff, c * a.K * 8);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) b.A[u][h] = load16(crs, aoff, (2 * c + h) * chunk_bytes);
+  }
+}
+template <bool B8>
+__device__ __forceinline__ void dw_consume(const DwBatch &b, uint32_t c0, uint32_t w_end,
+                                           int g, v16i &acc, uint32_t &tpart) {
+#pragma unroll
+  for (int u = 0; u < DW_PREF; ++u) {
+    if (c0 + u >= w_end) break;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t bits = uint32_t(b.word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
+      tpart += __popc(bits);
+      acc = mfma_i8(B8 ? bias128(b.A[u][h]) : b.A[u][h], signs16(bits), acc);
+    }
+  }
+}
 
 // The contraction of one wave's 32x32 tile over the words [c_first, w_end) of its split,
-// DW_PREF words per batch.  Every batch issues all its loads before the first product (a
-// sched_barrier keeps the compiler from sinking them), so a batch costs one memory
-// latency; past w_end the loads read word c0 again (in bounds) and a uniform test skips
-// the products.
+// double-buffered: the loads of batch i + 1 issue before the products of batch i (a
+// sched_barrier keeps the compiler from sinking them), so a long contraction costs one
+// exposed memory latency.
 template <bool B8>
 __device__ __forceinline__ void dw_accumulate(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
                                               __amdgpu_buffer_rsrc_t xrs, uint32_t aoff,
                                               uint32_t boff, uint32_t c_first, uint32_t w_end,
                                               int g, v16i &acc, uint32_t &tpart) {
-  const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
-  for (uint32_t c0 = c_first; c0 < w_end; c0 += DW_PREF) {
-    uint64_t word[DW_PREF];
-    v4i A[DW_PREF][2];
-#pragma unroll
-    for (int u = 0; u < DW_PREF; ++u) {
-      const uint32_t c = c0 + u < w_end ? c0 + u : c0;
-      word[u] = load8(xrs, boff, c * a.K * 8);
-#pragma unroll
-      for (int h = 0; h < 2; ++h) A[u][h] = load16(crs, aoff, (2 * c + h) * chunk_bytes);
-    }
+  if (c_first >= w_end) return;
+  DwBatch b0, b1;
+  uint32_t c0 = c_first;
+  dw_issue(a, crs, xrs, aoff, boff, c0, w_end, b0);
+  for (;;) {
+    if (c0 + DW_PREF < w_end) dw_issue(a, crs, xrs, aoff, boff, c0 + DW_PREF, w_end, b1);
     __builtin_amdgcn_sched_barrier(0);
+    dw_consume<B8>(b0, c0, w_end, g, acc, tpart);
+    c0 += DW_PREF;
+    if (c0 >= w_end) break;
+    if (c0 + DW_PREF < w_end) dw_issue(a, crs, xrs, aoff, boff, c0 + DW_PREF, w_end, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    dw_consume<B8>(b1, c0, w_end, g, acc, tpart);
+    c0 += DW_PREF;
+    if (c0 >= w_end) break;
+  }
+}
+
+// dW rows of the slot tile [j0, j0 + 32) of one wave's 32 columns written directly (one
+// split, S = 1): I, T, the rescale S_d I + Z'_d (2T - N*Ho*Wo) (b = 8 adds back
+// 128 (2T - Rp)), zero rows for pruned slots.  acc: the wave's tile (rows
+// acc_row(v, g) of column lane % 32); T: set bits of this lane's column.
+template <bool B8>
+__device__ __forceinline__ void dw_write_direct(const DwArgs &a, uint32_t j0, uint32_t kc,
+                                                int count, const v16i &acc, int T) {
+  const int g = (threadIdx.x & 63) >> 5;
+  if (kc >= a.K) return;
 #pragma unroll
-    for (int u = 0; u < DW_PREF; ++u) {
-      if (c0 + u >= w_end) break;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint32_t bits = uint32_t(word[u] >> (32 * h + 16 * g)) & 0xFFFFu;
-        tpart += __popc(bits);
-        acc = mfma_i8(B8 ? bias128(A[u][h]) : A[u][h], signs16(bits), acc);
-      }
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t j = j0 + uint32_t(acc_row(v, g));
+    if (j >= a.D) continue;
+    const size_t d = size_t(a.kept[j]);
+    int I = 0;
+    float out = 0.0f;
+    if (int(j) < count) {
+      const float2 sz = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[d], a.offset[d]);
+      I = acc[v] + (B8 ? 128 * (2 * T - int(a.Rp)) : 0);
+      out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
     }
+    a.dW[d * a.K + kc] = out;
+    if (a.I_out) a.I_out[d * a.K + kc] = I;
   }
 }
 
 // Split-R partial products.  Grid: S splits x ceil(ceil(K/32) / 4) column groups x
 // ceil(D/32) slot tiles over the slot capacity, the split index fastest (consecutive
 // blocks land on different XCDs, so each XCD reads its own slices of the codes and of the
-// signs) and the slot tile slowest (blocks past the kept channels exit at once).  Wave w
-// of a block computes the 32x32 MFMA tile (slot tile, column tile 4 * group + w) over the
-// words [s * wps, (s + 1) * wps) of the contraction over N*Ho*Wo: the four waves read the
-// same code rows (one fetch from L2) and their own sign columns, and each writes its tile
-// and the set-bit counts of its columns to the split's slice.  No LDS, no barrier.
-template <bool B8>
+// signs) and the slot tile slowest.  Wave w of a block computes the 32x32 MFMA tile (slot
+// tile, column tile 4 * group + w) over the words [s * wps, (s + 1) * wps) of the
+// contraction over N*Ho*Wo: the four waves read the same code rows (one fetch from L2)
+// and their own sign columns, and each writes its tile and the set-bit counts of its
+// columns to the split's slice.  No LDS, no barrier.
+// DIRECT (S = 1): the wave writes dW itself, and slot tiles past the kept channels zero
+// their rows; otherwise those blocks exit at once and the finish pass writes dW.
+template <bool B8, bool DIRECT>
 __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   const int lane = threadIdx.x & 63;
   const uint32_t wave = wave_id();
@@ -168,13 +222,17 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   const uint32_t rt = fdiv(rest, a.divKg);
   const uint32_t kt = (rest - rt * a.kgroups) * DW_WAVES + wave;
   const uint32_t j0 = rt * 32;
-  if (int(j0) >= count || kt >= a.ktiles) return;   // past the kept channels or the columns
+  if (kt >= a.ktiles) return;                   // past the columns
+  const uint32_t kc = kt * 32 + i;
+  if (int(j0) >= count) {                       // past the kept channels
+    if (DIRECT) dw_write_direct<B8>(a, j0, kc, count, v16i{0}, 0);
+    return;
+  }
 
   const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
   const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
   const uint32_t j = j0 + i;
   const uint32_t aoff = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
-  const uint32_t kc = kt * 32 + i;
   const bool b_ok = kc < a.K;
   const uint32_t boff = b_ok ? kc * 8 : BUF_NONE;
   const uint32_t w_end = min(a.Wr, (sp + 1) * a.wps);
@@ -185,6 +243,10 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   // Set bits of column kc in this split: lanes i and i + 32 counted the two halves of
   // every 32-bit piece.
   const uint32_t T = tpart + lane_xor<32>(tpart);
+  if (DIRECT) {
+    dw_write_direct<B8>(a, j0, kc, count, acc, int(T));
+    return;
+  }
   if (!b_ok) return;
   if (rt == 0 && g == 0) a.partT[size_t(sp) * a.Kp + kc] = int32_t(T);
   int32_t *out = a.part + (size_t(sp) * a.D + j0) * a.Kp + kc;
@@ -195,9 +257,9 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   }
 }
 
-template <bool B8>
+template <bool B8, bool DIRECT>
 __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
-  dw_part_body<B8>(a, blockIdx.x);
+  dw_part_body<B8, DIRECT>(a, blockIdx.x);
 }
 
 // dW from the split partials: one thread per 4 columns (slot, k .. k + 3) of the slot
@@ -241,6 +303,61 @@ __global__ __launch_bounds__(256) void k_dw_finish(DwArgs a) {
     if (a.I_out) a.I_out[d * a.K + k + u] = I[u];
   }
 }
+
+// The same for many splits: one block per (slot, 64 columns); thread t sums every 16th
+// split of column quad t % 16 from split t / 16, and the 16 partial sums of each quad
+// meet in LDS.
+constexpr int DWF_CHUNKS = 16;
+template <bool B8>
+__global__ __launch_bounds__(256) void k_dw_finish_wide(DwArgs a) {
+  __shared__ int4 red[DWF_CHUNKS][16], tred[DWF_CHUNKS][16];
+  const int t = threadIdx.x, quad = t & 15, chunk = t >> 4;
+  const uint32_t qblocks = a.Kp / 64 + (a.Kp % 64 ? 1 : 0);
+  const uint32_t slot = blockIdx.x / qblocks;
+  const uint32_t k = (blockIdx.x - slot * qblocks) * 64 + 4 * quad;
+  const int count = *a.count;
+  const bool live = int(slot) < count && k < a.Kp;
+  int4 acc = make_int4(0, 0, 0, 0), T4 = make_int4(0, 0, 0, 0);
+  if (live) {
+    for (uint32_t s = chunk; s < a.S; s += DWF_CHUNKS) {
+      const int4 v = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
+      const int4 t4 = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+      T4.x += t4.x; T4.y += t4.y; T4.z += t4.z; T4.w += t4.w;
+    }
+  }
+  red[chunk][quad] = acc;
+  tred[chunk][quad] = T4;
+  __syncthreads();
+  if (chunk != 0 || k >= a.K) return;
+#pragma unroll
+  for (int c = 1; c < DWF_CHUNKS; ++c) {
+    const int4 v = red[c][quad], t4 = tred[c][quad];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    T4.x += t4.x; T4.y += t4.y; T4.z += t4.z; T4.w += t4.w;
+  }
+  const size_t d = size_t(a.kept[slot]);
+  int I[4] = {0, 0, 0, 0};
+  float out[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (live) {
+    const int T[4] = {T4.x, T4.y, T4.z, T4.w};
+    I[0] = acc.x; I[1] = acc.y; I[2] = acc.z; I[3] = acc.w;
+    const float2 sz = a.slot_sz ? a.slot_sz[slot] : make_float2(a.scale[d], a.offset[d]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (B8) I[u] += 128 * (2 * T[u] - int(a.Rp));
+      out[u] = rescale(sz.x, I[u], sz.y, float(2 * T[u] - int(a.R)));
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (k + u >= a.K) break;
+    a.dW[d * a.K + k + u] = out[u];
+    if (a.I_out) a.I_out[d * a.K + k + u] = I[u];
+  }
+}
+// Splits above which the finish takes a block per (slot, 64 columns).
+constexpr uint32_t DWF_WIDE = 32;
 
 // ----------------------------------------------------------------------------- dX
 
@@ -429,37 +546,59 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
 
 // Both products in one launch (the layer backward): blocks [0, ndw) are dW split-R
 // partial blocks, the rest dX blocks; the two share the LDS allocation.
-template <bool B8, int NB>
+template <bool B8, int NB, bool DIRECT>
 __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
   __shared__ DxLds sm;
-  if (blockIdx.x < ndw) dw_part_body<B8>(dwa, blockIdx.x);
+  if (blockIdx.x < ndw) dw_part_body<B8, DIRECT>(dwa, blockIdx.x);
   else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm);
 }
 
 }  // namespace
 
-int gemm_dw_splits(const Layer &L) { return int(L.Wr < 8 ? L.Wr : 8); }
+// Splits of the dW contraction over N*Ho*Wo: enough 32x32 wave tiles of the expected
+// kept channels (all of them without AGP, about D / b with it) to give about 1024 waves,
+// and at most 256 words (16384 positions) per split, within at most DW_MAX_SPLITS splits,
+// 128 MB of partials and one batch of words per split.
+constexpr int64_t DW_TARGET_WAVES = 1024;
+constexpr int64_t DW_MAX_WORDS = 256;
+constexpr int64_t DW_MAX_SPLITS = 4096;
+constexpr int64_t DW_MAX_PART_BYTES = int64_t(128) << 20;
+int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
+  const int64_t dkeep =
+      cfg.agp_mode == FQT_AGP_OFF ? L.D : std::max<int64_t>(1, (L.D + cfg.bits - 1) / cfg.bits);
+  const int64_t tiles = ((dkeep + 31) / 32) * ((L.K + 31) / 32);
+  int64_t S = std::max((DW_TARGET_WAVES + tiles - 1) / tiles,
+                       (L.Wr + DW_MAX_WORDS - 1) / DW_MAX_WORDS);
+  const int64_t kp = ((L.K + 31) / 32) * 32;
+  S = std::min(S, std::max<int64_t>(1, DW_MAX_PART_BYTES / (L.D * kp * 4)));
+  S = std::min(S, DW_MAX_SPLITS);
+  S = std::min(S, (L.Wr + DW_PREF - 1) / DW_PREF);
+  return int(std::max<int64_t>(S, 1));
+}
 
-// dW workspace: partials [S][D][Kp] and set-bit counts [S][Kp], Kp = K rounded up to 32.
+// dW workspace: partials [S][D][Kp] and set-bit counts [S][Kp] (Kp = K rounded up to 32);
+// none when one split writes dW directly.
 static size_t dw_kp(const Layer &L) { return size_t((L.K + 31) / 32) * 32; }
-size_t gemm_dw_ws_bytes(const Layer &L) {
-  const size_t S = size_t(gemm_dw_splits(L));
+size_t gemm_dw_ws_bytes(const Layer &L, const fqt_quant_cfg &cfg) {
+  const size_t S = size_t(gemm_dw_splits(L, cfg));
+  if (S == 1) return 256;
   return align256(S * size_t(L.D) * dw_kp(L) * 4) + align256(S * dw_kp(L) * 4);
 }
 
 namespace {
 
-DwArgs make_dw_args(const Layer &L, const fqt_qgrad &q, const uint64_t *xsign, float *dW,
-                    int32_t *I_out, void *ws) {
+DwArgs make_dw_args(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                    const uint64_t *xsign, float *dW, int32_t *I_out, void *ws) {
   const uint32_t ktiles = uint32_t((L.K + 31) / 32);
-  const uint32_t S = uint32_t(gemm_dw_splits(L));
+  const uint32_t S = uint32_t(gemm_dw_splits(L, cfg));
   DwArgs a;
   a.codes = q.pcq_codes; a.kept = q.pcq_kept; a.count = q.pcq_count;
   a.scale = q.pcq_scale; a.offset = q.pcq_offset; a.slot_sz = nullptr; a.xsign = xsign;
   a.dW = dW; a.I_out = I_out;
-  a.part = static_cast<int32_t *>(ws);
-  a.partT = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
-                                        align256(size_t(S) * L.D * dw_kp(L) * 4));
+  a.part = S > 1 ? static_cast<int32_t *>(ws) : nullptr;
+  a.partT = S > 1 ? reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
+                                                align256(size_t(S) * L.D * dw_kp(L) * 4))
+                  : nullptr;
   a.D = uint32_t(L.D); a.K = uint32_t(L.K); a.Kp = uint32_t(dw_kp(L)); a.R = uint32_t(L.R);
   a.Rp = uint32_t(L.Wr * 64); a.Wr = uint32_t(L.Wr); a.ktiles = ktiles;
   a.codes_bytes = uint32_t(L.D * L.Wr * 64);
@@ -506,20 +645,33 @@ int dx_batch(const DxArgs &a) {
   return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;
 }
 
+template <bool B8>
+void launch_dw_finish(const Layer &L, const DwArgs &a, hipStream_t s) {
+  if (a.S > DWF_WIDE) {
+    const uint32_t qblocks = uint32_t((dw_kp(L) + 63) / 64);
+    hipLaunchKernelGGL(k_dw_finish_wide<B8>, dim3(unsigned(L.D) * qblocks), dim3(256), 0, s, a);
+  } else {
+    const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));
+    hipLaunchKernelGGL(k_dw_finish<B8>, fgrid, dim3(256), 0, s, a);
+  }
+}
+
 }  // namespace
 
 int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                    const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s) {
-  const DwArgs a = make_dw_args(L, q, xsign, dW, I_out, ws);
+  const DwArgs a = make_dw_args(L, cfg, q, xsign, dW, I_out, ws);
   const dim3 grid(dw_part_blocks(L, a));
-  const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));
-  if (cfg.bits == 8) {
-    hipLaunchKernelGGL(k_mfma_dw_part<true>, grid, dim3(DW_THREADS), 0, s, a);
-    hipLaunchKernelGGL(k_dw_finish<true>, fgrid, dim3(256), 0, s, a);
-  } else {
-    hipLaunchKernelGGL(k_mfma_dw_part<false>, grid, dim3(DW_THREADS), 0, s, a);
-    hipLaunchKernelGGL(k_dw_finish<false>, fgrid, dim3(256), 0, s, a);
-  }
+  auto go = [&]<bool B8>() {
+    if (a.S == 1) {
+      hipLaunchKernelGGL((k_mfma_dw_part<B8, true>), grid, dim3(DW_THREADS), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_mfma_dw_part<B8, false>), grid, dim3(DW_THREADS), 0, s, a);
+      launch_dw_finish<B8>(L, a, s);
+    }
+  };
+  if (cfg.bits == 8) go.template operator()<true>();
+  else go.template operator()<false>();
   return last_launch_status();
 }
 
@@ -545,22 +697,29 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
                     float *dW, void *dw_ws, const float2 *sslot, const float2 *cslot,
                     hipStream_t s) {
   if (L.kh * L.kw > DX_MAX_TAPS) return FQT_E_SHAPE;
-  DwArgs dwa = make_dw_args(L, q, xsign, dW, nullptr, dw_ws);
+  DwArgs dwa = make_dw_args(L, cfg, q, xsign, dW, nullptr, dw_ws);
   DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
   dwa.slot_sz = cslot;
   dxa.slot_sz = sslot;
   const uint32_t ndw = dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
-  const dim3 fgrid(unsigned((L.D * (dw_kp(L) / 4) + 255) / 256));
   const int nb = dx_batch(dxa);
-  auto go = [&]<bool B8>() {
-    if (nb == 4) hipLaunchKernelGGL((k_products<B8, 4>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
-    else if (nb == 8) hipLaunchKernelGGL((k_products<B8, 8>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
-    else hipLaunchKernelGGL((k_products<B8, 10>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
-    hipLaunchKernelGGL(k_dw_finish<B8>, fgrid, dim3(256), 0, s, dwa);
+  auto go = [&]<bool B8, bool DIRECT>() {
+    if (nb == 4)
+      hipLaunchKernelGGL((k_products<B8, 4, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    else if (nb == 8)
+      hipLaunchKernelGGL((k_products<B8, 8, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    else
+      hipLaunchKernelGGL((k_products<B8, 10, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+    if (!DIRECT) launch_dw_finish<B8>(L, dwa, s);
   };
-  if (cfg.bits == 8) go.template operator()<true>();
-  else go.template operator()<false>();
+  if (cfg.bits == 8) {
+    if (dwa.S == 1) go.template operator()<true, true>();
+    else go.template operator()<true, false>();
+  } else {
+    if (dwa.S == 1) go.template operator()<false, true>();
+    else go.template operator()<false, false>();
+  }
   return last_launch_status();
 }
 

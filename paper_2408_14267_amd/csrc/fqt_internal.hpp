@@ -95,7 +95,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                      const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s,
                      bool word_major = false);
-size_t gemm_dw_ws_bytes(const Layer &L);
+size_t gemm_dw_ws_bytes(const Layer &L, const fqt_quant_cfg &cfg);
 int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
                    const uint64_t *xsign, float *dW, int32_t *I_out, void *ws, hipStream_t s);
 int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, hipStream_t s);
