@@ -214,6 +214,7 @@ __global__ __launch_bounds__(RED_THREADS) void k_stats_reduce(const int2 *__rest
   if (b < N) {
     const uint32_t rt_lo = (b * g.P) / TILE, rt_hi = min(sg.nrt - 1, (b * g.P + g.P - 1) / TILE);
     const uint32_t cnt = rt_hi - rt_lo + 1;
+#pragma unroll 8
     for (uint32_t i = threadIdx.x; i < ndt * cnt; i += RED_THREADS) {
       const uint32_t dt = i / cnt, rt = rt_lo + i % cnt;
       const uint32_t k = b - fdiv(rt * TILE, g.divP);
@@ -223,6 +224,7 @@ __global__ __launch_bounds__(RED_THREADS) void k_stats_reduce(const int2 *__rest
     }
   } else {
     const uint32_t d = b - N;
+#pragma unroll 8
     for (uint32_t i = threadIdx.x; i < nrb; i += RED_THREADS) {
       const int2 v = part_c[size_t(i) * g.D + d];
       lo = min(lo, v.x);
@@ -1030,6 +1032,10 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   sa.bits = cfg.bits; sa.mode = cfg.agp_mode; sa.seed = cfg.seed; sa.step = cfg.step;
   sa.layer = cfg.layer_id;
   const int64_t gmax = L.N > L.D ? L.N : L.D;
+  // The one-workgroup selection reduces the partials itself; with many partials per group
+  // (large N*Ho*Wo) a workgroup per group reduces them first.
+  const bool many_partials =
+      nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256;
   int st;
   // Sign operands in the selection launch: a convolution whose X and W share a dtype and
   // whose band fits the LDS left beside the selection (64 KB per workgroup in all).
@@ -1037,7 +1043,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   size_t band_lds = 0;
   const int gp = gmax <= 256 ? 256 : 1024;
   const bool with_signs =
-      signs && gmax <= 1024 && L.x_t == L.w_t &&
+      signs && gmax <= 1024 && !many_partials && L.x_t == L.w_t &&
       band_geom(L, signs->X, L.x_t, SEL_NT, 65536 - 512 - select_signs_static_lds(gp), &bg,
                 &band_lds);
   if (with_signs) {
@@ -1062,10 +1068,10 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     });
     st = last_launch_status();
     signs->done = st == FQT_OK;
-  } else if (gmax <= 256) {
+  } else if (gmax <= 256 && !many_partials) {
     hipLaunchKernelGGL(k_select_fused<256>, dim3(2), dim3(SEL_NT), 0, s, sa);
     st = last_launch_status();
-  } else if (gmax <= 1024) {
+  } else if (gmax <= 1024 && !many_partials) {
     hipLaunchKernelGGL(k_select_fused<1024>, dim3(2), dim3(SEL_NT), 0, s, sa);
     st = last_launch_status();
   } else {

@@ -61,6 +61,10 @@ CASES = [
      0, Recipe("sample_lognormal", sigma=1.0), "bf16"),
     ("conv_p64_ragged_b2", LayerShape("c", "conv2d", 3, 33, 40, 8, 8, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # 65536 output pixels per sample: group partials reduced by a workgroup per group before
+    # the selection; many dW splits with the block-per-row finish.
+    ("conv_bigmap_b2", LayerShape("c", "conv2d", 2, 4, 16, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
 ]
 
 
