@@ -231,7 +231,8 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     BandGeom bg;
     size_t lds = 0;
     if (word_major && band_geom(L, src, dtype, THREADS, 48 * 1024, &bg, &lds)) {
-      const dim3 bgrid(unsigned(L.Wr), unsigned((L.C + BAND_CPW * WAVES - 1) / (BAND_CPW * WAVES)));
+      const dim3 bgrid(band_word_blocks(L, bg),
+                       unsigned((L.C + BAND_CPW * WAVES - 1) / (BAND_CPW * WAVES)));
       dispatch_dtype(dtype, [&]<int DT>() {
         if (L.kh == 3 && L.kw == 3)
           hipLaunchKernelGGL((k_pack_im2col_band<DT, 3, 3>), bgrid, dim3(THREADS), lds, s, src,

@@ -255,6 +255,7 @@ struct SetArgs {
   const int2 *key;     // [G] (min, max) keys (k_select)
   const int2 *part;    // partials (k_select_fused)
   uint32_t slots;      // 0: group g reduces part[u * ld + g], u < U (channels)
+                       // 2: key[g] already holds the group's key (k_stats_reduce ran)
                        // 1: sample slots of part_s (P, nrt, SL, ndt)
   uint32_t U, ld;
   uint32_t P, nrt, SL, ndt;
@@ -574,7 +575,13 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
     constexpr int SPLIT = SEL_NT / GP;
     const int g = t % GP, r0 = t / GP;
     int lo = INT_MAX, hi = INT_MIN;
-    if (g < G && !S.slots) {            // channels: row-block partials, adjacent per row
+    if (S.slots == 2) {                 // keys reduced beforehand
+      if (g < G && r0 == 0) {
+        const int2 k = S.key[g];
+        lo = k.x;
+        hi = k.y;
+      }
+    } else if (g < G && !S.slots) {     // channels: row-block partials, adjacent per row
       // One per-lane offset (the group) and a wave-uniform one per row block (r0 is
       // uniform across each wave).
       const __amdgpu_buffer_rsrc_t prs = buffer_of(S.part, S.U * S.ld * 8);
@@ -763,13 +770,13 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
 
 // The same two selection workgroups, then spare workgroups that pack the products' sign
 // operands (they do not depend on dY): blocks [2, 2 + npw) the weight bytes, the rest the
-// band im2col of X (word fastest, then 64-channel groups).
+// band im2col of X (word group fastest, then 64-channel groups).
 struct SignArgs {
   const void *x;
   BandGeom bg;
   uint64_t *xsign;
-  uint32_t Wr;
-  FastDiv divWr;
+  uint32_t nwb;          // word-group blocks of the band (samples x word groups)
+  FastDiv divNwb;
   const void *w;
   PackWGeom pg;
   int8_t *wsb;
@@ -788,8 +795,8 @@ __global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) voi
     pack_w_body<DT>(sg.w, sg.pg, sg.wsb, sg.wlsum, b - 2, pws);
   } else {
     const uint32_t f = b - 2 - sg.npw;
-    const uint32_t cb = fdiv(f, sg.divWr);
-    band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.Wr, cb, band);
+    const uint32_t cb = fdiv(f, sg.divNwb);
+    band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.nwb, cb, band);
   }
 }
 // Static LDS of k_select_signs<GP>: the selection's arrays and the weight-byte tile.
@@ -1037,23 +1044,30 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   const bool many_partials =
       nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256;
   int st;
+  if (gmax <= 1024 && many_partials) {
+    hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,
+                       w.part_c, w.part_s, sg, nrb, ndt, w.skey, w.ckey);
+    if (last_launch_status() != FQT_OK) return FQT_E_HIP;
+    sa.set[0].slots = 2;          // the selection reads the reduced keys
+    sa.set[1].slots = 2;
+  }
   // Sign operands in the selection launch: a convolution whose X and W share a dtype and
   // whose band fits the LDS left beside the selection (64 KB per workgroup in all).
   BandGeom bg;
   size_t band_lds = 0;
   const int gp = gmax <= 256 ? 256 : 1024;
   const bool with_signs =
-      signs && gmax <= 1024 && !many_partials && L.x_t == L.w_t &&
+      signs && gmax <= 1024 && L.x_t == L.w_t &&
       band_geom(L, signs->X, L.x_t, SEL_NT, 65536 - 512 - select_signs_static_lds(gp), &bg,
                 &band_lds);
   if (with_signs) {
     SignArgs sg;
     sg.x = signs->X; sg.bg = bg; sg.xsign = signs->xsign;
-    sg.Wr = uint32_t(L.Wr); sg.divWr = make_fastdiv(uint32_t(L.Wr));
+    sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);
     sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
     sg.npw = pack_w_blocks(L);
     const uint32_t cgroups = uint32_t((L.C + BAND_CPW * SEL_NW - 1) / (BAND_CPW * SEL_NW));
-    const dim3 grid(2 + sg.npw + uint32_t(L.Wr) * cgroups);
+    const dim3 grid(2 + sg.npw + sg.nwb * cgroups);
     dispatch_dtype(L.x_t, [&]<int DT>() {
       auto go = [&]<int GPT>() {
         if (L.kh == 3 && L.kw == 3)
@@ -1068,11 +1082,9 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     });
     st = last_launch_status();
     signs->done = st == FQT_OK;
-  } else if (gmax <= 256 && !many_partials) {
-    hipLaunchKernelGGL(k_select_fused<256>, dim3(2), dim3(SEL_NT), 0, s, sa);
-    st = last_launch_status();
-  } else if (gmax <= 1024 && !many_partials) {
-    hipLaunchKernelGGL(k_select_fused<1024>, dim3(2), dim3(SEL_NT), 0, s, sa);
+  } else if (gmax <= 1024) {
+    if (gmax <= 256) hipLaunchKernelGGL(k_select_fused<256>, dim3(2), dim3(SEL_NT), 0, s, sa);
+    else hipLaunchKernelGGL(k_select_fused<1024>, dim3(2), dim3(SEL_NT), 0, s, sa);
     st = last_launch_status();
   } else {
     hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,

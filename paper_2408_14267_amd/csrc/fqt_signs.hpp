@@ -7,6 +7,8 @@
 // of the AGP selection launch, whose two selection workgroups leave the chip idle.
 #pragma once
 
+#include <algorithm>
+
 #include "fqt_internal.hpp"
 
 namespace fqt {
@@ -14,61 +16,80 @@ namespace fqt {
 // ----------------------------------------------------------------------------- band im2col
 // Bit-im2col through LDS, word-major output, for layers whose output positions per sample
 // are a multiple of 64 (every 64-position word lies in one sample) and whose rows are
-// whole 16-byte quads (W % 4 == 0, pw <= 4).  A block takes one word w (output positions
-// p0 .. p0 + 63 of sample n) and BAND_CPW channels per wave: it stages, per channel, the
-// band of input rows those positions read as one byte per pixel (1 = positive), each band
-// row framed by four zero bytes on either side and rows outside the image all zero; a
-// lane loads one 16-byte quad and writes one LDS dword.  Then each (channel, tap) word is
-// one LDS byte per lane and a ballot.  Lane l reads band row (ho - ho_lo) * sh + i, column
-// wo * sw + j - pw + 4 for its position (ho, wo) and tap (i, j); band row 0 is image row
-// ho_lo * sh - ph.
+// whole 16-byte quads (W % 4 == 0, pw <= 4).  A block takes up to wpb consecutive words of
+// one sample (output positions p0 .. p0 + 64 wpb - 1) and BAND_CPW channels per wave: it
+// stages, per channel, the band of input rows those positions read as one byte per pixel
+// (1 = positive), each band row framed by four zero bytes on either side and rows outside
+// the image all zero; a lane loads one 16-byte quad and writes one LDS dword.  Then each
+// (word, channel, tap) is one LDS byte per lane and a ballot.  Lane l of word j reads band
+// row (ho - ho_lo) * sh + i, column wo * sw + j' - pw + 4 for its position (ho, wo) and tap
+// (i, j'); band row 0 is image row ho_lo * sh - ph.  Several words per block keep wide
+// images from staging whole rows for a fraction of their columns.
 constexpr int BAND_CPW = 4;            // channels per wave
 struct BandGeom {
   uint32_t C, H, W, Wo, P, K, taps, BR, WL, plane;   // WL = W + 8, plane = BR * WL
   uint32_t qrow;                                     // dwords per band row, WL / 4
+  uint32_t wps, wpb, wgroups;    // words per sample, per block, word groups per sample
   int kw, sh, sw, ph, pw;
-  FastDiv divWo, divP, divQrow, divBR, divKw;
+  FastDiv divWo, divP, divQrow, divBR, divKw, divWg;
 };
 
 // Geometry of the band im2col for blocks of `nt` threads (BAND_CPW * nt / 64 channels),
-// or false when the layer does not fit it or its band exceeds `lds_max` bytes.
+// or false when the layer does not fit it or its band exceeds `lds_max` bytes.  Up to 16
+// words per block, as many as the band for them fits while the grid keeps about 2048
+// blocks.
 inline bool band_geom(const Layer &L, const void *x, int dtype, int nt, size_t lds_max,
                       BandGeom *bg, size_t *lds) {
   const bool quads_ok = reinterpret_cast<uintptr_t>(x) % (dtype == FQT_BF16 ? 8 : 16) == 0;
   if (L.kind != FQT_CONV2D || !quads_ok || L.P % 64 != 0 || L.W % 4 != 0 || L.pw > 4 ||
       L.kh * L.kw > 64)
     return false;
-  // Band of input rows read by one word: its output rows times the stride plus the kernel
-  // height.
-  const int64_t orows = (64 + L.Wo - 1) / L.Wo + 1;
-  const int64_t BR = (orows - 1) * L.sh + L.kh;
+  const int64_t wps = L.P / 64;
   const int64_t WL = L.W + 8;
-  const int64_t plane = BR * WL;
-  const size_t bytes = size_t(plane) * BAND_CPW * (nt / 64);
-  if (bytes > lds_max) return false;
-  *bg = BandGeom{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
-                 uint32_t(L.K), uint32_t(L.kh * L.kw), uint32_t(BR), uint32_t(WL),
-                 uint32_t(plane), uint32_t(WL / 4), L.kw, L.sh, L.sw, L.ph, L.pw,
-                 make_fastdiv(uint32_t(L.Wo)), make_fastdiv(uint32_t(L.P)),
-                 make_fastdiv(uint32_t(WL / 4)), make_fastdiv(uint32_t(BR)),
-                 make_fastdiv(uint32_t(L.kw))};
-  *lds = bytes;
-  return true;
+  const int64_t chans = int64_t(BAND_CPW) * (nt / 64);
+  const int64_t cgroups = (L.C + chans - 1) / chans;
+  const int64_t wmax = std::max<int64_t>(1, L.N * wps * cgroups / 2048);
+  for (int64_t wpb = std::min<int64_t>({wps, 16, wmax}); wpb >= 1; --wpb) {
+    // Band of input rows read by wpb words: the output rows they can span times the
+    // stride plus the kernel height.
+    const int64_t orows = (64 * wpb - 1 + L.Wo - 1) / L.Wo + 1;
+    const int64_t BR = (orows - 1) * L.sh + L.kh;
+    const int64_t plane = BR * WL;
+    const size_t bytes = size_t(plane * chans);
+    if (bytes > lds_max) continue;
+    const int64_t wgroups = (wps + wpb - 1) / wpb;
+    *bg = BandGeom{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
+                   uint32_t(L.K), uint32_t(L.kh * L.kw), uint32_t(BR), uint32_t(WL),
+                   uint32_t(plane), uint32_t(WL / 4), uint32_t(wps), uint32_t(wpb),
+                   uint32_t(wgroups), L.kw, L.sh, L.sw, L.ph, L.pw,
+                   make_fastdiv(uint32_t(L.Wo)), make_fastdiv(uint32_t(L.P)),
+                   make_fastdiv(uint32_t(WL / 4)), make_fastdiv(uint32_t(BR)),
+                   make_fastdiv(uint32_t(L.kw)), make_fastdiv(uint32_t(wgroups))};
+    *lds = bytes;
+    return true;
+  }
+  return false;
+}
+// Blocks along the words: samples x word groups.
+inline uint32_t band_word_blocks(const Layer &L, const BandGeom &bg) {
+  return uint32_t(L.N) * bg.wgroups;
 }
 
-// One block of NT threads: word w, channels [cblk * BAND, (cblk + 1) * BAND).  band: the
-// block's LDS, BAND * plane bytes.
+// One block of NT threads: word group `wb` (sample wb / wgroups), channels
+// [cblk * BAND, (cblk + 1) * BAND).  band: the block's LDS, BAND * plane bytes.
 template <int DT, int KH, int KW, int NT>
 __device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, const BandGeom &g,
-                                                 uint64_t *__restrict__ dst, uint32_t w,
+                                                 uint64_t *__restrict__ dst, uint32_t wb,
                                                  uint32_t cblk, uint32_t *band) {
   constexpr int NW = NT / 64, BAND = BAND_CPW * NW;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const uint32_t c0 = cblk * BAND;
   const uint32_t nch = min(uint32_t(BAND), g.C - c0);
-  const uint32_t r0 = w * 64;
-  const uint32_t n = fdiv(r0, g.divP), p0 = r0 - n * g.P;
+  const uint32_t n = fdiv(wb, g.divWg), wg = wb - n * g.wgroups;
+  const uint32_t wfirst = wg * g.wpb;                       // first word within the sample
+  const uint32_t nwords = min(g.wpb, g.wps - wfirst);
+  const uint32_t p0 = wfirst * 64;
   const uint32_t ho_lo = fdiv(p0, g.divWo);
   const int h_base = int(ho_lo) * g.sh - g.ph;   // image row of band row 0
   const size_t xbase = (size_t(n) * g.C + c0) * g.H * g.W;   // element (c0, 0, 0) of sample n
@@ -103,46 +124,49 @@ __device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, con
   }
   __syncthreads();
 
-  // This lane's output position and its band byte offset for tap (0, 0).
   const uint8_t *bb = reinterpret_cast<const uint8_t *>(band);
-  const uint32_t p = p0 + lane;
-  const uint32_t ho = fdiv(p, g.divWo), wo = p - ho * g.Wo;
-  const uint32_t base = (ho - ho_lo) * g.sh * g.WL + wo * g.sw + 4 - g.pw;
   const uint32_t cl_lo = wave * BAND_CPW, cl_hi = min(nch, cl_lo + BAND_CPW);
-  uint32_t mlo = 0, mhi = 0;                     // words gather in lanes 0 .. 63
-  int filled = 0;
-  uint64_t *out = dst + size_t(w) * g.K;
-  auto put = [&](uint64_t m, uint32_t line_last) {
-    mlo = writelane(uint32_t(m), filled, mlo);
-    mhi = writelane(uint32_t(m >> 32), filled, mhi);
-    if (++filled == 64) {                        // 64 words of consecutive lines
-      out[line_last - 63 + lane] = (uint64_t(mhi) << 32) | mlo;
-      filled = 0;
-    }
-  };
-  for (uint32_t cl = cl_lo; cl < cl_hi; ++cl) {
-    const uint8_t *pl = bb + cl * g.plane + base;
-    if constexpr (KH > 0) {
-      // Kernel size fixed at compile time: every tap's LDS read issues before the ballots.
-      uint8_t b[KH * KW];
+  if (cl_hi <= cl_lo) return;
+  for (uint32_t j = 0; j < nwords; ++j) {
+    // This lane's output position in word j and its band byte offset for tap (0, 0).
+    const uint32_t p = p0 + 64 * j + lane;
+    const uint32_t ho = fdiv(p, g.divWo), wo = p - ho * g.Wo;
+    const uint32_t base = (ho - ho_lo) * g.sh * g.WL + wo * g.sw + 4 - g.pw;
+    uint32_t mlo = 0, mhi = 0;                   // words gather in lanes 0 .. 63
+    int filled = 0;
+    uint64_t *out = dst + size_t(n * g.wps + wfirst + j) * g.K;
+    auto put = [&](uint64_t m, uint32_t line_last) {
+      mlo = writelane(uint32_t(m), filled, mlo);
+      mhi = writelane(uint32_t(m >> 32), filled, mhi);
+      if (++filled == 64) {                      // 64 words of consecutive lines
+        out[line_last - 63 + lane] = (uint64_t(mhi) << 32) | mlo;
+        filled = 0;
+      }
+    };
+    for (uint32_t cl = cl_lo; cl < cl_hi; ++cl) {
+      const uint8_t *pl = bb + cl * g.plane + base;
+      if constexpr (KH > 0) {
+        // Kernel size fixed at compile time: every tap's LDS read issues before the ballots.
+        uint8_t b[KH * KW];
 #pragma unroll
-      for (int i = 0; i < KH; ++i)
+        for (int i = 0; i < KH; ++i)
 #pragma unroll
-        for (int j = 0; j < KW; ++j) b[i * KW + j] = pl[i * g.WL + j];
+          for (int jj = 0; jj < KW; ++jj) b[i * KW + jj] = pl[i * g.WL + jj];
 #pragma unroll
-      for (int tap = 0; tap < KH * KW; ++tap)
-        put(__ballot(b[tap] != 0), (c0 + cl) * (KH * KW) + tap);
-    } else {
-      for (uint32_t tap = 0; tap < g.taps; ++tap) {
-        const uint32_t i = fdiv(tap, g.divKw), j = tap - i * g.kw;
-        put(__ballot(pl[i * g.WL + j] != 0), (c0 + cl) * g.taps + tap);
+        for (int tap = 0; tap < KH * KW; ++tap)
+          put(__ballot(b[tap] != 0), (c0 + cl) * (KH * KW) + tap);
+      } else {
+        for (uint32_t tap = 0; tap < g.taps; ++tap) {
+          const uint32_t i = fdiv(tap, g.divKw), jj = tap - i * g.kw;
+          put(__ballot(pl[i * g.WL + jj] != 0), (c0 + cl) * g.taps + tap);
+        }
       }
     }
-  }
-  if (filled > 0 && cl_hi > cl_lo) {
-    // The words left end at the wave's last line.
-    const uint32_t l_end = (c0 + cl_hi) * g.taps;
-    if (lane < filled) out[l_end - filled + lane] = (uint64_t(mhi) << 32) | mlo;
+    if (filled > 0) {
+      // The words left end at the wave's last line.
+      const uint32_t l_end = (c0 + cl_hi) * g.taps;
+      if (lane < filled) out[l_end - filled + lane] = (uint64_t(mhi) << 32) | mlo;
+    }
   }
 }
 
