@@ -197,6 +197,61 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
   if (wave == 1 && d0 + lane < g.D) part_c[size_t(blockIdx.x) * g.D + d0 + lane] = cpart[lane];
 }
 
+// Large maps (Ho*Wo >= 1024): the (min, max) key of every (sample, channel) plane of dY,
+// each a contiguous run of P elements, streamed by one wave with 8 quads per lane in
+// flight; ppl[n * D + d].  A sample's key is the reduction of its D planes, a channel's of
+// its N planes.
+constexpr int PLANE_U = 8;
+template <int DT>
+__global__ __launch_bounds__(256) void k_stats_planes(const void *__restrict__ dy,
+                                                      uint32_t planes, uint32_t P4,
+                                                      int2 *__restrict__ ppl) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t nwaves = gridDim.x * 4;
+  for (uint32_t pl = blockIdx.x * 4 + (threadIdx.x >> 6); pl < planes; pl += nwaves) {
+    int lo = INT_MAX, hi = INT_MIN;
+    const int64_t base = int64_t(pl) * P4 * 4;
+    // Whole batches (no per-lane test: every load issues before the first use), then the
+    // tail with out-of-plane quads reading element 0 and masked.
+    uint32_t qb = 0;
+    for (; qb + 64 * PLANE_U <= P4; qb += 64 * PLANE_U) {
+      float v[PLANE_U][4];
+#pragma unroll
+      for (int u = 0; u < PLANE_U; ++u)
+        load_quad<DT>(dy, base + 4 * int64_t(qb + 64 * u + lane), v[u]);
+#pragma unroll
+      for (int u = 0; u < PLANE_U; ++u)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int key = f2key(v[u][k] + 0.0f);
+          lo = min(lo, key);
+          hi = max(hi, key);
+        }
+    }
+    if (qb < P4) {
+      float v[PLANE_U][4];
+#pragma unroll
+      for (int u = 0; u < PLANE_U; ++u) {
+        const uint32_t q = qb + 64 * u + lane;
+        load_quad<DT>(dy, q < P4 ? base + 4 * int64_t(q) : 0, v[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < PLANE_U; ++u) {
+        const bool in = qb + 64 * u + lane < P4;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int key = f2key(v[u][k] + 0.0f);
+          lo = min(lo, in ? key : INT_MAX);
+          hi = max(hi, in ? key : INT_MIN);
+        }
+      }
+    }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    if (lane == 0) ppl[pl] = make_int2(lo, hi);
+  }
+}
+
 // Large group sets: block b < N reduces sample b over its slots, block N + d channel d
 // over its row-block partials.
 constexpr int RED_THREADS = 256;
@@ -255,7 +310,9 @@ struct SetArgs {
   const int2 *key;     // [G] (min, max) keys (k_select)
   const int2 *part;    // partials (k_select_fused)
   uint32_t slots;      // 0: group g reduces part[u * ld + g], u < U (channels)
+                       // 1: sample slots of part_s (P, nrt, SL, ndt)
                        // 2: key[g] already holds the group's key (k_stats_reduce ran)
+                       // 3: group g reduces part[g * ld + u], u < U (per-plane partials)
                        // 1: sample slots of part_s (P, nrt, SL, ndt)
   uint32_t U, ld;
   uint32_t P, nrt, SL, ndt;
@@ -592,6 +649,22 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
         for (int k = 0; k < 16; ++k) {
           const uint32_t u = u0 + k * SPLIT;
           v[k] = load8(prs, u < S.U ? voff : BUF_NONE, u < S.U ? u * S.ld * 8 : 0);
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          if (u0 + k * SPLIT >= S.U) break;
+          lo = min(lo, int(uint32_t(v[k])));
+          hi = max(hi, int(uint32_t(v[k] >> 32)));
+        }
+      }
+    } else if (g < G && S.slots == 3) { // group g reduces part[g * ld + u], u < U
+      const __amdgpu_buffer_rsrc_t prs = buffer_of(S.part, uint32_t(S.G) * S.ld * 8);
+      for (uint32_t u0 = r0; u0 < S.U; u0 += 16 * SPLIT) {
+        uint64_t v[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const uint32_t u = u0 + k * SPLIT;
+          v[k] = load8(prs, u < S.U ? (uint32_t(g) * S.ld + u) * 8 : BUF_NONE, 0);
         }
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
@@ -1016,7 +1089,18 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   const uint32_t nrb = uint32_t(stats_row_blocks(L));
   const dim3 grid(nrb, ndt);
   const int mode = (L.P % 4 == 0) ? TILE_PIX : (L.P == 1 && L.D % 4 == 0) ? TILE_CHAN : TILE_SCALAR;
-  dispatch_dtype(L.dy_t, [&]<int DT>() {
+  const int64_t gmax = L.N > L.D ? L.N : L.D;
+  // Large maps with both group sets in one-workgroup selections: per-plane statistics
+  // (part_c holds the N * D plane keys: it has D * stats_row_blocks >= D * N entries).
+  const bool planes = L.P >= 1024 && L.P % 4 == 0 && gmax <= 1024;
+  if (planes) {
+    const uint32_t np = uint32_t(L.N * L.D);
+    const uint32_t blocks = std::min<uint32_t>((np + 3) / 4, 4096);
+    dispatch_dtype(L.dy_t, [&]<int DT>() {
+      hipLaunchKernelGGL(k_stats_planes<DT>, dim3(blocks), dim3(256), 0, s, dY, np,
+                         uint32_t(L.P / 4), w.part_c);
+    });
+  } else dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
       hipLaunchKernelGGL((k_stats<TILE_PIX, DT>), grid, dim3(THREADS), 0, s, dY, sg, w.part_c,
                          w.part_s);
@@ -1038,11 +1122,15 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
                       q.pcq_scale, q.pcq_offset, q.pcq_prob, w.cp, w.cslot};
   sa.bits = cfg.bits; sa.mode = cfg.agp_mode; sa.seed = cfg.seed; sa.step = cfg.step;
   sa.layer = cfg.layer_id;
-  const int64_t gmax = L.N > L.D ? L.N : L.D;
+  if (planes) {
+    sa.set[0].slots = 3; sa.set[0].part = w.part_c; sa.set[0].U = uint32_t(L.D);
+    sa.set[0].ld = uint32_t(L.D);
+    sa.set[1].slots = 0; sa.set[1].U = uint32_t(L.N); sa.set[1].ld = uint32_t(L.D);
+  }
   // The one-workgroup selection reduces the partials itself; with many partials per group
   // (large N*Ho*Wo) a workgroup per group reduces them first.
   const bool many_partials =
-      nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256;
+      !planes && (nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256);
   int st;
   if (gmax <= 1024 && many_partials) {
     hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,
