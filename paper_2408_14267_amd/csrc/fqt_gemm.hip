@@ -376,9 +376,11 @@ struct DxArgs {
   int kh, kw, sh, sw, ph, pw;
   FastDiv divHW, divW, divKw, divNch, divCt;
   uint32_t nblocks;              // blocks of the dX grid (compute tiles + zero pool)
+  uint32_t zpieces;              // pieces of DX_ZCHUNK elements per pruned sample
 };
 
 constexpr int DX_MAX_TAPS = 64;
+constexpr uint32_t DX_ZCHUNK = 65536;    // elements of a pruned sample one block zeroes
 constexpr int DX_WAVES = 4;
 constexpr int DX_THREADS = DX_WAVES * 64;
 
@@ -386,8 +388,8 @@ constexpr int DX_THREADS = DX_WAVES * 64;
 // that the common shapes take one batch: the loads of a wave then cost one memory latency.
 // Grid: one block per 32x32 tile of (channel, row m = (kept slot, h, w)) over the capacity
 // N*H*W rows, plus a pool of extra blocks.  Blocks of the first ceil(count*H*W/32) row
-// tiles compute; all later blocks zero the pruned samples of dX, each a contiguous run of
-// C*H*W elements.
+// tiles compute; all later blocks zero the pruned samples of dX (each a contiguous run of
+// C*H*W elements) in pieces of DX_ZCHUNK elements.
 // A computing block is one 32x32 MFMA tile with the sign operand as src0 (rows =
 // channels) so output lanes run along pixels.  Its four waves take every fourth
 // contraction step (tap, 32 bytes of D).  For tap (i, j) a pixel (h, w) reads the code row
@@ -438,12 +440,16 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   const uint32_t live_rows = uint32_t(count) * a.HW;
   const uint32_t live_blocks = ((live_rows + 31) / 32) * a.ctiles;
 
-  if (bid >= live_blocks) {      // zero the pruned samples, one sample per block
+  if (bid >= live_blocks) {      // zero the pruned samples, a piece of one per block
     const uint32_t nz = a.nblocks - live_blocks;
-    for (uint32_t slot = bid - live_blocks; slot < a.N - uint32_t(count); slot += nz) {
+    const uint32_t tasks = (a.N - uint32_t(count)) * a.zpieces;
+    for (uint32_t task = bid - live_blocks; task < tasks; task += nz) {
+      const uint32_t slot = task / a.zpieces, piece = task - slot * a.zpieces;
       const size_t n = size_t(a.kept[uint32_t(count) + slot]);
-      zero_run(a.dX, n * a.CHW, a.CHW, a.dx_t == FQT_BF16 ? 2 : 4, t, DX_THREADS);
-      if (a.I_out) zero_run(a.I_out, n * a.CHW, a.CHW, 4, t, DX_THREADS);
+      const size_t first = size_t(piece) * DX_ZCHUNK;
+      const size_t len = min(size_t(DX_ZCHUNK), size_t(a.CHW) - first);
+      zero_run(a.dX, n * a.CHW + first, len, a.dx_t == FQT_BF16 ? 2 : 4, t, DX_THREADS);
+      if (a.I_out) zero_run(a.I_out, n * a.CHW + first, len, 4, t, DX_THREADS);
     }
     return;
   }
@@ -633,9 +639,12 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
   a.divHW = make_fastdiv(uint32_t(L.HW)); a.divW = make_fastdiv(uint32_t(L.W));
   a.divKw = make_fastdiv(uint32_t(L.kw)); a.divNch = make_fastdiv(a.nch);
   a.divCt = make_fastdiv(a.ctiles);
-  // Capacity tiles plus a pool of blocks that only zero pruned samples: whatever the
-  // device-side count, at least min(256, N) blocks are left for the zeroing.
-  a.nblocks = uint32_t(((L.N * L.HW + 31) / 32) * a.ctiles + std::min<int64_t>(256, L.N));
+  // Capacity tiles plus a pool of blocks that only zero pruned samples, a piece of at most
+  // DX_ZCHUNK elements each: whatever the device-side count, at least
+  // min(2048, N * pieces) blocks are left for the zeroing.
+  a.zpieces = uint32_t((int64_t(a.CHW) + DX_ZCHUNK - 1) / DX_ZCHUNK);
+  a.nblocks = uint32_t(((L.N * L.HW + 31) / 32) * a.ctiles +
+                       std::min<int64_t>(2048, L.N * int64_t(a.zpieces)));
   return a;
 }
 // Contraction steps of one dX wave, rounded to the instantiated batch depths (10 steps
