@@ -26,6 +26,7 @@
 // word-major X signs, chunk-major weight bytes), so one operand load of a wave reads
 // about 1 KB of contiguous memory instead of one cache line per lane.
 #include <algorithm>
+#include <type_traits>
 
 #include "fqt_internal.hpp"
 
@@ -377,6 +378,7 @@ struct DxArgs {
   FastDiv divHW, divW, divKw, divNch, divCt;
   uint32_t nblocks;              // blocks of the dX grid (compute tiles + zero pool)
   uint32_t zpieces;              // pieces of DX_ZCHUNK elements per pruned sample
+  uint32_t wide;                 // 1: four pixel tiles per block, one per wave
 };
 
 constexpr int DX_MAX_TAPS = 64;
@@ -406,6 +408,22 @@ struct alignas(16) DxLds {
   int32_t pix_out[32];                  // NCHW offset of (sample, pixel) minus channel
   float pix_s[32], pix_z[32];
 };
+
+// Zeroing of the pruned samples by the blocks of the zero pool: task t of
+// (N - count) * zpieces is piece t % zpieces of pruned slot t / zpieces.
+__device__ __forceinline__ void dx_zero_pool(const DxArgs &a, uint32_t zb, uint32_t nz,
+                                             int count) {
+  const int t = threadIdx.x;
+  const uint32_t tasks = (a.N - uint32_t(count)) * a.zpieces;
+  for (uint32_t task = zb; task < tasks; task += nz) {
+    const uint32_t slot = task / a.zpieces, piece = task - slot * a.zpieces;
+    const size_t n = size_t(a.kept[uint32_t(count) + slot]);
+    const size_t first = size_t(piece) * DX_ZCHUNK;
+    const size_t len = min(size_t(DX_ZCHUNK), size_t(a.CHW) - first);
+    zero_run(a.dX, n * a.CHW + first, len, a.dx_t == FQT_BF16 ? 2 : 4, t, DX_THREADS);
+    if (a.I_out) zero_run(a.I_out, n * a.CHW + first, len, 4, t, DX_THREADS);
+  }
+}
 
 template <bool B8, int NB>
 __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm) {
@@ -441,16 +459,7 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   const uint32_t live_blocks = ((live_rows + 31) / 32) * a.ctiles;
 
   if (bid >= live_blocks) {      // zero the pruned samples, a piece of one per block
-    const uint32_t nz = a.nblocks - live_blocks;
-    const uint32_t tasks = (a.N - uint32_t(count)) * a.zpieces;
-    for (uint32_t task = bid - live_blocks; task < tasks; task += nz) {
-      const uint32_t slot = task / a.zpieces, piece = task - slot * a.zpieces;
-      const size_t n = size_t(a.kept[uint32_t(count) + slot]);
-      const size_t first = size_t(piece) * DX_ZCHUNK;
-      const size_t len = min(size_t(DX_ZCHUNK), size_t(a.CHW) - first);
-      zero_run(a.dX, n * a.CHW + first, len, a.dx_t == FQT_BF16 ? 2 : 4, t, DX_THREADS);
-      if (a.I_out) zero_run(a.I_out, n * a.CHW + first, len, 4, t, DX_THREADS);
-    }
+    dx_zero_pool(a, bid - live_blocks, a.nblocks - live_blocks, count);
     return;
   }
 
@@ -544,19 +553,163 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   }
 }
 
+// Large layers (many row tiles, at most DXW_MAX_TAPS taps): a block holds four pixel
+// tiles of 32 rows and one channel tile; wave w runs the whole contraction of tile w (no
+// split over the waves, no reduction), the four waves sharing the sign operand through
+// the L1 cache.  The per-(tap, pixel) code row offsets of the block's 128 pixels and the
+// channel sign sums are tabulated in LDS as in the split form.
+constexpr int DXW_TILES = DX_WAVES;
+constexpr int DXW_MAX_TAPS = 16;
+struct alignas(16) DxWideLds {
+  uint32_t rowoff[DXW_MAX_TAPS][DXW_TILES * 32];
+  int32_t wl[DXW_MAX_TAPS][32];
+  int32_t pix_out[DXW_TILES * 32];
+  float pix_s[DXW_TILES * 32], pix_z[DXW_TILES * 32];
+};
+
 template <bool B8, int NB>
+__device__ __forceinline__ void dx_body_wide(const DxArgs &a, uint32_t bid, DxWideLds &sm) {
+  constexpr uint32_t BP = DXW_TILES * 32;        // pixel rows per block
+  const int t = threadIdx.x, lane = t & 63;
+  const uint32_t wave = wave_id();
+  const int i = lane & 31, g = lane >> 5;
+  const int count = *a.count;
+  const uint32_t mt = fdiv(bid, a.divCt);
+  const uint32_t m0 = mt * BP, c0 = (bid - mt * a.ctiles) * 32;
+  const int taps = int(a.taps);
+  // Loads that do not depend on the count issue with it (clamped indices).
+  int kn = 0;
+  float2 sz = make_float2(0.0f, 0.0f);
+  uint32_t ppix = 0;
+  if (t < int(BP)) {
+    const uint32_t m = min(m0 + uint32_t(t), a.N * a.HW - 1);
+    const uint32_t pslot = fdiv(m, a.divHW);
+    ppix = m - pslot * a.HW;
+    kn = a.kept[pslot];
+    if (a.slot_sz) sz = a.slot_sz[pslot];
+  }
+  constexpr int WLT = DXW_MAX_TAPS * 32 / DX_THREADS;
+  int wlv[WLT];
+#pragma unroll
+  for (int k = 0; k < WLT; ++k) {
+    const int e = t + k * DX_THREADS, p = e & 31, tap = e >> 5;
+    const uint32_t ch = c0 + uint32_t(p);
+    wlv[k] = (e < 32 * taps && ch < a.C) ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
+  }
+  const uint32_t live_rows = uint32_t(count) * a.HW;
+  const uint32_t live_blocks = ((live_rows + BP - 1) / BP) * a.ctiles;
+  if (bid >= live_blocks) {
+    dx_zero_pool(a, bid - live_blocks, a.nblocks - live_blocks, count);
+    return;
+  }
+  if (t < int(BP)) {
+    const bool live = m0 + uint32_t(t) < live_rows;
+    if (!a.slot_sz && live) sz = make_float2(a.scale[kn], a.offset[kn]);
+    sm.pix_out[t] = live ? int(uint32_t(kn) * a.CHW + ppix) : -1;
+    sm.pix_s[t] = live ? sz.x : 0.0f;
+    sm.pix_z[t] = live ? sz.y : 0.0f;
+  }
+#pragma unroll
+  for (int k = 0; k < WLT; ++k) {
+    const int e = t + k * DX_THREADS;
+    if (e < 32 * taps) sm.wl[e >> 5][e & 31] = wlv[k];
+  }
+  for (int e = t; e < int(BP) * taps; e += DX_THREADS) {
+    const int p = e % int(BP), tap = e / int(BP);
+    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
+    const uint32_t m = m0 + uint32_t(p);
+    uint32_t off = BUF_NONE;
+    if (m < live_rows) {
+      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
+      const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
+      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
+      if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
+        const int ho = th / a.sh, wo = tw / a.sw;
+        if (ho < int(a.Ho) && wo < int(a.Wo))
+          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
+      }
+    }
+    sm.rowoff[tap][p] = off;
+  }
+  __syncthreads();
+
+  // This lane: A row = channel c0 + i, B column = pixel m0 + 32 wave + i.
+  const uint32_t px = wave * 32 + uint32_t(i);
+  const uint32_t ch = c0 + i;
+  const uint32_t abase = ch < a.C ? ch * 32 + 16 * g : BUF_NONE;
+  const __amdgpu_buffer_rsrc_t ars = buffer_of(a.wsb, a.wsb_bytes);
+  const __amdgpu_buffer_rsrc_t brs = buffer_of(a.codes, a.codes_bytes);
+  const uint32_t steps = a.taps * a.nch;
+  v16i acc = {0};
+  for (uint32_t s0 = 0; s0 < steps; s0 += NB) {
+    v4i A[NB], B[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const uint32_t st0 = s0 + u;
+      const bool live = st0 < steps;
+      const uint32_t st = live ? st0 : 0;
+      const uint32_t tap = fdiv(st, a.divNch);
+      const uint32_t kc = st - tap * a.nch;
+      A[u] = load16(ars, live ? abase : BUF_NONE, (kc * a.taps + tap) * a.C * 32);
+      B[u] = load16(brs, sm.rowoff[tap][px] + 16 * g, kc * a.R * 32);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < NB; ++u) acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
+  }
+
+  const int off = sm.pix_out[px];
+  if (off < 0) return;                    // rows past the count belong to the zero blocks
+  const float S = sm.pix_s[px], Z = sm.pix_z[px];
+  int c[16], lt[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) { c[v] = 0; lt[v] = 0; }
+  for (int tap = 0; tap < taps; ++tap) {
+    const bool reach = sm.rowoff[tap][px] != BUF_NONE;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {          // rows 8 q + 4 g .. + 3 = acc_row(4 q .. 4 q + 3, g)
+      const int4 w4 = *reinterpret_cast<const int4 *>(&sm.wl[tap][8 * q + 4 * g]);
+      c[4 * q + 0] += reach ? w4.x : 0; c[4 * q + 1] += reach ? w4.y : 0;
+      c[4 * q + 2] += reach ? w4.z : 0; c[4 * q + 3] += reach ? w4.w : 0;
+      if (B8) {
+        lt[4 * q + 0] += w4.x; lt[4 * q + 1] += w4.y; lt[4 * q + 2] += w4.z; lt[4 * q + 3] += w4.w;
+      }
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t cc = c0 + uint32_t(acc_row(v, g));
+    if (cc >= a.C) continue;
+    const int Iv = acc[v] + (B8 ? 128 * lt[v] : 0);
+    const float out = rescale(S, Iv, Z, float(c[v]));
+    const size_t o = size_t(off) + size_t(cc) * a.HW;
+    if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
+    else static_cast<float *>(a.dX)[o] = out;
+    if (a.I_out) a.I_out[o] = Iv;
+  }
+}
+
+template <bool WIDE>
+using DxLdsOf = std::conditional_t<WIDE, DxWideLds, DxLds>;
+
+template <bool B8, int NB, bool WIDE>
 __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
-  __shared__ DxLds sm;
-  dx_body<B8, NB>(a, blockIdx.x, sm);
+  __shared__ DxLdsOf<WIDE> sm;
+  if constexpr (WIDE) dx_body_wide<B8, NB>(a, blockIdx.x, sm);
+  else dx_body<B8, NB>(a, blockIdx.x, sm);
 }
 
 // Both products in one launch (the layer backward): blocks [0, ndw) are dW split-R
-// partial blocks, the rest dX blocks; the two share the LDS allocation.
-template <bool B8, int NB, bool DIRECT>
+// partial blocks (no LDS), the rest dX blocks.
+template <bool B8, int NB, bool DIRECT, bool WIDE>
 __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
-  __shared__ DxLds sm;
-  if (blockIdx.x < ndw) dw_part_body<B8, DIRECT>(dwa, blockIdx.x);
-  else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm);
+  __shared__ DxLdsOf<WIDE> sm;
+  if (blockIdx.x < ndw) {
+    dw_part_body<B8, DIRECT>(dwa, blockIdx.x);
+  } else {
+    if constexpr (WIDE) dx_body_wide<B8, NB>(dxa, blockIdx.x - ndw, sm);
+    else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm);
+  }
 }
 
 }  // namespace
@@ -643,14 +796,18 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
   // DX_ZCHUNK elements each: whatever the device-side count, at least
   // min(2048, N * pieces) blocks are left for the zeroing.
   a.zpieces = uint32_t((int64_t(a.CHW) + DX_ZCHUNK - 1) / DX_ZCHUNK);
-  a.nblocks = uint32_t(((L.N * L.HW + 31) / 32) * a.ctiles +
+  // Four pixel tiles per block once the capacity has 16384 tiles (with few taps).
+  const int64_t tiles = ((L.N * L.HW + 31) / 32) * a.ctiles;
+  a.wide = (a.taps <= uint32_t(DXW_MAX_TAPS) && tiles >= 16384) ? 1u : 0u;
+  const int64_t rows = a.wide ? DXW_TILES * 32 : 32;
+  a.nblocks = uint32_t(((L.N * L.HW + rows - 1) / rows) * a.ctiles +
                        std::min<int64_t>(2048, L.N * int64_t(a.zpieces)));
   return a;
 }
 // Contraction steps of one dX wave, rounded to the instantiated batch depths (10 steps
 // per batch still leaves four resident blocks per CU).
 int dx_batch(const DxArgs &a) {
-  const uint32_t per_wave = (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
+  const uint32_t per_wave = a.wide ? a.taps * a.nch : (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
   return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;
 }
 
@@ -691,13 +848,18 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   const DxArgs a = make_dx_args(L, q, wsb, wlsum, dX, I_out);
   const dim3 grid(a.nblocks);
   const int nb = dx_batch(a);
-  auto go = [&]<bool B8>() {
-    if (nb == 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4>), grid, dim3(DX_THREADS), 0, s, a);
-    else if (nb == 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8>), grid, dim3(DX_THREADS), 0, s, a);
-    else hipLaunchKernelGGL((k_mfma_dx<B8, 10>), grid, dim3(DX_THREADS), 0, s, a);
+  auto go = [&]<bool B8, bool WIDE>() {
+    if (nb == 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (nb == 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
+    else hipLaunchKernelGGL((k_mfma_dx<B8, 10, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
   };
-  if (cfg.bits == 8) go.template operator()<true>();
-  else go.template operator()<false>();
+  if (cfg.bits == 8) {
+    if (a.wide) go.template operator()<true, true>();
+    else go.template operator()<true, false>();
+  } else {
+    if (a.wide) go.template operator()<false, true>();
+    else go.template operator()<false, false>();
+  }
   return last_launch_status();
 }
 
@@ -713,21 +875,28 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   const uint32_t ndw = dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const int nb = dx_batch(dxa);
-  auto go = [&]<bool B8, bool DIRECT>() {
+  auto go = [&]<bool B8, bool DIRECT, bool WIDE>() {
     if (nb == 4)
-      hipLaunchKernelGGL((k_products<B8, 4, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+      hipLaunchKernelGGL((k_products<B8, 4, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+                         dwa, ndw);
     else if (nb == 8)
-      hipLaunchKernelGGL((k_products<B8, 8, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+      hipLaunchKernelGGL((k_products<B8, 8, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+                         dwa, ndw);
     else
-      hipLaunchKernelGGL((k_products<B8, 10, DIRECT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa, ndw);
+      hipLaunchKernelGGL((k_products<B8, 10, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+                         dwa, ndw);
     if (!DIRECT) launch_dw_finish<B8>(L, dwa, s);
   };
+  auto go2 = [&]<bool B8, bool DIRECT>() {
+    if (dxa.wide) go.template operator()<B8, DIRECT, true>();
+    else go.template operator()<B8, DIRECT, false>();
+  };
   if (cfg.bits == 8) {
-    if (dwa.S == 1) go.template operator()<true, true>();
-    else go.template operator()<true, false>();
+    if (dwa.S == 1) go2.template operator()<true, true>();
+    else go2.template operator()<true, false>();
   } else {
-    if (dwa.S == 1) go.template operator()<false, true>();
-    else go.template operator()<false, false>();
+    if (dwa.S == 1) go2.template operator()<false, true>();
+    else go2.template operator()<false, false>();
   }
   return last_launch_status();
 }

@@ -65,6 +65,9 @@ CASES = [
     # the selection; many dW splits with the block-per-row finish.
     ("conv_bigmap_b2", LayerShape("c", "conv2d", 2, 4, 16, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("sample_lognormal", sigma=1.0), "f32"),
+    # 16384 dX tiles of 32 x 32: the dX product in its four-tiles-per-block form.
+    ("conv_wide_dx_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
+     Recipe("channel_lognormal", sigma=1.0), "f32"),
 ]
 
 
