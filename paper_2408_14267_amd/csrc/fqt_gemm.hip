@@ -258,6 +258,112 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   }
 }
 
+// Large dW outputs in one split (DIRECT): each wave holds a 64 x 64 block of the output,
+// 2 x 2 MFMA tiles, so every code chunk it loads feeds two column tiles and every sign
+// piece it expands two row tiles.  A block's four waves take four adjacent 64-column
+// blocks of the same 64 slots (the code rows come from L2 once).  Grid: ceil(D/64) slot
+// blocks x ceil(K/256) column groups, slots slowest.  Double-buffered like the split form.
+constexpr int DWB_PREF = 2;
+struct DwBigBatch {
+  uint64_t word[DWB_PREF][2];
+  v4i A[DWB_PREF][2][2];                  // [word][half][row tile]
+};
+__device__ __forceinline__ void dwb_issue(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
+                                          __amdgpu_buffer_rsrc_t xrs, const uint32_t (&aoff)[2],
+                                          const uint32_t (&boff)[2], uint32_t c0, DwBigBatch &b) {
+  const uint32_t chunk_bytes = a.D * 32;
+#pragma unroll
+  for (int u = 0; u < DWB_PREF; ++u) {
+    const uint32_t c = c0 + u < a.Wr ? c0 + u : c0;
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) b.word[u][ct] = load8(xrs, boff[ct], c * a.K * 8);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) b.A[u][h][rt] = load16(crs, aoff[rt], (2 * c + h) * chunk_bytes);
+  }
+}
+template <bool B8>
+__device__ __forceinline__ void dwb_consume(const DwArgs &a, const DwBigBatch &b, uint32_t c0,
+                                            int g, v16i (&acc)[2][2], uint32_t (&tpart)[2]) {
+#pragma unroll
+  for (int u = 0; u < DWB_PREF; ++u) {
+    if (c0 + u >= a.Wr) break;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const uint32_t bits = uint32_t(b.word[u][ct] >> (32 * h + 16 * g)) & 0xFFFFu;
+        tpart[ct] += __popc(bits);
+        const v4i B = signs16(bits);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+          acc[rt][ct] = mfma_i8(B8 ? bias128(b.A[u][h][rt]) : b.A[u][h][rt], B, acc[rt][ct]);
+      }
+  }
+}
+template <bool B8>
+__device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t wave = wave_id();
+  const int i = lane & 31, g = lane >> 5;
+  const int count = *a.count;
+  const uint32_t kgroups = (a.K + 255) / 256;
+  const uint32_t rb = bid / kgroups;
+  const uint32_t j0 = rb * 64, k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * 64;
+  if (k0 >= a.K) return;
+  v16i acc[2][2];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = v16i{0};
+  uint32_t tpart[2] = {0u, 0u};
+  if (int(j0) < count) {
+    const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
+    const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
+    uint32_t aoff[2], boff[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const uint32_t j = j0 + 32 * rt + i;
+      aoff[rt] = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
+    }
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      const uint32_t kc = k0 + 32 * ct + i;
+      boff[ct] = kc < a.K ? kc * 8 : BUF_NONE;
+    }
+    DwBigBatch b0, b1;
+    uint32_t c0 = 0;
+    dwb_issue(a, crs, xrs, aoff, boff, c0, b0);
+    for (;;) {
+      if (c0 + DWB_PREF < a.Wr) dwb_issue(a, crs, xrs, aoff, boff, c0 + DWB_PREF, b1);
+      __builtin_amdgcn_sched_barrier(0);
+      dwb_consume<B8>(a, b0, c0, g, acc, tpart);
+      c0 += DWB_PREF;
+      if (c0 >= a.Wr) break;
+      if (c0 + DWB_PREF < a.Wr) dwb_issue(a, crs, xrs, aoff, boff, c0 + DWB_PREF, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      dwb_consume<B8>(a, b1, c0, g, acc, tpart);
+      c0 += DWB_PREF;
+      if (c0 >= a.Wr) break;
+    }
+  }
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const uint32_t T = tpart[ct] + lane_xor<32>(tpart[ct]);
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+      dw_write_direct<B8>(a, j0 + 32 * rt, k0 + 32 * ct + i, count, acc[rt][ct], int(T));
+  }
+}
+// Blocks of the 64 x 64-per-wave form.
+uint32_t dw_big_blocks(uint32_t D, uint32_t K) { return ((D + 63) / 64) * ((K + 255) / 256); }
+
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_big(DwArgs a) {
+  dw_big_body<B8>(a, blockIdx.x);
+}
+
 template <bool B8, bool DIRECT>
 __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
   dw_part_body<B8, DIRECT>(a, blockIdx.x);
@@ -811,6 +917,11 @@ int dx_batch(const DxArgs &a) {
   return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;
 }
 
+// One split and at least 1024 waves of 64 x 64: the 2 x 2-tile form.
+bool dw_big(const Layer &L, const DwArgs &a) {
+  return a.S == 1 && ((L.D + 63) / 64) * ((L.K + 63) / 64) >= 1024;
+}
+
 template <bool B8>
 void launch_dw_finish(const Layer &L, const DwArgs &a, hipStream_t s) {
   if (a.S > DWF_WIDE) {
@@ -829,7 +940,10 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   const DwArgs a = make_dw_args(L, cfg, q, xsign, dW, I_out, ws);
   const dim3 grid(dw_part_blocks(L, a));
   auto go = [&]<bool B8>() {
-    if (a.S == 1) {
+    if (dw_big(L, a)) {
+      hipLaunchKernelGGL(k_mfma_dw_big<B8>, dim3(dw_big_blocks(a.D, a.K)), dim3(DW_THREADS), 0,
+                         s, a);
+    } else if (a.S == 1) {
       hipLaunchKernelGGL((k_mfma_dw_part<B8, true>), grid, dim3(DW_THREADS), 0, s, a);
     } else {
       hipLaunchKernelGGL((k_mfma_dw_part<B8, false>), grid, dim3(DW_THREADS), 0, s, a);
@@ -872,7 +986,18 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   DxArgs dxa = make_dx_args(L, q, wsb, wlsum, dX, nullptr);
   dwa.slot_sz = cslot;
   dxa.slot_sz = sslot;
-  const uint32_t ndw = dw_part_blocks(L, dwa);
+  // A large one-split dW runs as its own launch in the 2 x 2-tile form; the products
+  // launch then holds only dX blocks.
+  const bool big = dw_big(L, dwa);
+  if (big) {
+    if (cfg.bits == 8)
+      hipLaunchKernelGGL(k_mfma_dw_big<true>, dim3(dw_big_blocks(dwa.D, dwa.K)), dim3(DW_THREADS),
+                         0, s, dwa);
+    else
+      hipLaunchKernelGGL(k_mfma_dw_big<false>, dim3(dw_big_blocks(dwa.D, dwa.K)),
+                         dim3(DW_THREADS), 0, s, dwa);
+  }
+  const uint32_t ndw = big ? 0u : dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const int nb = dx_batch(dxa);
   auto go = [&]<bool B8, bool DIRECT, bool WIDE>() {

@@ -68,6 +68,11 @@ CASES = [
     # 16384 dX tiles of 32 x 32: the dX product in its four-tiles-per-block form.
     ("conv_wide_dx_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # Large one-split dW outputs: the 2 x 2-tile dW form (ragged sizes, b = 8 bias).
+    ("linear_bigdw_b2", LayerShape("fc", "linear", 64, 2048, 2048), 2, 0,
+     Recipe("channel_lognormal", sigma=1.5), "f32"),
+    ("linear_bigdw_ragged_b8", LayerShape("fc", "linear", 100, 2100, 2050), 8, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
 ]
 
 
