@@ -67,6 +67,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="bound on the CPU oracle sample (seconds of work)")
     p.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep"),
+                   help="instead of the benchmark line: per-layer times of a whole network's "
+                        "layer backwards, or the dW binary GEMM sweep (one JSON line each)")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="first run a plain device copy of this many MiB (three times), so that "
                         "a counter run can scale FETCH_SIZE / WRITE_SIZE by a known byte count")
@@ -94,8 +97,120 @@ def cpu_baseline(x, w, dy, layer, wl, ops_per_step, budget_s):
                       f"({el / reps * 1e3:.0f} ms each; numpy, BLAS threads={threads})"}
 
 
+def _gen(torch, shape, dtype, dev, scale=None):
+    x = torch.randn(shape, device=dev, dtype=torch.float32)
+    if scale is not None:
+        x *= scale
+    return x.to(dtype)
+
+
+def suite(name, reps=10):
+    """Per-layer eager times of the layer backward over a whole network (inputs drawn on the
+    GPU with the workload's recipe distributions), or the dW binary GEMM sweep."""
+    import torch
+
+    from paper_2408_14267_amd import fqt
+    from paper_2408_14267_amd.workloads import WORKLOADS, LayerShape
+    dev = torch.device("cuda:0")
+    st = torch.cuda.current_stream()
+    torch.manual_seed(0)
+
+    def timed(fn, k):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(st)
+        for _ in range(k):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / k
+
+    if name == "gemm_sweep":
+        from paper_2408_14267_amd.workloads import gemm_sweep_points
+        for M, _, K in gemm_sweep_points():
+            # dW of a linear layer with batch K, in = out = M: an M x M x K binary GEMM of
+            # 1-bit codes (b = 1, no pruning) against packed signs.
+            L = LayerShape(name="gemm", kind="linear", N=K, C=M, D=M)
+            desc = fqt.layer_desc(L)
+            cfg = fqt.quant_cfg(1, fqt.FQT_AGP_OFF, 0, 0, 0)
+            dY = _gen(torch, (K, M), torch.float32, dev)
+            X = _gen(torch, (K, M), torch.float32, dev)
+            q = fqt.QGrad(desc, cfg, device=dev)
+            qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
+            dws = fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW, device=dev)
+            xs = torch.empty(((K + 63) // 64) * M, dtype=torch.int64, device=dev)
+            dW = torch.empty((M, M), dtype=torch.float32, device=dev)
+            qz = lambda: fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st)
+            px = lambda: fqt.fqt_pack_input_signs(desc, X, xs, st)
+            gd = lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, dws, None, st)
+            for f in (qz, px, gd):
+                f()
+            k = 3 if M * M * K > 2 ** 36 else reps
+            tq, tp, tg = timed(qz, k), timed(px, k), timed(gd, k)
+            ops = 2.0 * M * M * K
+            # quantize: dY read twice (statistics, codes) + 1-byte codes and b-bit planes of
+            # both encodings written
+            qbytes = K * M * 4 * 2 + 2 * K * M + 2 * K * M / 8
+            print(json.dumps({"suite": name, "gemm_MxNxK": [M, M, K],
+                              "gemm_dw_ms": round(tg, 4), "int8_TOPS": round(ops / tg / 1e9, 1),
+                              "mfma_frac": round(ops / tg / 1e9 / MFMA_I8_PEAK_TOPS, 4),
+                              "quantize_ms": round(tq, 4),
+                              "quantize_GBps": round(qbytes / tq / 1e6, 1),
+                              "pack_x_ms": round(tp, 4)}), flush=True)
+            del dY, X, q, qws, dws, xs, dW
+            torch.cuda.empty_cache()
+        return
+
+    wl = WORKLOADS[name]
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    tot_ms, tot_ops = 0.0, 0.0
+    for li, L in enumerate(wl.layers):
+        X = _gen(torch, L.x_shape, tdt, dev)
+        W = _gen(torch, L.w_shape, torch.float32, dev)
+        nd = len(L.dy_shape)
+        r = wl.recipe
+        if r.kind == "sample_lognormal":
+            sc = torch.exp(r.sigma * torch.randn((L.N,) + (1,) * (nd - 1), device=dev))
+            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
+        elif r.kind == "channel_lognormal":
+            sc = torch.exp(r.sigma * torch.randn((1, L.D) + (1,) * (nd - 2), device=dev))
+            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
+        else:
+            dY = torch.distributions.StudentT(r.df).sample(L.dy_shape).to(dev).to(tdt)
+        dX, dW = torch.empty_like(X), torch.empty_like(W)
+        if tdt == torch.bfloat16:
+            desc = fqt.layer_desc(L, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+        else:
+            desc = fqt.layer_desc(L)
+        cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, wl.philox_seed, 0, li)
+        ws = fqt.workspace(desc, cfg, device=dev)
+        step = lambda: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st)
+        for _ in range(3):
+            step()
+        ms = timed(step, reps)
+        ops = 4.0 * L.binary_macs()
+        es = 2 if tdt == torch.bfloat16 else 4
+        # each tensor crossing HBM once: dY, X, W read; dX, dW written
+        mbytes = (L.N * L.D * L.Ho * L.Wo + 2 * L.N * L.C * L.H * L.W) * es + 2 * L.D * L.C * L.kh * L.kw * 4
+        tot_ms += ms
+        tot_ops += ops
+        print(json.dumps({"suite": name, "layer": li, "name": L.name, "ms": round(ms, 4),
+                          "binary_TOPS": round(ops / ms / 1e9, 1),
+                          "min_bytes_MB": round(mbytes / 1e6, 2),
+                          "GBps_of_min_bytes": round(mbytes / ms / 1e6, 1)}), flush=True)
+        del X, W, dY, dX, dW, ws
+        torch.cuda.empty_cache()
+    print(json.dumps({"suite": name, "total_ms": round(tot_ms, 3),
+                      "binary_TOPS": round(tot_ops / tot_ms / 1e9, 1)}), flush=True)
+
+
 def main():
     args = parse()
+    if args.suite:
+        if args.gpus != 1:
+            sys.exit("the suites run on one GPU")
+        suite(args.suite)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the layer backward "
                                    "shards by data parallelism with one dW all-reduce, which "
