@@ -821,10 +821,12 @@ __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa,
 }  // namespace
 
 // Splits of the dW contraction over N*Ho*Wo: enough 32x32 wave tiles of the expected
-// kept channels (all of them without AGP, about D / b with it) to give about 1024 waves,
-// and at most 256 words (16384 positions) per split, within at most DW_MAX_SPLITS splits,
-// 128 MB of partials and one batch of words per split.
+// kept channels (all of them without AGP, about D / b with it) to give about 1024 waves
+// while every split keeps at least 16 words (1024 positions), and at most 256 words per
+// split, within at most DW_MAX_SPLITS splits, 128 MB of partials and one batch of words
+// per split.
 constexpr int64_t DW_TARGET_WAVES = 1024;
+constexpr int64_t DW_MIN_WORDS = 16;
 constexpr int64_t DW_MAX_WORDS = 256;
 constexpr int64_t DW_MAX_SPLITS = 4096;
 constexpr int64_t DW_MAX_PART_BYTES = int64_t(128) << 20;
@@ -832,7 +834,8 @@ int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   const int64_t dkeep =
       cfg.agp_mode == FQT_AGP_OFF ? L.D : std::max<int64_t>(1, (L.D + cfg.bits - 1) / cfg.bits);
   const int64_t tiles = ((dkeep + 31) / 32) * ((L.K + 31) / 32);
-  int64_t S = std::max((DW_TARGET_WAVES + tiles - 1) / tiles,
+  int64_t S = std::max(std::min((DW_TARGET_WAVES + tiles - 1) / tiles,
+                                (L.Wr + DW_MIN_WORDS - 1) / DW_MIN_WORDS),
                        (L.Wr + DW_MAX_WORDS - 1) / DW_MAX_WORDS);
   const int64_t kp = ((L.K + 31) / 32) * 32;
   S = std::min(S, std::max<int64_t>(1, DW_MAX_PART_BYTES / (L.D * kp * 4)));
