@@ -28,33 +28,37 @@ MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
 
 # HBM traffic per launch from rocprofv3 counter runs of this benchmark (FETCH_SIZE and
 # WRITE_SIZE in KiB per dispatch, one run each), scaled by what the same counters read for
-# a 256 MiB device copy in those runs (FETCH_SIZE reads half the copied bytes).  A figure is
-# reported only while its kernel source is byte-identical to the one it was measured on.
+# a 256 MiB device copy in those runs (FETCH_SIZE reads half the copied bytes).  The figures
+# are reported only while the kernel sources are byte-identical to the ones they were
+# measured on (TRAFFIC_DIGEST: sha256 over the names and contents of every file in csrc/).
 FETCH_SCALE = 262144.0 / 131086.7
 WRITE_SCALE = 1.0
+TRAFFIC_DIGEST = "8f166083959e0b979a50b56d737375ed66a2fa5741ac86f03464befd1c6b2295"
 TRAFFIC = {
-    # entry: (kernel source, its sha256, FETCH_SIZE KiB, WRITE_SIZE KiB per launch)
-    "gemm_dx": ("paper_2408_14267_amd/csrc/fqt_gemm.hip",
-                "8c39232ab5faf825ca4386edcc1cd24ae45e5b4fec60e0c560e09a7d7c1caa0e", 2543.0, 8192.0),
-    "gemm_dw": ("paper_2408_14267_amd/csrc/fqt_gemm.hip",
-                "8c39232ab5faf825ca4386edcc1cd24ae45e5b4fec60e0c560e09a7d7c1caa0e",
-                1532.0 + 2907.2, 5256.0 + 2304.0),
-    "pack_x": ("paper_2408_14267_amd/csrc/fqt_pack.hip",
-               "1e27c043efa0ddb4ea8f17788d588b6ac0ad5bf32f54da8428c0fa5f22b08b36", 4130.4, 2304.0),
-    "pack_w": ("paper_2408_14267_amd/csrc/fqt_pack.hip",
-               "1e27c043efa0ddb4ea8f17788d588b6ac0ad5bf32f54da8428c0fa5f22b08b36", 1177.5, 585.0),
+    # entry: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch of its kernels
+    "gemm_dx": (2537.5, 8192.0),
+    "pack_x": (4130.1, 2304.0),
+    "pack_w": (1179.5, 585.0),
 }
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel`, or None when not measured on its current source."""
+def sources_digest():
     import hashlib
-    if kernel not in TRAFFIC:
+    d = os.path.join(ROOT, "paper_2408_14267_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".hpp", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel`, or None when not measured on the current sources."""
+    if kernel not in TRAFFIC or sources_digest() != TRAFFIC_DIGEST:
         return None
-    src, sha, fetch_kib, write_kib = TRAFFIC[kernel]
-    with open(os.path.join(ROOT, src), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != sha:
-            return None
+    fetch_kib, write_kib = TRAFFIC[kernel]
     return (fetch_kib * FETCH_SCALE + write_kib * WRITE_SCALE) * 1024.0
 
 
