@@ -137,8 +137,14 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
 /* Workspace sizes (host call).  which = FQT_WS_QUANTIZE for fqt_agp_scq_quantize,
  * FQT_WS_GEMM_DW for fqt_binary_gemm_dw (its split partial sums), FQT_WS_LAYER for
  * fqt_layer_backward (which holds an fqt_qgrad, the packed signs and the partial sums
- * inside it).  The library carves the workspace; its contents need no initialisation
- * and are garbage after the call. */
+ * inside it).  The library carves the workspace.  A FQT_WS_QUANTIZE or FQT_WS_LAYER
+ * workspace keeps state between calls in its first 128 KiB (FQT_WS_STATE_BYTES): the group
+ * keys that the statistics combine with atomics.  Zero-fill those bytes once before the
+ * first call that uses the workspace; every call leaves them zero again (and the rest of
+ * the workspace garbage).  Such a workspace may serve layers of any shape, one call at a
+ * time, but nothing else may write its first 128 KiB (do not share it with a
+ * FQT_WS_GEMM_DW workspace).  A FQT_WS_GEMM_DW workspace needs no initialisation. */
+#define FQT_WS_STATE_BYTES 131072
 #define FQT_WS_QUANTIZE 0
 #define FQT_WS_LAYER 1
 #define FQT_WS_GEMM_DW 2

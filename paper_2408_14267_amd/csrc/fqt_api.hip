@@ -32,6 +32,8 @@ struct LayerWs {
 };
 
 void carve_quant_ws(Carver *c, const Layer &L, QuantWs *q) {
+  static_assert(MKEY_SLOTS * sizeof(uint2) == FQT_WS_STATE_BYTES, "state bytes");
+  q->mkeys = c->take<uint2>(MKEY_SLOTS);            // first: a fixed place in every layout
   q->part_c = c->take<int2>(size_t(L.D) * stats_row_blocks(L));
   q->part_s = c->take<int2>(size_t(L.Wd) * L.Wr * stats_slots(L));
   q->skey = c->take<int2>(L.N);

@@ -37,7 +37,18 @@ struct GroupParam {
 
 // Quantize workspace: per-tile partial min/max keys, the reduced keys of both group
 // sets, and the per-group parameters of the quantizer.
+// Merged group keys: (min, max) keys of every sample and channel combined by atomics while
+// the statistics run (both stored so that 0 is the identity of an unsigned max), at the
+// start of the quantizer's workspace.  MKEY_REP replicas of each key, written by different
+// workgroups, cut the number of atomics that meet at one address.  They are zero between
+// calls: the workspace is zero-filled once before its first use and each selection clears
+// the entries it reads.
+constexpr int MKEY_GROUPS = 2 * 1024;
+constexpr int MKEY_REP = 8;
+constexpr int MKEY_SLOTS = MKEY_GROUPS * MKEY_REP;
 struct QuantWs {
+  uint2 *mkeys;            // [MKEY_REP][MKEY_GROUPS]: samples at [0, N), channels at
+                           //   [N, N + D) of each replica
   int2 *part_c;            // [stats_row_blocks][D]  channel partials of each row block
   int2 *part_s;            // [ceil(D/64)][ceil(R/64)][stats_slots]  sample partials of
                            //   each 64 x 64 tile, one slot per sample the tile meets

@@ -92,14 +92,32 @@ __device__ __forceinline__ void stats_load(const void *dy, const TileGeom &g, ui
   }
 }
 
+// Merged key encoding: max key as its unsigned order (k ^ 2^31), min key as the complement
+// of that, so that both combine with an unsigned atomic max and 0 is the identity of both.
+__device__ __forceinline__ void merge_key(uint2 *mk, int lo, int hi) {
+  uint32_t *p = reinterpret_cast<uint32_t *>(mk);
+  __hip_atomic_fetch_max(p, ~(uint32_t(lo) ^ 0x80000000u), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_fetch_max(p + 1, uint32_t(hi) ^ 0x80000000u, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int2 merged_key(uint2 u) {
+  return make_int2(int(~u.x ^ 0x80000000u), int(u.y ^ 0x80000000u));
+}
+
 // One block per (rs row tiles, 64 channels).  Each 64 x 64 tile goes through LDS as
 // order-preserving integer keys; channel rows are reduced over the rows (kept across the
 // block's row tiles), row columns over the channels and then over the rows of each sample
 // in the tile.
+// With mks / mkc set (merged keys), the sample and channel keys are combined into them
+// with atomics instead of being stored as partials: channel keys into replica
+// blockIdx.x % MKEY_REP, sample keys into replica blockIdx.y % MKEY_REP.
 template <int MODE, int DT>
 __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, StatsGeom sg,
                                                    int2 *__restrict__ part_c,
-                                                   int2 *__restrict__ part_s) {
+                                                   int2 *__restrict__ part_s,
+                                                   uint2 *__restrict__ mks,
+                                                   uint2 *__restrict__ mkc) {
   __shared__ int32_t key[TILE][TILE + 1];
   __shared__ int32_t pmin[WAVES][TILE], pmax[WAVES][TILE];
   __shared__ int2 cpart[TILE];
@@ -176,12 +194,22 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
       const uint32_t slot = row_ok ? fdiv(r0 + lane, g.divP) - n_first : 0xFFFFFFFFu;
       int2 *ps = part_s + (size_t(blockIdx.y) * sg.nrt + rt) * sg.SL;
       if (g.P == 1) {
-        ps[lane] = row_ok ? make_int2(lo, hi) : make_int2(INT_MAX, INT_MIN);
+        if (mks) {
+          if (row_ok) merge_key(mks + (blockIdx.y % MKEY_REP) * MKEY_GROUPS + r0 + lane, lo, hi);
+        } else {
+          ps[lane] = row_ok ? make_int2(lo, hi) : make_int2(INT_MAX, INT_MIN);
+        }
       } else {
         for (uint32_t k = 0; k < sg.SL; ++k) {
           const int l = wave_min(slot == k ? lo : INT_MAX);
           const int h = wave_max(slot == k ? hi : INT_MIN);
-          if (lane == 0) ps[k] = make_int2(l, h);
+          if (mks) {
+            // A slot holds data only for a sample that the tile meets (then n < N).
+            if (lane == 0 && l <= h)
+              merge_key(mks + (blockIdx.y % MKEY_REP) * MKEY_GROUPS + n_first + k, l, h);
+          } else if (lane == 0) {
+            ps[k] = make_int2(l, h);
+          }
         }
       }
     }
@@ -194,7 +222,12 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
     for (int i = 0; i < TILE / WAVES; ++i) cpart[wave + WAVES * i] = make_int2(clo[i], chi[i]);
   }
   __syncthreads();
-  if (wave == 1 && d0 + lane < g.D) part_c[size_t(blockIdx.x) * g.D + d0 + lane] = cpart[lane];
+  if (wave == 1 && d0 + lane < g.D) {
+    if (mkc)
+      merge_key(mkc + (blockIdx.x % MKEY_REP) * MKEY_GROUPS + d0 + lane, cpart[lane].x,
+                cpart[lane].y);
+    else part_c[size_t(blockIdx.x) * g.D + d0 + lane] = cpart[lane];
+  }
 }
 
 // Large maps (Ho*Wo >= 1024): the (min, max) key of every (sample, channel) plane of dY,
@@ -313,7 +346,8 @@ struct SetArgs {
                        // 1: sample slots of part_s (P, nrt, SL, ndt)
                        // 2: key[g] already holds the group's key (k_stats_reduce ran)
                        // 3: group g reduces part[g * ld + u], u < U (per-plane partials)
-                       // 1: sample slots of part_s (P, nrt, SL, ndt)
+                       // 4: key[r * MKEY_GROUPS + g], r < MKEY_REP, are the group's merged
+                       //    key replicas (cleared once read)
   uint32_t U, ld;
   uint32_t P, nrt, SL, ndt;
   FastDiv divP;
@@ -637,6 +671,24 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
         const int2 k = S.key[g];
         lo = k.x;
         hi = k.y;
+      }
+    } else if (S.slots == 4) {          // merged keys, left zero for the next call
+      if (g < G) {
+        uint2 *mk = reinterpret_cast<uint2 *>(const_cast<int2 *>(S.key));
+        uint2 u[(MKEY_REP + SPLIT - 1) / SPLIT];
+#pragma unroll
+        for (int i = 0; i < (MKEY_REP + SPLIT - 1) / SPLIT; ++i) {
+          const int r = r0 + i * SPLIT;
+          u[i] = r < MKEY_REP ? mk[r * MKEY_GROUPS + g] : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int i = 0; i < (MKEY_REP + SPLIT - 1) / SPLIT; ++i) {
+          const int r = r0 + i * SPLIT;
+          const int2 k = merged_key(u[i]);
+          lo = min(lo, k.x);
+          hi = max(hi, k.y);
+          if (r < MKEY_REP) mk[r * MKEY_GROUPS + g] = make_uint2(0u, 0u);
+        }
       }
     } else if (g < G && !S.slots) {     // channels: row-block partials, adjacent per row
       // One per-lane offset (the group) and a wave-uniform one per row block (r0 is
@@ -1093,6 +1145,15 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   // Large maps with both group sets in one-workgroup selections: per-plane statistics
   // (part_c holds the N * D plane keys: it has D * stats_row_blocks >= D * N entries).
   const bool planes = L.P >= 1024 && L.P % 4 == 0 && gmax <= 1024;
+  // The one-workgroup selection reduces the partials itself; with many partials per group
+  // (large N*Ho*Wo) a workgroup per group reduces them first.  With few partials per group
+  // the statistics merge the keys with atomics instead (the selection then reads one key
+  // per group).
+  const bool many_partials =
+      !planes && (nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256);
+  const bool merged = !planes && !many_partials && gmax <= 1024;
+  uint2 *mks = merged ? w.mkeys : nullptr;
+  uint2 *mkc = merged ? w.mkeys + L.N : nullptr;
   if (planes) {
     const uint32_t np = uint32_t(L.N * L.D);
     const uint32_t blocks = std::min<uint32_t>((np + 3) / 4, 4096);
@@ -1103,13 +1164,13 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   } else dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
       hipLaunchKernelGGL((k_stats<TILE_PIX, DT>), grid, dim3(THREADS), 0, s, dY, sg, w.part_c,
-                         w.part_s);
+                         w.part_s, mks, mkc);
     else if (mode == TILE_CHAN)
       hipLaunchKernelGGL((k_stats<TILE_CHAN, DT>), grid, dim3(THREADS), 0, s, dY, sg, w.part_c,
-                         w.part_s);
+                         w.part_s, mks, mkc);
     else
       hipLaunchKernelGGL((k_stats<TILE_SCALAR, DT>), grid, dim3(THREADS), 0, s, dY, sg,
-                         w.part_c, w.part_s);
+                         w.part_c, w.part_s, mks, mkc);
   });
   if (last_launch_status() != FQT_OK) return FQT_E_HIP;
 
@@ -1127,10 +1188,10 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     sa.set[0].ld = uint32_t(L.D);
     sa.set[1].slots = 0; sa.set[1].U = uint32_t(L.N); sa.set[1].ld = uint32_t(L.D);
   }
-  // The one-workgroup selection reduces the partials itself; with many partials per group
-  // (large N*Ho*Wo) a workgroup per group reduces them first.
-  const bool many_partials =
-      !planes && (nrb > 256 || int64_t(ndt) * ((L.P + TILE - 1) / TILE + 1) > 256);
+  if (merged) {
+    sa.set[0].slots = 4; sa.set[0].key = reinterpret_cast<const int2 *>(mks);
+    sa.set[1].slots = 4; sa.set[1].key = reinterpret_cast<const int2 *>(mkc);
+  }
   int st;
   if (gmax <= 1024 && many_partials) {
     hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,

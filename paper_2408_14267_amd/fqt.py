@@ -22,6 +22,7 @@ FQT_LINEAR, FQT_CONV2D = 0, 1
 FQT_AGP_BERNOULLI, FQT_AGP_TOPK, FQT_AGP_OFF = 0, 1, 2
 FQT_PACK_ALONG_ROWS, FQT_PACK_ALONG_COLS, FQT_PACK_IM2COL = 0, 1, 2
 FQT_WS_QUANTIZE, FQT_WS_LAYER, FQT_WS_GEMM_DW = 0, 1, 2
+FQT_WS_STATE_BYTES = 131072    # zeroed state at the start of quantize and layer workspaces
 FQT_MAX_BITS = 8
 FQT_MAX_AGP_GROUPS = 16384
 EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_agp_scq_quantize",
@@ -213,6 +214,7 @@ class QGrad:
 
 
 def workspace(desc, cfg, which=FQT_WS_LAYER, device="cuda"):
-    """A 256-byte aligned uint8 workspace tensor of the size the library asks for."""
+    """A 256-byte aligned uint8 workspace tensor of the size the library asks for, zero-filled
+    (quantize and layer workspaces keep zeroed state between calls in their first bytes)."""
     n = fqt_workspace_size(desc, cfg, which)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)

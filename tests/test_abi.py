@@ -112,3 +112,12 @@ def test_null_and_small_workspace_rejected_before_launch():
     st = lib.fqt_pack_weight_signs(ctypes.byref(d), fake, ctypes.c_void_p((1 << 20) + 8), fake,
                                    None)
     assert st == fqt.FQT_E_ALIGN            # the sign bytes must be 16-byte aligned
+
+
+def test_state_bytes_constant_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define FQT_WS_STATE_BYTES (\d+)", text)
+    assert m and int(m.group(1)) == fqt.FQT_WS_STATE_BYTES
+    d = _desc()
+    c = fqt.quant_cfg(4)
+    assert fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE) > fqt.FQT_WS_STATE_BYTES

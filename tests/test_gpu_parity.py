@@ -327,3 +327,37 @@ def test_seed_step_layer_change_the_draws():
         _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
         outs.append(dX.cpu())
     assert all(not torch.equal(outs[0], o) for o in outs[1:])
+
+
+def test_workspace_shared_across_layers():
+    """One zero-filled workspace, sized for the largest of several layers, serves them in
+    turn (twice over): every call matches the oracle and leaves the workspace's state bytes
+    (the merged group keys) zero."""
+    fqt = _fqt()
+    layers = [
+        (LayerShape("c", "conv2d", 5, 7, 70, 9, 9, 3, 3, 1, 1, 1, 1), 3,
+         Recipe("sample_lognormal", sigma=1.5)),
+        (LayerShape("fc", "linear", 37, 300, 77), 8, Recipe("sample_lognormal", sigma=2.0)),
+        # 32 x 32 maps: per-plane statistics, no merged keys
+        (LayerShape("c", "conv2d", 2, 4, 8, 32, 32, 3, 3, 1, 1, 1, 1), 2,
+         Recipe("channel_lognormal", sigma=1.0)),
+        (LayerShape("c", "conv2d", 3, 33, 40, 8, 8, 3, 3, 1, 1, 1, 1), 2,
+         Recipe("channel_lognormal", sigma=1.0)),
+    ]
+    runs = []
+    size = 0
+    for i, (layer, bits, recipe) in enumerate(layers):
+        fqt_, ref, desc, cfg, X, W, dY = _run_case(layer, bits, 0, recipe, "f32", data_seed=i)
+        runs.append((layer, ref, desc, cfg, X, W, dY))
+        size = max(size, fqt.fqt_workspace_size(desc, cfg, fqt.FQT_WS_LAYER))
+    ws = torch.zeros(size, dtype=torch.uint8, device="cuda")
+    state = fqt.FQT_WS_STATE_BYTES
+    for rnd in range(2):
+        for layer, ref, desc, cfg, X, W, dY in runs:
+            _announce(f"[gpu parity] shared workspace round {rnd}: {layer}")
+            dX, dW = torch.full_like(X, 7.0), torch.full_like(W, 7.0)
+            fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws)
+            torch.cuda.synchronize()
+            _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
+            _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
+            assert torch.count_nonzero(ws[:state]).item() == 0, "state bytes left non-zero"
