@@ -157,6 +157,18 @@ __global__ __launch_bounds__(THREADS) void k_pack_im2col_band(const void *__rest
   band_im2col_body<DT, KH, KW, THREADS>(x, g, dst, blockIdx.x, blockIdx.y, band);
 }
 
+// Bit-level im2col of a stride-1 same-padded convolution (the body is shared with the
+// layer backward's selection launch): 1024 threads per block, so that a block stages
+// several channels and the grid still spreads the loads of X over every CU.
+constexpr int BITS_THREADS = 1024;
+template <int DT>
+__global__ __launch_bounds__(BITS_THREADS) void k_pack_im2col_bits(const void *__restrict__ x,
+                                                                   BitGeom g,
+                                                                   uint64_t *__restrict__ dst) {
+  extern __shared__ uint64_t bsm[];
+  bit_im2col_body<DT, BITS_THREADS>(x, g, dst, blockIdx.x, bsm);
+}
+
 // linesum[l] = sum of the +-1 signs of line l = 2 * popcount - len.
 __global__ __launch_bounds__(THREADS) void k_linesum(const uint64_t *__restrict__ words,
                                                      int64_t lines, int64_t nw, int64_t len,
@@ -228,8 +240,16 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     nw = L.Wr;
     lines = L.K;
     len = L.R;
+    BitGeom bt;
     BandGeom bg;
     size_t lds = 0;
+    if (word_major && bit_geom(L, BITS_THREADS, 512, 48 * 1024, &bt, &lds)) {
+      dispatch_dtype(dtype, [&]<int DT>() {
+        hipLaunchKernelGGL(k_pack_im2col_bits<DT>, dim3(bit_blocks(bt)), dim3(BITS_THREADS), lds,
+                           s, src, bt, dst);
+      });
+      return last_launch_status();
+    }
     if (word_major && band_geom(L, src, dtype, THREADS, 48 * 1024, &bg, &lds)) {
       const dim3 bgrid(band_word_blocks(L, bg),
                        unsigned((L.C + BAND_CPW * WAVES - 1) / (BAND_CPW * WAVES)));

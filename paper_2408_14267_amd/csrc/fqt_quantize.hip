@@ -895,10 +895,12 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
 
 // The same two selection workgroups, then spare workgroups that pack the products' sign
 // operands (they do not depend on dY): blocks [2, 2 + npw) the weight bytes, the rest the
-// band im2col of X (word group fastest, then 64-channel groups).
+// im2col of X: bit-level (KH < 0; block order of bit_im2col_body) or through the band
+// (word group fastest, then 64-channel groups).
 struct SignArgs {
   const void *x;
   BandGeom bg;
+  BitGeom bt;
   uint64_t *xsign;
   uint32_t nwb;          // word-group blocks of the band (samples x word groups)
   FastDiv divNwb;
@@ -908,16 +910,20 @@ struct SignArgs {
   int32_t *wlsum;
   uint32_t npw;
 };
-template <int GP, int DT, int KH, int KW>
-__global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) void k_select_signs(SelectArgs a,
-                                                                                 SignArgs sg) {
+// DT: dtype of X; WDT: dtype of W.
+template <int GP, int DT, int KH, int KW, int WDT = DT>
+__global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) void k_select_signs(
+    SelectArgs a, SignArgs sg) {
   extern __shared__ uint32_t band[];
   __shared__ PackWLds pws;
   const uint32_t b = blockIdx.x;
   if (b < 2) {
     select_fused_body<GP>(a, int(b));
   } else if (b - 2 < sg.npw) {
-    pack_w_body<DT>(sg.w, sg.pg, sg.wsb, sg.wlsum, b - 2, pws);
+    pack_w_body<WDT>(sg.w, sg.pg, sg.wsb, sg.wlsum, b - 2, pws);
+  } else if constexpr (KH < 0) {
+    bit_im2col_body<DT, SEL_NT>(sg.x, sg.bt, sg.xsign, b - 2 - sg.npw,
+                                reinterpret_cast<uint64_t *>(band));
   } else {
     const uint32_t f = b - 2 - sg.npw;
     const uint32_t cb = fdiv(f, sg.divNwb);
@@ -1201,30 +1207,53 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     sa.set[1].slots = 2;
   }
   // Sign operands in the selection launch: a convolution whose X and W share a dtype and
-  // whose band fits the LDS left beside the selection (64 KB per workgroup in all).
+  // whose im2col staging fits the LDS left beside the selection (64 KB per workgroup in
+  // all): bit-level for stride-1 same-padded convolutions (at most about 448 im2col
+  // workgroups: with two 1024-thread workgroups per CU the launch fits the chip in one
+  // round), else through the band.
+  BitGeom bt;
   BandGeom bg;
-  size_t band_lds = 0;
+  size_t sign_lds = 0;
   const int gp = gmax <= 256 ? 256 : 1024;
-  const bool with_signs =
-      signs && gmax <= 1024 && L.x_t == L.w_t &&
-      band_geom(L, signs->X, L.x_t, SEL_NT, 65536 - 512 - select_signs_static_lds(gp), &bg,
-                &band_lds);
-  if (with_signs) {
+  const size_t lds_left = 65536 - 512 - select_signs_static_lds(gp);
+  const bool sign_ok = signs && gmax <= 1024;
+  const bool with_bits = sign_ok && bit_geom(L, SEL_NT, 448, lds_left, &bt, &sign_lds);
+  const bool with_band = sign_ok && !with_bits && L.x_t == L.w_t &&
+                         band_geom(L, signs->X, L.x_t, SEL_NT, lds_left, &bg, &sign_lds);
+  if (with_bits || with_band) {
     SignArgs sg;
-    sg.x = signs->X; sg.bg = bg; sg.xsign = signs->xsign;
-    sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);
+    sg.x = signs->X; sg.xsign = signs->xsign;
     sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
     sg.npw = pack_w_blocks(L);
-    const uint32_t cgroups = uint32_t((L.C + BAND_CPW * SEL_NW - 1) / (BAND_CPW * SEL_NW));
-    const dim3 grid(2 + sg.npw + sg.nwb * cgroups);
+    uint32_t xblocks;
+    if (with_bits) {
+      sg.bt = bt;
+      xblocks = bit_blocks(bt);
+    } else {
+      sg.bg = bg;
+      sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);
+      xblocks = sg.nwb * uint32_t((L.C + BAND_CPW * SEL_NW - 1) / (BAND_CPW * SEL_NW));
+    }
+    const dim3 grid(2 + sg.npw + xblocks);
     dispatch_dtype(L.x_t, [&]<int DT>() {
       auto go = [&]<int GPT>() {
-        if (L.kh == 3 && L.kw == 3)
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 3, 3>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+        if (with_bits && L.w_t != DT)
+          dispatch_dtype(L.w_t, [&]<int WDT>() {
+            hipLaunchKernelGGL((k_select_signs<GPT, DT, -1, -1, WDT>), grid, dim3(SEL_NT),
+                               sign_lds, s, sa, sg);
+          });
+        else if (with_bits)
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, -1, -1>), grid, dim3(SEL_NT), sign_lds, s,
+                             sa, sg);
+        else if (L.kh == 3 && L.kw == 3)
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 3, 3>), grid, dim3(SEL_NT), sign_lds, s,
+                             sa, sg);
         else if (L.kh == 1 && L.kw == 1)
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 1, 1>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 1, 1>), grid, dim3(SEL_NT), sign_lds, s,
+                             sa, sg);
         else
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 0, 0>), grid, dim3(SEL_NT), band_lds, s, sa, sg);
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, 0, 0>), grid, dim3(SEL_NT), sign_lds, s,
+                             sa, sg);
       };
       if (gp == 256) go.template operator()<256>();
       else go.template operator()<1024>();

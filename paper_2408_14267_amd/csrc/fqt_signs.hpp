@@ -170,6 +170,177 @@ __device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, con
   }
 }
 
+// ----------------------------------------------------------------------------- bit im2col
+// Bit-level im2col for stride-1 convolutions with "same" padding (2 ph = kh - 1,
+// 2 pw = kw - 1, so Ho = H and Wo = W and an output position and the input position a tap
+// reads differ by a constant offset in the row-major order of N*H*W).  Let s_c be the
+// string of sign bits of channel c over all N*H*W positions (bit r = X[n][c][h][w] > 0 at
+// r = (n H + h) W + w).  Output word w of line (c, tap) (positions 64 w .. 64 w + 63) is
+// then the 64 bits of s_c from bit 64 w + off(tap), off = (i - ph) W + (j - pw), with the
+// positions whose tap falls outside the image (row ho + i - ph or column wo + j - pw out
+// of range) cleared by a row mask and a column mask of the word.  A block builds s_c for
+// its CB channels over its WB words plus the halo words the offsets reach, one ballot per
+// word, in LDS; every output word is then one funnel shift and two masks, 64 lines per
+// wave instruction.  Compared with a ballot per output word this takes the VALU work of
+// the packing from once per (position, tap) to once per position.
+struct BitGeom {
+  uint32_t N, C, H, W, P, R, Wr, K, taps;
+  int kh, kw, ph, pw;
+  uint32_t CB, WB;            // channels and output words per block
+  uint32_t dlo, span;         // halo words below the block's first word; words staged
+  uint32_t cgroups, wgroups;
+  FastDiv divP, divW, divSpan, divTaps, divKw, divWB, divWg;
+};
+
+constexpr int BIT_U = 8;        // sign words a wave loads back to back
+
+// Geometry for blocks of `nt` threads: the staged words per channel (span) a multiple of
+// BIT_U with at most a sixteenth of them halo, WB = span - halo output words per block;
+// CB channels, a power of two, at least enough for one batch of BIT_U words per wave and
+// then doubled up to 64 while the grid has more than about `target_blocks` blocks (many
+// small blocks spread the loads of X over every CU), and halved while the staging
+// exceeds `lds_max` bytes.  False when the layer is not a stride-1 same-padded
+// convolution or one channel's staging does not fit.
+inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_max,
+                     BitGeom *g, size_t *lds) {
+  if (L.kind != FQT_CONV2D || L.sh != 1 || L.sw != 1 || 2 * L.ph != L.kh - 1 ||
+      2 * L.pw != L.kw - 1 || L.kh * L.kw > 64)
+    return false;
+  const int64_t reach = int64_t(L.ph) * L.W + L.pw;     // largest |offset| of a tap, bits
+  const int64_t dlo = (reach + 63) / 64, dhi = reach / 64 + 1;
+  int64_t span = BIT_U;
+  while (span < 16 * (dlo + dhi)) span += BIT_U;
+  // No more staged words than the layer has (plus its halo), in whole batches.
+  const int64_t need = (L.Wr + dlo + dhi + BIT_U - 1) / BIT_U * BIT_U;
+  if (span > need) span = need;
+  const int64_t WB = span - dlo - dhi;
+  const int64_t wgroups = (L.Wr + WB - 1) / WB;
+  int64_t CB = 1;
+  while (CB < 64 && CB * (span / BIT_U) < nt / 64) CB *= 2;
+  while (CB < 64 && CB < L.C && ((L.C + CB - 1) / CB) * wgroups > target_blocks) CB *= 2;
+  auto lds_bytes = [&](int64_t cb) { return size_t(8) * size_t(cb * span + WB * (L.kh + L.kw)); };
+  while (CB > 1 && lds_bytes(CB) > lds_max) CB /= 2;
+  const size_t bytes = lds_bytes(CB);
+  if (bytes > lds_max) return false;
+  const int64_t cgroups = (L.C + CB - 1) / CB;
+  *g = BitGeom{uint32_t(L.N), uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.P),
+               uint32_t(L.R), uint32_t(L.Wr), uint32_t(L.K), uint32_t(L.kh * L.kw),
+               L.kh, L.kw, L.ph, L.pw, uint32_t(CB), uint32_t(WB), uint32_t(dlo),
+               uint32_t(span), uint32_t(cgroups), uint32_t(wgroups),
+               make_fastdiv(uint32_t(L.P)), make_fastdiv(uint32_t(L.W)),
+               make_fastdiv(uint32_t(span)), make_fastdiv(uint32_t(L.kh * L.kw)),
+               make_fastdiv(uint32_t(L.kw)), make_fastdiv(uint32_t(WB)),
+               make_fastdiv(uint32_t(wgroups))};
+  *lds = bytes;
+  return true;
+}
+inline uint32_t bit_blocks(const BitGeom &g) { return g.cgroups * g.wgroups; }
+
+// One block of NT threads: block index `blk` = channel group * wgroups + word group.
+// sm: 8 * (CB * span + WB * (kh + kw)) bytes of LDS.
+template <int DT, int NT>
+__device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, const BitGeom &g,
+                                                uint64_t *__restrict__ dst, uint32_t blk,
+                                                uint64_t *sm) {
+  constexpr int NW = NT / 64, U = BIT_U;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const uint32_t cg = fdiv(blk, g.divWg), wg = blk - cg * g.wgroups;
+  const uint32_t c0 = cg * g.CB, nch = min(g.CB, g.C - c0);
+  const uint32_t w0 = wg * g.WB, nw = min(g.WB, g.Wr - w0);
+  uint64_t *bits = sm;                               // [CB][span]: word w0 - dlo + j of s_c
+  uint64_t *rowm = sm + g.CB * g.span;               // [WB][kh]
+  uint64_t *colm = rowm + g.WB * g.kh;               // [WB][kw]
+
+  // Sign words in items (channel c, batch of U consecutive words; span is a multiple of
+  // U), item i to wave i % NW, the U loads of an item back to back: every load is in
+  // bounds (words outside the layer read the nearest word of it, and a flag clears the
+  // bit).  Whole-sample words step a wave-uniform element index through X; others take
+  // each lane's (sample, position).
+  const bool whole = (g.P & 63) == 0;      // every word lies in one sample
+  const uint32_t wps = g.P >> 6;
+  const uint32_t nb = g.span / U;          // batches per channel
+  for (uint32_t it = wave; it < nch * nb; it += NW) {
+    const uint32_t c = it / nb, j0 = (it - c * nb) * U;
+    const int32_t wa0 = int32_t(w0 + j0) - int32_t(g.dlo);
+    float v[U];
+    if (whole) {
+      // Word u = clamp(wa): sample u / wps, positions (u % wps) * 64 onwards.
+      const uint32_t u0 = uint32_t(min(max(wa0, 0), int32_t(g.Wr) - 1));
+      const uint32_t n0 = fdiv(u0 * 64, g.divP);
+      uint32_t q = u0 - n0 * wps;                          // word within the sample
+      int64_t e = (int64_t(n0) * g.C + c0 + c) * g.P + int64_t(q) * 64;
+      const int64_t skip = int64_t(g.C - 1) * g.P;      // to the next sample's plane
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        v[k] = load_elem<DT>(x, e + lane);
+        // Step to the next word when it is a new one (selects, no branch).
+        const int32_t wa = wa0 + k;
+        const bool step = wa >= 0 && wa + 1 < int32_t(g.Wr);
+        const bool wrap = step && q + 1 == wps;
+        e += step ? (wrap ? 64 + skip : int64_t(64)) : int64_t(0);
+        q = wrap ? 0u : (step ? q + 1 : q);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const int32_t wa = wa0 + k;
+        const uint32_t r = min(uint32_t(max(wa, 0)) * 64 + lane, g.R - 1);
+        const uint32_t n = fdiv(r, g.divP), p = r - n * g.P;
+        v[k] = load_elem<DT>(x, (int64_t(n) * g.C + c0 + c) * g.P + p);
+      }
+    }
+    uint64_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int32_t wa = wa0 + k;
+      const bool in = wa >= 0 && uint32_t(wa) * 64 + lane < g.R;
+      const uint64_t m = __ballot(in && v[k] > 0.0f);
+      if (lane == k) mine = m;
+    }
+    if (lane < U) bits[c * g.span + j0 + lane] = mine;
+  }
+  // Row and column masks of each output word.
+  for (uint32_t j = wave; j < nw; j += NW) {
+    const uint32_t r = (w0 + j) * 64 + lane;
+    const bool in = r < g.R;
+    const uint32_t n = fdiv(r, g.divP), p = r - n * g.P;
+    const uint32_t ho = fdiv(p, g.divW), wo = p - ho * g.W;
+    uint64_t mr = 0, mc = 0;
+    for (int i = 0; i < g.kh; ++i) {
+      const int h = int(ho) + i - g.ph;
+      const uint64_t m = __ballot(in && h >= 0 && h < int(g.H));
+      if (lane == i) mr = m;
+    }
+    for (int i = 0; i < g.kw; ++i) {
+      const int w = int(wo) + i - g.pw;
+      const uint64_t m = __ballot(in && w >= 0 && w < int(g.W));
+      if (lane == i) mc = m;
+    }
+    if (lane < g.kh) rowm[j * g.kh + lane] = mr;
+    if (lane < g.kw) colm[j * g.kw + lane] = mc;
+  }
+  __syncthreads();
+
+  // Output words: item o = (line chunk lc, word j), 64 lines (c, tap) per chunk.
+  const uint32_t nl = nch * g.taps, nlc = (nl + 63) / 64;
+  for (uint32_t o = wave; o < nlc * g.WB; o += NW) {
+    const uint32_t lc = fdiv(o, g.divWB), j = o - lc * g.WB;
+    if (j >= nw) continue;
+    const uint32_t ll = lc * 64 + lane;
+    if (ll >= nl) continue;
+    const uint32_t c = fdiv(ll, g.divTaps), tap = ll - c * g.taps;
+    const uint32_t i = fdiv(tap, g.divKw), jj = tap - i * g.kw;
+    const int off = (int(i) - g.ph) * int(g.W) + int(jj) - g.pw;
+    const uint32_t bp = uint32_t(int((j + g.dlo) * 64) + off);     // >= 0 by dlo
+    const uint32_t q = bp >> 6, sh = bp & 63;
+    const uint64_t lo = bits[c * g.span + q], hi = bits[c * g.span + q + 1];
+    uint64_t v = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
+    v &= rowm[j * g.kh + i] & colm[j * g.kw + jj];
+    dst[size_t(w0 + j) * g.K + size_t(c0) * g.taps + ll] = v;
+  }
+}
+
 // ----------------------------------------------------------------------------- weight bytes
 // sign(W) as signed bytes for the int8 dX product.  W is viewed as [D][K] (K = C*kh*kw,
 // line l = (c, tap)); byte d of line l is +1 if W[d][l] > 0 else -1 for d < D, 0 for

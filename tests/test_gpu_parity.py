@@ -61,6 +61,14 @@ CASES = [
      0, Recipe("sample_lognormal", sigma=1.0), "bf16"),
     ("conv_p64_ragged_b2", LayerShape("c", "conv2d", 3, 33, 40, 8, 8, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # Stride-1 same-padded kernels that are not square (bit-level im2col: 1x1, 1x3).
+    ("conv1x1_s1_b2", LayerShape("c", "conv2d", 3, 20, 12, 5, 6, 1, 1, 1, 1, 0, 0), 2, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv1x3_b3", LayerShape("c", "conv2d", 2, 5, 9, 6, 7, 1, 3, 1, 1, 0, 1), 3, 0,
+     Recipe("channel_lognormal", sigma=1.0), "bf16"),
+    # 8x8 maps, odd batch, 256 channels: the sign packs in the selection launch.
+    ("conv_p64_odd_batch_b4", LayerShape("c", "conv2d", 129, 256, 32, 8, 8, 3, 3, 1, 1, 1, 1),
+     4, 0, Recipe("sample_lognormal", sigma=1.0), "f32"),
     # 65536 output pixels per sample: group partials reduced by a workgroup per group before
     # the selection; many dW splits with the block-per-row finish.
     ("conv_bigmap_b2", LayerShape("c", "conv2d", 2, 4, 16, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
