@@ -768,10 +768,65 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
   const uint64_t own_w = t < G ? agp_weight(own_R, rmax) : 0;
 
   int64_t s_sat = 0;           // number of saturated groups (p capped at 1)
-  uint64_t w_thr = 0;          // weight of the last saturated group
   uint64_t w_rem = 0;          // weight of the unsaturated groups
   uint64_t key_thr = 0;        // TOPK: smallest kept sort key
-  if (a.mode != FQT_AGP_OFF) {
+  bool own_sat = false;        // group t is saturated
+  bool need_sort = a.mode == FQT_AGP_TOPK;
+  if (a.mode == FQT_AGP_BERNOULLI) {
+    // Saturation by rounds.  With s groups saturated and W the weight of the others, every
+    // unsaturated group with (G - b s) w >= b W saturates; the rounds end when none does.
+    // A group that passes a round passes the sorted-order test at its own position (the
+    // weights ranked between it and the saturated ones are at least its own), and a round
+    // that adds none fails that test at position s, so the rounds end at s_sat.  They
+    // usually take a few rounds (ranges that decay geometrically over the groups take the
+    // most); past SAT_ROUNDS the sort below decides instead.
+    constexpr int SAT_ROUNDS = 8;
+    __shared__ uint64_t rsum[2][SEL_NW];
+    __shared__ int32_t rcnt[2][SEL_NW];
+    uint64_t W = 0;
+    {
+      const uint64_t ws = wave_scan_add_u64(own_w);
+      if (lane == 63) rsum[1][wave] = ws;
+      __syncthreads();
+      for (int w = 0; w < SEL_NW; ++w) W += rsum[1][w];
+    }
+    int64_t s = 0;
+    bool done = false;
+    for (int round = 0; round < SAT_ROUNDS; ++round) {
+      const int64_t A = int64_t(G) - int64_t(b) * s;
+      const bool pass = t < G && !own_sat && own_w > 0 &&
+                        A * int64_t(own_w) >= int64_t(b) * int64_t(W);
+      const uint64_t ws = wave_scan_add_u64(pass ? own_w : 0ull);
+      const int32_t wc = __builtin_popcountll(__ballot(pass));
+      const int buf = round & 1;
+      if (lane == 63) {
+        rsum[buf][wave] = ws;
+        rcnt[buf][wave] = wc;
+      }
+      __syncthreads();
+      uint64_t sum = 0;
+      int32_t cnt = 0;
+      for (int w = 0; w < SEL_NW; ++w) {
+        sum += rsum[buf][w];
+        cnt += rcnt[buf][w];
+      }
+      if (cnt == 0) {
+        done = true;
+        break;
+      }
+      own_sat = own_sat || pass;
+      s += cnt;
+      W -= sum;
+    }
+    if (done) {
+      s_sat = s;
+      w_rem = s < G ? W : 0;
+    } else {
+      own_sat = false;
+      need_sort = true;
+    }
+  }
+  if (need_sort) {
     // Bitonic sort of one key per thread, descending.
     uint64_t x = t < G ? sort_key(own_w, t) : 0ull;
     int buf = 0;
@@ -820,7 +875,8 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       if (t == s_sat - 1) sat_w[1] = w;
       __syncthreads();
       w_rem = s_sat < G ? sat_w[0] : 0;
-      w_thr = s_sat > 0 ? sat_w[1] : 0;
+      const uint64_t w_thr = s_sat > 0 ? sat_w[1] : 0;   // weight of the last saturated
+      own_sat = s_sat > 0 && own_w > 0 && own_w >= w_thr;
     }
   }
 
@@ -832,7 +888,7 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       keep = true;
     } else if (a.mode == FQT_AGP_TOPK) {
       keep = sort_key(own_w, t) >= key_thr;
-    } else if (s_sat > 0 && own_w > 0 && own_w >= w_thr) {
+    } else if (own_sat) {
       keep = true;
     } else if (A > 0 && w_rem > 0 && own_w > 0) {
       const Ctr4 u = philox_block(uint64_t(t) >> 2, S.stream, a.seed, a.step, a.layer);
@@ -852,7 +908,7 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
   const float R = own_R;
   const float Z = key2f(own.x);
   float Sc = 0.0f, Zp = 0.0f, p = 0.0f;
-  const bool unit_p = a.mode != FQT_AGP_BERNOULLI || (s_sat > 0 && own_w > 0 && own_w >= w_thr);
+  const bool unit_p = a.mode != FQT_AGP_BERNOULLI || own_sat;
   if (a.mode == FQT_AGP_OFF) {
     p = 1.0f;
   } else if (a.mode == FQT_AGP_TOPK) {

@@ -75,12 +75,14 @@ class Recipe:
                         are multiplied by `outlier_factor`.
     "channel_lognormal" dy = z * s_d, s_d ~ exp(sigma N(0,1)) per output channel.
     "student_t"         dy ~ Student-t with `df` degrees of freedom, i.i.d.
+    "sample_geometric"  dy = z * ratio^n for sample n (group ranges decaying geometrically).
     """
     kind: str = "sample_lognormal"
     sigma: float = 1.5
     outlier_count: int = 0
     outlier_factor: float = 100.0
     df: float = 3.0
+    ratio: float = 0.8
 
 
 @dataclass(frozen=True)
@@ -121,6 +123,9 @@ def draw_layer(layer, recipe, seed, dtype="f32"):
         dy = z * s.reshape((1, layer.D) + (1,) * (z.ndim - 2))
     elif recipe.kind == "student_t":
         dy = rng.standard_t(recipe.df, layer.dy_shape).astype(np.float32)
+    elif recipe.kind == "sample_geometric":
+        s = np.power(np.float64(recipe.ratio), np.arange(layer.N)).astype(np.float32)
+        dy = z * s.reshape((layer.N,) + (1,) * (z.ndim - 1))
     else:
         raise ValueError(recipe.kind)
     dy = dy.astype(np.float32)

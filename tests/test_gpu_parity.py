@@ -66,6 +66,12 @@ CASES = [
      Recipe("sample_lognormal", sigma=1.0), "f32"),
     ("conv1x3_b3", LayerShape("c", "conv2d", 2, 5, 9, 6, 7, 1, 3, 1, 1, 0, 1), 3, 0,
      Recipe("channel_lognormal", sigma=1.0), "bf16"),
+    # Sample ranges decaying geometrically: AGP saturation takes 8 rounds (the most the
+    # selection runs) and 9 rounds (the selection falls back to sorting the weights).
+    ("conv_geometric_8_rounds_b2", LayerShape("c", "conv2d", 96, 8, 40, 6, 6, 3, 3, 1, 1, 1, 1),
+     2, 0, Recipe("sample_geometric", ratio=0.8), "f32"),
+    ("conv_geometric_sorted_b3", LayerShape("c", "conv2d", 200, 8, 24, 6, 6, 3, 3, 1, 1, 1, 1),
+     3, 0, Recipe("sample_geometric", ratio=0.8), "f32"),
     # 8x8 maps, odd batch, 256 channels: the sign packs in the selection launch.
     ("conv_p64_odd_batch_b4", LayerShape("c", "conv2d", 129, 256, 32, 8, 8, 3, 3, 1, 1, 1, 1),
      4, 0, Recipe("sample_lognormal", sigma=1.0), "f32"),
