@@ -187,20 +187,26 @@ struct BitGeom {
   uint32_t N, C, H, W, P, R, Wr, K, taps;
   int kh, kw, ph, pw;
   uint32_t CB, WB;            // channels and output words per block
-  uint32_t dlo, span;         // halo words below the block's first word; words staged
+  uint32_t dlo, span;         // staged words below the block's first word; words staged
+  uint32_t jl0, jl1;          // staged words [jl0, jl1) are loaded, the others are zero
+  uint32_t own;               // 1: only the block's own words are loaded (whole samples)
   uint32_t cgroups, wgroups;
-  FastDiv divP, divW, divSpan, divTaps, divKw, divWB, divWg;
+  FastDiv divP, divW, divTaps, divKw, divWB, divWg;
 };
 
 constexpr int BIT_U = 8;        // sign words a wave loads back to back
 
-// Geometry for blocks of `nt` threads: the staged words per channel (span) a multiple of
-// BIT_U with at most a sixteenth of them halo, WB = span - halo output words per block;
-// CB channels, a power of two, at least enough for one batch of BIT_U words per wave and
-// then doubled up to 64 while the grid has more than about `target_blocks` blocks (many
-// small blocks spread the loads of X over every CU), and halved while the staging
-// exceeds `lds_max` bytes.  False when the layer is not a stride-1 same-padded
-// convolution or one channel's staging does not fit.
+// Geometry for blocks of `nt` threads.  The words staged per channel are dlo + WB + dhi:
+// the WB output words of the block and the words the tap offsets reach below and above
+// them.  When a sample is a whole number of words (P % 64 == 0), WB is a whole number of
+// samples and only the block's own words are loaded: every tap a mask keeps reads its
+// own sample, so the reached words of other samples are staged as zeros.  Otherwise the
+// reached words are loaded too, and WB is large enough that they are at most a sixteenth
+// of the loads.  CB channels, a power of two, at least enough for one batch of BIT_U
+// words per wave and then doubled up to 64 while the grid has more than about
+// `target_blocks` blocks, and halved while the staging exceeds `lds_max` bytes.  False
+// when the layer is not a stride-1 same-padded convolution or one channel's staging does
+// not fit.
 inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_max,
                      BitGeom *g, size_t *lds) {
   if (L.kind != FQT_CONV2D || L.sh != 1 || L.sw != 1 || 2 * L.ph != L.kh - 1 ||
@@ -208,15 +214,28 @@ inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_m
     return false;
   const int64_t reach = int64_t(L.ph) * L.W + L.pw;     // largest |offset| of a tap, bits
   const int64_t dlo = (reach + 63) / 64, dhi = reach / 64 + 1;
-  int64_t span = BIT_U;
-  while (span < 16 * (dlo + dhi)) span += BIT_U;
-  // No more staged words than the layer has (plus its halo), in whole batches.
-  const int64_t need = (L.Wr + dlo + dhi + BIT_U - 1) / BIT_U * BIT_U;
-  if (span > need) span = need;
-  const int64_t WB = span - dlo - dhi;
+  const bool own = L.P % 64 == 0;
+  int64_t WB, jl0, jl1, span;
+  if (own) {
+    const int64_t wps = L.P / 64;
+    WB = wps * std::max<int64_t>(1, BIT_U / wps);
+    jl0 = dlo;
+    jl1 = dlo + (WB + BIT_U - 1) / BIT_U * BIT_U;
+    span = jl1 + dhi;
+  } else {
+    span = BIT_U;
+    while (span < 16 * (dlo + dhi)) span += BIT_U;
+    // No more staged words than the layer has (plus its halo), in whole batches.
+    const int64_t need = (L.Wr + dlo + dhi + BIT_U - 1) / BIT_U * BIT_U;
+    if (span > need) span = need;
+    WB = span - dlo - dhi;
+    jl0 = 0;
+    jl1 = span;
+  }
+  const int64_t batches = (jl1 - jl0) / BIT_U;
   const int64_t wgroups = (L.Wr + WB - 1) / WB;
   int64_t CB = 1;
-  while (CB < 64 && CB * (span / BIT_U) < nt / 64) CB *= 2;
+  while (CB < 64 && CB * batches < nt / 64) CB *= 2;
   while (CB < 64 && CB < L.C && ((L.C + CB - 1) / CB) * wgroups > target_blocks) CB *= 2;
   auto lds_bytes = [&](int64_t cb) { return size_t(8) * size_t(cb * span + WB * (L.kh + L.kw)); };
   while (CB > 1 && lds_bytes(CB) > lds_max) CB /= 2;
@@ -226,11 +245,11 @@ inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_m
   *g = BitGeom{uint32_t(L.N), uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.P),
                uint32_t(L.R), uint32_t(L.Wr), uint32_t(L.K), uint32_t(L.kh * L.kw),
                L.kh, L.kw, L.ph, L.pw, uint32_t(CB), uint32_t(WB), uint32_t(dlo),
-               uint32_t(span), uint32_t(cgroups), uint32_t(wgroups),
+               uint32_t(span), uint32_t(jl0), uint32_t(jl1), own ? 1u : 0u,
+               uint32_t(cgroups), uint32_t(wgroups),
                make_fastdiv(uint32_t(L.P)), make_fastdiv(uint32_t(L.W)),
-               make_fastdiv(uint32_t(span)), make_fastdiv(uint32_t(L.kh * L.kw)),
-               make_fastdiv(uint32_t(L.kw)), make_fastdiv(uint32_t(WB)),
-               make_fastdiv(uint32_t(wgroups))};
+               make_fastdiv(uint32_t(L.kh * L.kw)), make_fastdiv(uint32_t(L.kw)),
+               make_fastdiv(uint32_t(WB)), make_fastdiv(uint32_t(wgroups))};
   *lds = bytes;
   return true;
 }
@@ -252,21 +271,30 @@ __device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, cons
   uint64_t *rowm = sm + g.CB * g.span;               // [WB][kh]
   uint64_t *colm = rowm + g.WB * g.kh;               // [WB][kw]
 
-  // Sign words in items (channel c, batch of U consecutive words; span is a multiple of
-  // U), item i to wave i % NW, the U loads of an item back to back: every load is in
-  // bounds (words outside the layer read the nearest word of it, and a flag clears the
-  // bit).  Whole-sample words step a wave-uniform element index through X; others take
-  // each lane's (sample, position).
+  // Staged words [0, jl0) and [jl1, span) of every channel are zero.
+  const uint32_t pad = g.span - (g.jl1 - g.jl0);
+  for (uint32_t e = t; e < nch * pad; e += NT) {
+    const uint32_t c = e / pad, k = e - c * pad;
+    bits[c * g.span + (k < g.jl0 ? k : g.jl1 + (k - g.jl0))] = 0;
+  }
+  // Sign words [jl0, jl1) in items (channel c, batch of U consecutive words), item i to
+  // wave i % NW, the U loads of an item back to back: every load is in bounds (words
+  // outside the loaded range read the nearest word of it, and a flag clears the bit).
+  // Whole-sample words step a wave-uniform element index through X; others take each
+  // lane's (sample, position).
   const bool whole = (g.P & 63) == 0;      // every word lies in one sample
   const uint32_t wps = g.P >> 6;
-  const uint32_t nb = g.span / U;          // batches per channel
+  const uint32_t nb = (g.jl1 - g.jl0) / U; // batches per channel
+  // Words the block loads: its own [w0, w0 + nw), or everything in the layer.
+  const int32_t lo_w = g.own ? int32_t(w0) : 0;
+  const int32_t hi_w = g.own ? int32_t(w0 + nw) : int32_t(g.Wr);
   for (uint32_t it = wave; it < nch * nb; it += NW) {
-    const uint32_t c = it / nb, j0 = (it - c * nb) * U;
+    const uint32_t c = it / nb, j0 = g.jl0 + (it - c * nb) * U;
     const int32_t wa0 = int32_t(w0 + j0) - int32_t(g.dlo);
     float v[U];
     if (whole) {
       // Word u = clamp(wa): sample u / wps, positions (u % wps) * 64 onwards.
-      const uint32_t u0 = uint32_t(min(max(wa0, 0), int32_t(g.Wr) - 1));
+      const uint32_t u0 = uint32_t(min(max(wa0, lo_w), hi_w - 1));
       const uint32_t n0 = fdiv(u0 * 64, g.divP);
       uint32_t q = u0 - n0 * wps;                          // word within the sample
       int64_t e = (int64_t(n0) * g.C + c0 + c) * g.P + int64_t(q) * 64;
@@ -276,7 +304,7 @@ __device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, cons
         v[k] = load_elem<DT>(x, e + lane);
         // Step to the next word when it is a new one (selects, no branch).
         const int32_t wa = wa0 + k;
-        const bool step = wa >= 0 && wa + 1 < int32_t(g.Wr);
+        const bool step = wa >= lo_w && wa + 1 < hi_w;
         const bool wrap = step && q + 1 == wps;
         e += step ? (wrap ? 64 + skip : int64_t(64)) : int64_t(0);
         q = wrap ? 0u : (step ? q + 1 : q);
@@ -294,7 +322,7 @@ __device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, cons
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int32_t wa = wa0 + k;
-      const bool in = wa >= 0 && uint32_t(wa) * 64 + lane < g.R;
+      const bool in = wa >= lo_w && wa < hi_w && uint32_t(wa) * 64 + lane < g.R;
       const uint64_t m = __ballot(in && v[k] > 0.0f);
       if (lane == k) mine = m;
     }
