@@ -622,15 +622,17 @@ __device__ __forceinline__ uint64_t xor_partner(uint64_t v, int j) {
   }
 }
 
-// Inclusive prefix sum of v over the block's thread order, and the block total.
-template <typename T>
+// Inclusive prefix sum of v over the block's thread order, and the block total, when only
+// the first NWR waves hold non-zero values (the others get their offsets wrong).
+template <int NWR, typename T>
 __device__ T block_incl_scan(T v, T *scr, T &total, int lane, int wave) {
   if constexpr (sizeof(T) == 8) v = wave_scan_add_u64(v);
   else v = wave_scan_i32(v, 0, [](int a, int b) { return a + b; });
   if (lane == 63) scr[wave] = v;
   __syncthreads();
   T off = 0, tot = 0;
-  for (int w = 0; w < SEL_NW; ++w) {
+#pragma unroll
+  for (int w = 0; w < NWR; ++w) {
     const T x = scr[w];
     off += w < wave ? x : T(0);
     tot += x;
@@ -761,7 +763,8 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
     if (lane == 0) scr_f[wave] = __int_as_float(m);
     __syncthreads();
     rmax = 0.0f;
-    for (int w = 0; w < SEL_NW; ++w) rmax = fmaxf(rmax, scr_f[w]);
+#pragma unroll
+    for (int w = 0; w < GP / 64; ++w) rmax = fmaxf(rmax, scr_f[w]);   // groups: t < G <= GP
   }
   const int2 own = t < G ? gk[t] : make_int2(0, 0);
   const float own_R = group_range(own);
@@ -788,7 +791,8 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       const uint64_t ws = wave_scan_add_u64(own_w);
       if (lane == 63) rsum[1][wave] = ws;
       __syncthreads();
-      for (int w = 0; w < SEL_NW; ++w) W += rsum[1][w];
+#pragma unroll
+      for (int w = 0; w < GP / 64; ++w) W += rsum[1][w];
     }
     int64_t s = 0;
     bool done = false;
@@ -806,7 +810,8 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       __syncthreads();
       uint64_t sum = 0;
       int32_t cnt = 0;
-      for (int w = 0; w < SEL_NW; ++w) {
+#pragma unroll
+      for (int w = 0; w < GP / 64; ++w) {
         sum += rsum[buf][w];
         cnt += rcnt[buf][w];
       }
@@ -864,12 +869,12 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       // is s_sat.
       const uint64_t w = t < G ? (x >> ID_BITS) : 0ull;
       uint64_t total;
-      const uint64_t incl = block_incl_scan<uint64_t>(w, scr_u, total, lane, wave);
+      const uint64_t incl = block_incl_scan<GP / 64, uint64_t>(w, scr_u, total, lane, wave);
       const uint64_t Wp = total - incl + w;
       const bool pass = t < G && w > 0 &&
                         (int64_t(G) - int64_t(b) * t) * int64_t(w) >= int64_t(b) * int64_t(Wp);
       int32_t cnt_total;
-      block_incl_scan<int32_t>(pass ? 1 : 0, scr_i, cnt_total, lane, wave);
+      block_incl_scan<GP / 64, int32_t>(pass ? 1 : 0, scr_i, cnt_total, lane, wave);
       s_sat = cnt_total;
       if (t == s_sat) sat_w[0] = Wp;
       if (t == s_sat - 1) sat_w[1] = w;
@@ -901,7 +906,7 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
     }
   }
   int32_t count;
-  const int32_t rank = block_incl_scan<int32_t>(keep ? 1 : 0, scr_i, count, lane, wave) -
+  const int32_t rank = block_incl_scan<GP / 64, int32_t>(keep ? 1 : 0, scr_i, count, lane, wave) -
                        (keep ? 1 : 0);
   if (t == 0) *S.count = count;
   if (t >= G) return;
