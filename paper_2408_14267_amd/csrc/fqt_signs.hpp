@@ -198,11 +198,12 @@ constexpr int BIT_U = 8;        // sign words a wave loads back to back
 
 // Geometry for blocks of `nt` threads.  The words staged per channel are dlo + WB + dhi:
 // the WB output words of the block and the words the tap offsets reach below and above
-// them.  When a sample is a whole number of words (P % 64 == 0), WB is a whole number of
-// samples and only the block's own words are loaded: every tap a mask keeps reads its
-// own sample, so the reached words of other samples are staged as zeros.  Otherwise the
-// reached words are loaded too, and WB is large enough that they are at most a sixteenth
-// of the loads.  CB channels, a power of two, at least enough for one batch of BIT_U
+// them.  When a sample is a whole number of words, at most 16 (P % 64 == 0, P <= 1024), WB
+// is a whole number of samples and only the block's own words are loaded: every tap a
+// mask keeps reads its own sample, so the reached words of other samples are staged as
+// zeros.  Otherwise the reached words are loaded too, and WB is large enough that they are
+// at most a sixteenth of the loads (whole-sample blocks of larger samples would be many
+// serial batches per wave).  CB channels, a power of two, at least enough for one batch of BIT_U
 // words per wave and then doubled up to 64 while the grid has more than about
 // `target_blocks` blocks, and halved while the staging exceeds `lds_max` bytes.  False
 // when the layer is not a stride-1 same-padded convolution or one channel's staging does
@@ -214,7 +215,7 @@ inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_m
     return false;
   const int64_t reach = int64_t(L.ph) * L.W + L.pw;     // largest |offset| of a tap, bits
   const int64_t dlo = (reach + 63) / 64, dhi = reach / 64 + 1;
-  const bool own = L.P % 64 == 0;
+  const bool own = L.P % 64 == 0 && L.P <= 1024;
   int64_t WB, jl0, jl1, span;
   if (own) {
     const int64_t wps = L.P / 64;
