@@ -18,6 +18,6 @@ fqt    : the method itself -- group statistics, AGP probabilities and masks,
          integer contractions and the per-group rescale (Sections 3.2, 5.2,
          5.3 and Appendix C of the paper).
 
-Parity status of each function is stated in its docstring; the readings taken
-where the paper is silent are listed in the design doc of the repository.
+Parity status of each function, and the reading taken where the paper is silent,
+are stated in its docstring.
 """

@@ -29,8 +29,8 @@ Integer contractions go through a float64 matrix product, which is exact
 because every partial sum stays far below 2^53 (asserted).
 
 Where the paper is silent or garbled, the reading taken is stated at the
-function; the design doc lists all of them.  The functions with no independent pin
-say "parity unpinned" in their docstring.
+function.  The functions with no independent pin say "parity unpinned" in their
+docstring.
 """
 import math
 from dataclasses import dataclass, field
