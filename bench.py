@@ -217,8 +217,8 @@ def main():
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; the layer backward "
-                                   "shards by data parallelism with one dW all-reduce, which "
-                                   "is not part of this build", "n_gpus": args.gpus}))
+                                   "would shard by data parallelism with one dW all-reduce, "
+                                   "which is not implemented", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
