@@ -498,3 +498,39 @@ def layer_backward(x, w, dy, bits, mode=AGP_BERNOULLI, seed=0, step=0, layer_id=
                     dW=dW.reshape(wshape), dX=dX.reshape(xshape),
                     dW_t1=t1w.reshape(wshape), dW_t2=t2w.reshape(wshape),
                     dX_t1=t1x.reshape(xshape), dX_t2=t2x.reshape(xshape))
+
+
+# --------------------------------------------------------------------------- forward (binary layer)
+
+@dataclass
+class Forward:
+    I: np.ndarray           # int64 [N][D][Ho][Wo] (linear: [N][D]) sum_k sign(X_u) sign(Theta_u)
+    Y: np.ndarray           # float64, I scaled by Gamma per output channel
+
+
+def layer_forward(x, w, gamma, stride=(1, 1), pad=(0, 0)):
+    """Forward of a binary linear/conv layer (Section 5.1: H = (sign(H_prev) sign(Theta))
+    scaled per output channel by the learnable Gamma; Appendix C, Alg. 1 forward with the
+    Unfolder for convolutions).
+
+    x : [N][C] (linear) or [N][C][H][W];  w : [D][C] or [D][C][kh][kw];  gamma : [D].
+    The integer product I[r][d] = sum over k = (c, i, j) of sign(X_u)[r][k] sign(Theta_u)[d][k]
+    is exact; Y = gamma_d * I in float64.  Padding as in unfold_sign_bits (sign -1).
+    """
+    x = np.asarray(x)
+    w = np.asarray(w)
+    gamma = np.asarray(gamma, dtype=np.float64)
+    linear = x.ndim == 2
+    x4 = x.reshape(x.shape[0], x.shape[1], 1, 1) if linear else x
+    D = w.shape[0]
+    kh, kw = (1, 1) if linear else w.shape[2:]
+    N, C, H, W = x4.shape
+    Ho, Wo = conv_out_hw(H, W, kh, kw, stride, pad)
+    sx = unfold_sign_bits(x4, kh, kw, stride, pad).astype(np.int64) * 2 - 1   # [K][R]
+    sw = weight_sign_bits(w).astype(np.int64) * 2 - 1                          # [K][D]
+    I_rd = int_matmul(sx.T, sw)                                                # [R][D]
+    I = I_rd.reshape(N, Ho, Wo, D).transpose(0, 3, 1, 2)
+    Y = I.astype(np.float64) * gamma[None, :, None, None]
+    if linear:
+        I, Y = I.reshape(N, D), Y.reshape(N, D)
+    return Forward(I=I, Y=Y)
