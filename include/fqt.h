@@ -148,6 +148,7 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
 #define FQT_WS_QUANTIZE 0
 #define FQT_WS_LAYER 1
 #define FQT_WS_GEMM_DW 2
+#define FQT_WS_FORWARD 3   /* fqt_binary_forward; cfg may be NULL for this one */
 int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
                        size_t *bytes);
 
@@ -240,6 +241,23 @@ int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
 int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
                        const void *W, const void *dY, void *dX, float *dW, void *ws,
                        size_t ws_bytes, void *hip_stream);
+
+/* Binary layer forward (Section 5.1: the output is sign(H_prev) times sign(Theta), scaled
+ * per output channel by the learnable Gamma; Appendix C, Alg. 1 forward, with the Unfolder
+ * for convolutions):
+ *   I[n][d][ho][wo] = sum over (c, i, j) of sign(X)[n][c][ho*sh - ph + i][wo*sw - pw + j]
+ *                     * sign(W)[d][c][i][j],   sign(x) = -1 for x <= 0 (NaN too), +1 else,
+ *   Y = gamma[d] * I (one float32 rounding; bf16 Y rounds that to nearest even).
+ * Padded positions of X count as sign -1 (the unfold is zero-padded, then binarized).
+ * X: x_dtype [N][C][H][W] (linear [N][C]); W: w_dtype [D][C][kh][kw] ([D][C]); gamma:
+ * float32 [D]; Y: dy_dtype, the layout of dY ([N][D][Ho][Wo], linear [N][D]); I_out
+ * (optional, NULL to skip): int32 in Y's layout.  ws: >= fqt_workspace_size(FQT_WS_FORWARD)
+ * bytes, 256-byte aligned, no initialisation needed (it holds the packed operands:
+ * sign(X_u) bits and sign(W) bytes).  All pointers are device pointers; stream-ordered on
+ * hip_stream; returns FQT_E_SHAPE when an operand exceeds 2 GiB. */
+int fqt_binary_forward(const fqt_layer_desc *desc, const void *X, const void *W,
+                       const float *gamma, void *Y, int32_t *I_out, void *ws, size_t ws_bytes,
+                       void *hip_stream);
 
 /* Static description of a status code. */
 const char *fqt_status_string(int status);

@@ -71,6 +71,25 @@ size_t carve_layer_ws(void *ws, const Layer &L, const fqt_quant_cfg &cfg, LayerW
   return c.off;
 }
 
+// Forward workspace: sign(X_u) word-major [Wr][K], the same bits k-block-major [Kw][Wr*64]
+// and sign(W) as +-1 bytes [Dp][Kp] (Dp, Kp: D and K rounded up to 64).
+struct ForwardWs {
+  uint64_t *xwm, *xrows;
+  int8_t *wrows;
+  int64_t Dp, Kp;
+};
+size_t carve_forward_ws(void *ws, const Layer &L, ForwardWs *out) {
+  Carver c{static_cast<char *>(ws)};
+  ForwardWs f;
+  f.Dp = (L.D + 63) / 64 * 64;
+  f.Kp = (L.K + 63) / 64 * 64;
+  f.xwm = c.take<uint64_t>(size_t(L.Wr) * L.K);
+  f.xrows = c.take<uint64_t>(size_t(f.Kp / 64) * L.Wr * 64);
+  f.wrows = c.take<int8_t>(size_t(f.Dp) * f.Kp);
+  if (out) *out = f;
+  return c.off;
+}
+
 int check_qgrad(const fqt_qgrad *q, bool psq, bool pcq) {
   if (!q) return FQT_E_NULL;
   if (psq) {
@@ -201,8 +220,12 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
                        size_t *bytes) {
   Layer L;
   FQT_TRY(make_layer(desc, &L));
-  FQT_TRY(check_cfg(cfg, L));
   if (!bytes) return FQT_E_NULL;
+  if (which == FQT_WS_FORWARD) {          // the forward takes no quantizer configuration
+    *bytes = carve_forward_ws(nullptr, L, nullptr);
+    return FQT_OK;
+  }
+  FQT_TRY(check_cfg(cfg, L));
   if (which == FQT_WS_QUANTIZE) *bytes = quant_ws_bytes(L);
   else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, *cfg, nullptr);
   else if (which == FQT_WS_GEMM_DW) *bytes = gemm_dw_ws_bytes(L, *cfg);
@@ -333,6 +356,33 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   }
   return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, w.qws.sslot,
                          w.qws.cslot, s);
+}
+
+int fqt_binary_forward(const fqt_layer_desc *desc, const void *X, const void *W,
+                       const float *gamma, void *Y, int32_t *I_out, void *ws, size_t ws_bytes,
+                       void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  if (!X || !W || !gamma || !Y || !ws) return FQT_E_NULL;
+  if (!aligned(X, dtype_size(L.x_t)) || !aligned(W, dtype_size(L.w_t)) || !aligned(gamma, 4) ||
+      !aligned(Y, dtype_size(L.dy_t)) || (I_out && !aligned(I_out, 4)) || !aligned(ws, 256))
+    return FQT_E_ALIGN;
+  ForwardWs f;
+  const size_t need = carve_forward_ws(ws, L, &f);
+  if (ws_bytes < need) return FQT_E_WORKSPACE;
+  // Byte offsets the kernels form stay below 2^31.
+  if (f.Dp * f.Kp > LIMIT31 || (f.Kp / 64) * L.Wr * 64 * 8 > LIMIT31 ||
+      int64_t(L.N) * L.D * L.P > LIMIT31)
+    return FQT_E_SHAPE;
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  if (L.kind == FQT_LINEAR)
+    FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, f.xwm,
+                             nullptr, s, true));
+  else
+    FQT_TRY(launch_pack_bits(X, L.x_t, 0, 0, 0, FQT_PACK_IM2COL, &L, f.xwm, nullptr, s, true));
+  FQT_TRY(launch_transpose_bits(f.xwm, L.Wr, L.K, f.xrows, s));
+  FQT_TRY(launch_pack_w_rows(W, L, f.Dp, f.Kp, f.wrows, s));
+  return launch_forward_gemm(L, f.wrows, f.Dp, f.Kp, f.xrows, gamma, Y, I_out, s);
 }
 
 }  // extern "C"

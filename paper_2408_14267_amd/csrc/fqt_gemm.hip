@@ -818,6 +818,95 @@ __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa,
   }
 }
 
+
+// ----------------------------------------------------------------------------- forward
+
+// Binary forward product (Section 5.1; Appendix C, Alg. 1 forward and the Unfolder):
+// I[r][d] = sum_k sign(X_u)[r][k] sign(W)[d][k] over k < Kp, and Y = gamma_d * I.
+// Operands: sign(W) as +-1 bytes, row-major [Dp][Kp] (0 past D and K), the MFMA's src0
+// (rows = output channels); sign(X_u) as bits, k-block-major [Kw][Rp] (word (kb, r) holds
+// lines 64 kb .. 64 kb + 63 of row r), expanded in registers 16 bits at a time into the
+// src1 bytes (columns = rows r of the unfolded input, so output lanes run along pixels).
+// Lines past K are -1 in X and 0 in W, so they add nothing.  Each wave holds 64 channels
+// x 32 rows (two MFMA tiles sharing one expanded X operand); a block's four waves take
+// four consecutive row tiles of the same 64 channels.  Grid: ceil(Dp/64) x ceil(R/128),
+// channel blocks fastest.
+struct FwdArgs {
+  const int8_t *wb;              // [Dp][Kp]
+  const uint64_t *xr;            // [Kw][Rp]
+  const float *gamma;            // [D]
+  void *Y;                       // [N][D][P]
+  int32_t *I_out;
+  int y_t;
+  uint32_t D, Dp, Kp, R, Rp, P, dblocks;
+  uint32_t wb_bytes, xr_bytes;
+  FastDiv divP, divDb;
+};
+constexpr int FWD_WAVES = 4;
+constexpr int FWD_THREADS = FWD_WAVES * 64;
+
+template <int NB>
+__global__ __launch_bounds__(FWD_THREADS) void k_mfma_fwd(FwdArgs a) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t wave = wave_id();
+  const int i = lane & 31, g = lane >> 5;
+  const uint32_t rb = fdiv(blockIdx.x, a.divDb), db = blockIdx.x - rb * a.dblocks;
+  const uint32_t d0 = db * 64, r0 = (rb * FWD_WAVES + wave) * 32;
+  if (r0 >= a.R) return;                               // wave-uniform: no barrier follows
+  const __amdgpu_buffer_rsrc_t wrs = buffer_of(a.wb, a.wb_bytes);
+  const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xr, a.xr_bytes);
+  // src0 rows d0 + i and d0 + 32 + i (always inside Dp), bytes 16 g .. 16 g + 15 of a step.
+  const uint32_t aoff0 = (d0 + uint32_t(i)) * a.Kp + 16 * g, aoff1 = aoff0 + 32 * a.Kp;
+  const uint32_t boff = (r0 + uint32_t(i)) * 8;        // word (kb, r0 + i) at kb * Rp * 8
+  const uint32_t steps = a.Kp / 32;                    // Kp is a multiple of 64
+  v16i acc0 = {0}, acc1 = {0};
+  for (uint32_t s0 = 0; s0 < steps; s0 += 2 * NB) {
+    // NB words of X (two steps each) and their 4 NB byte pieces of W, all issued before
+    // the first product.
+    uint64_t xw[NB];
+    v4i A0[2 * NB], A1[2 * NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const uint32_t st = s0 + 2 * u;
+      const bool live = st < steps;
+      xw[u] = live ? __builtin_bit_cast(uint64_t, load8(xrs, boff, (st / 2) * a.Rp * 8)) : 0ull;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        A0[2 * u + h] = load16(wrs, live ? aoff0 : BUF_NONE, (st + h) * 32);
+        A1[2 * u + h] = load16(wrs, live ? aoff1 : BUF_NONE, (st + h) * 32);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const v4i b = signs16(uint32_t(xw[u] >> (32 * h + 16 * g)) & 0xFFFFu);
+        acc0 = mfma_i8(A0[2 * u + h], b, acc0);
+        acc1 = mfma_i8(A1[2 * u + h], b, acc1);
+      }
+    }
+  }
+  const uint32_t r = r0 + uint32_t(i);
+  if (r >= a.R) return;
+  const uint32_t n = fdiv(r, a.divP), p = r - n * a.P;
+  const size_t base = size_t(n) * a.D * a.P + p;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const uint32_t d = d0 + 32 * t + uint32_t(acc_row(v, g));
+      if (d >= a.D) continue;
+      const int I = t ? acc1[v] : acc0[v];
+      const float y = __fmul_rn(a.gamma[d], float(I));
+      const size_t o = base + size_t(d) * a.P;
+      if (a.y_t == FQT_BF16) static_cast<uint16_t *>(a.Y)[o] = f32_to_bf16(y);
+      else static_cast<float *>(a.Y)[o] = y;
+      if (a.I_out) a.I_out[o] = I;
+    }
+  }
+}
+
 }  // namespace
 
 // Splits of the dW contraction over N*Ho*Wo: enough 32x32 wave tiles of the expected
@@ -1026,6 +1115,22 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
     if (dwa.S == 1) go2.template operator()<false, true>();
     else go2.template operator()<false, false>();
   }
+  return last_launch_status();
+}
+
+int launch_forward_gemm(const Layer &L, const int8_t *wrows, int64_t Dp, int64_t Kp,
+                        const uint64_t *xrows, const float *gamma, void *Y, int32_t *I_out,
+                        hipStream_t s) {
+  FwdArgs a;
+  a.wb = wrows; a.xr = xrows; a.gamma = gamma; a.Y = Y; a.I_out = I_out; a.y_t = L.dy_t;
+  a.D = uint32_t(L.D); a.Dp = uint32_t(Dp); a.Kp = uint32_t(Kp); a.R = uint32_t(L.R);
+  a.Rp = uint32_t(L.Wr * 64); a.P = uint32_t(L.P);
+  a.dblocks = uint32_t(Dp / 64);
+  a.wb_bytes = uint32_t(Dp * Kp);
+  a.xr_bytes = uint32_t((Kp / 64) * L.Wr * 64 * 8);
+  a.divP = make_fastdiv(uint32_t(L.P)); a.divDb = make_fastdiv(a.dblocks);
+  const uint32_t rblocks = uint32_t((L.R + 32 * FWD_WAVES - 1) / (32 * FWD_WAVES));
+  hipLaunchKernelGGL(k_mfma_fwd<4>, dim3(a.dblocks * rblocks), dim3(FWD_THREADS), 0, s, a);
   return last_launch_status();
 }
 

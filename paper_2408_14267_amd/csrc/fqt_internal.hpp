@@ -120,6 +120,19 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
                     float *dW, void *dw_ws, const float2 *sslot, const float2 *cslot,
                     hipStream_t s);
 
+// Binary forward (Section 5.1): the operands and the product.
+// Word-major sign words [Wr][K] -> k-block-major [Kw][Wr * 64] (bit b of word (kb, r) is
+// line 64 kb + b of row r; lines past K are 0).
+int launch_transpose_bits(const uint64_t *src, int64_t Wr, int64_t K, uint64_t *dst,
+                          hipStream_t s);
+// sign(W) as +-1 bytes [Dp][Kp] in W's own [D][C*kh*kw] order, 0 past D and past K.
+int launch_pack_w_rows(const void *W, const Layer &L, int64_t Dp, int64_t Kp, int8_t *dst,
+                       hipStream_t s);
+// Y[n][d][p] = gamma[d] * sum_k sign(X_u)[r][k] sign(W)[d][k] from the two packed operands.
+int launch_forward_gemm(const Layer &L, const int8_t *wrows, int64_t Dp, int64_t Kp,
+                        const uint64_t *xrows, const float *gamma, void *Y, int32_t *I_out,
+                        hipStream_t s);
+
 inline int hip_status(hipError_t e) { return e == hipSuccess ? FQT_OK : FQT_E_HIP; }
 inline int last_launch_status() { return hip_status(hipGetLastError()); }
 

@@ -194,7 +194,78 @@ __global__ __launch_bounds__(WB_THREADS) void k_pack_w_i8(const void *__restrict
   pack_w_body<DT>(w, g, dst, lsum, blockIdx.x, sm);
 }
 
+// 64 x 64 bit transpose, one wave per block (w, kb): lane l loads word (w, 64 kb + l) and
+// ends with word (kb, 64 w + l).  Six stages swap the off-diagonal S x S sub-blocks
+// (S = 32, 16, ..., 1) between lanes l and l ^ S: the lane with bit S of its index clear
+// keeps the bits b with bit S of b clear and takes its partner's, shifted up by S; the
+// other lane keeps the bits with bit S set and takes its partner's, shifted down.
+template <int S>
+__device__ __forceinline__ uint64_t transpose_stage(uint64_t x, int lane) {
+  constexpr uint64_t m = S == 32 ? 0x00000000FFFFFFFFull : S == 16 ? 0x0000FFFF0000FFFFull
+                       : S == 8 ? 0x00FF00FF00FF00FFull : S == 4 ? 0x0F0F0F0F0F0F0F0Full
+                       : S == 2 ? 0x3333333333333333ull : 0x5555555555555555ull;
+  const uint64_t y = lane_xor64<S>(x);
+  return (lane & S) == 0 ? (x & m) | ((y & m) << S) : (x & ~m) | ((y & ~m) >> S);
+}
+__global__ __launch_bounds__(THREADS) void k_transpose_bits(const uint64_t *__restrict__ src,
+                                                            uint32_t Wr, uint32_t K,
+                                                            uint32_t Kw,
+                                                            uint64_t *__restrict__ dst) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t blk = blockIdx.x * WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (blk >= Wr * Kw) return;
+  const uint32_t kb = blk / Wr, w = blk - kb * Wr;     // consecutive waves: consecutive w
+  const uint32_t line = kb * 64 + uint32_t(lane);
+  uint64_t x = line < K ? src[size_t(w) * K + line] : 0ull;
+  x = transpose_stage<32>(x, lane);
+  x = transpose_stage<16>(x, lane);
+  x = transpose_stage<8>(x, lane);
+  x = transpose_stage<4>(x, lane);
+  x = transpose_stage<2>(x, lane);
+  x = transpose_stage<1>(x, lane);
+  dst[size_t(kb) * Wr * 64 + size_t(w) * 64 + lane] = x;
+}
+
+// sign(W) rows as +-1 bytes, 16 per thread: row d, bytes [16 q, 16 q + 16) of Kp.
+template <int DT>
+__global__ __launch_bounds__(THREADS) void k_pack_w_rows(const void *__restrict__ w, uint32_t D,
+                                                         uint32_t K, uint32_t Kp, uint32_t Dp,
+                                                         int8_t *__restrict__ dst) {
+  const uint32_t qpr = Kp / 16;                          // 16-byte pieces per row
+  const uint32_t e = blockIdx.x * THREADS + threadIdx.x;
+  if (e >= Dp * qpr) return;
+  const uint32_t d = e / qpr, k0 = (e - d * qpr) * 16;
+  uint32_t word[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const uint32_t k = k0 + uint32_t(j);
+    uint32_t b = 0u;                                     // 0 past D or K
+    if (d < D && k < K) b = load_elem<DT>(w, int64_t(d) * K + k) > 0.0f ? 0x01u : 0xFFu;
+    word[j >> 2] |= b << (8 * (j & 3));
+  }
+  *reinterpret_cast<uint4 *>(dst + size_t(d) * Kp + k0) = make_uint4(word[0], word[1], word[2], word[3]);
+}
+
 }  // namespace
+
+int launch_transpose_bits(const uint64_t *src, int64_t Wr, int64_t K, uint64_t *dst,
+                          hipStream_t s) {
+  const int64_t Kw = (K + 63) / 64;
+  hipLaunchKernelGGL(k_transpose_bits, dim3(blocks_for(Wr * Kw)), dim3(THREADS), 0, s, src,
+                     uint32_t(Wr), uint32_t(K), uint32_t(Kw), dst);
+  return last_launch_status();
+}
+
+int launch_pack_w_rows(const void *W, const Layer &L, int64_t Dp, int64_t Kp, int8_t *dst,
+                       hipStream_t s) {
+  const int64_t items = Dp * (Kp / 16);
+  dispatch_dtype(L.w_t, [&]<int DT>() {
+    hipLaunchKernelGGL(k_pack_w_rows<DT>, dim3(unsigned((items + THREADS - 1) / THREADS)),
+                       dim3(THREADS), 0, s, W, uint32_t(L.D), uint32_t(L.K), uint32_t(Kp),
+                       uint32_t(Dp), dst);
+  });
+  return last_launch_status();
+}
 
 int launch_pack_w_i8(const void *W, const Layer &L, int8_t *dst, int32_t *lsum, hipStream_t s) {
   const PackWGeom g = pack_w_geom(L);

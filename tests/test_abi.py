@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     lib = ctypes.CDLL(fqt.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -121,3 +121,20 @@ def test_state_bytes_constant_matches_header():
     d = _desc()
     c = fqt.quant_cfg(4)
     assert fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE) > fqt.FQT_WS_STATE_BYTES
+
+
+def test_forward_workspace_and_validation():
+    lib = fqt._lib
+    d = _desc()
+    n = fqt.fqt_workspace_size(d, None, fqt.FQT_WS_FORWARD)     # no quantizer config needed
+    L = WORKLOADS["vgg_cifar_conv3x3_256"].layers[0]
+    K, R = L.C * 9, L.N * 64
+    assert n >= K * (R // 64) * 8 * 2 + 256 * K
+    fake = ctypes.c_void_p(1 << 20)
+    st = lib.fqt_binary_forward(ctypes.byref(d), fake, fake, None, fake, None, fake, n, None)
+    assert st == fqt.FQT_E_NULL
+    st = lib.fqt_binary_forward(ctypes.byref(d), fake, fake, fake, fake, None, fake, 16, None)
+    assert st == fqt.FQT_E_WORKSPACE
+    st = lib.fqt_binary_forward(ctypes.byref(d), fake, fake, ctypes.c_void_p((1 << 20) + 2),
+                                fake, None, fake, n, None)
+    assert st == fqt.FQT_E_ALIGN

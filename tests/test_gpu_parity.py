@@ -375,3 +375,43 @@ def test_workspace_shared_across_layers():
             _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
             _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
             assert torch.count_nonzero(ws[:state]).item() == 0, "state bytes left non-zero"
+
+
+FORWARD_CASES = [
+    ("conv3x3_p1", LayerShape("c", "conv2d", 3, 7, 70, 9, 9, 3, 3, 1, 1, 1, 1), "f32"),
+    ("conv_s2", LayerShape("c", "conv2d", 2, 16, 32, 11, 11, 3, 3, 2, 2, 1, 1), "f32"),
+    ("conv1x1_s2", LayerShape("c", "conv2d", 4, 64, 128, 8, 8, 1, 1, 2, 2, 0, 0), "f32"),
+    ("conv7x7_s2", LayerShape("c", "conv2d", 2, 3, 64, 32, 32, 7, 7, 2, 2, 3, 3), "f32"),
+    ("conv5x5_p2", LayerShape("c", "conv2d", 3, 6, 40, 10, 10, 5, 5, 1, 1, 2, 2), "f32"),
+    ("conv2x3_mixed", LayerShape("c", "conv2d", 2, 5, 9, 6, 7, 2, 3, 1, 2, 0, 1), "f32"),
+    ("conv_p64_bf16", LayerShape("c", "conv2d", 5, 33, 96, 8, 8, 3, 3, 1, 1, 1, 1), "bf16"),
+    ("linear_ragged", LayerShape("fc", "linear", 37, 300, 77), "f32"),
+    ("linear_wide", LayerShape("fc", "linear", 64, 2048, 1000), "f32"),
+    ("vgg_cifar_full", WORKLOADS["vgg_cifar_conv3x3_256"].layers[0], "f32"),
+]
+
+
+@pytest.mark.parametrize("name,layer,dtype", FORWARD_CASES, ids=[c[0] for c in FORWARD_CASES])
+def test_forward_matches_oracle(name, layer, dtype):
+    """fqt_binary_forward against the oracle's forward: the integer product bit-exact, Y
+    within the one float32 rounding of gamma * I (bf16 Y: within bf16 rounding)."""
+    _announce(f"[gpu parity] forward {name}: {layer} {dtype}")
+    fqt = _fqt()
+    x, w, _ = draw_layer(layer, Recipe(), 7, dtype)
+    gamma = np.random.default_rng(11).standard_normal(layer.D).astype(np.float32)
+    ref = ofqt.layer_forward(x, w, gamma, stride=layer.stride, pad=layer.pad)
+    dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
+    desc = fqt.layer_desc(layer, dy_dtype=dt, x_dtype=dt, w_dtype=fqt.FQT_F32, dx_dtype=dt)
+    X, W = _to_dev(x, dtype), _to_dev(w, "f32")
+    G = torch.from_numpy(gamma).cuda()
+    ydt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    Y = torch.full(ref.Y.shape, 7.0, dtype=ydt, device="cuda")
+    I = torch.full(ref.I.shape, 7, dtype=torch.int32, device="cuda")
+    ws = fqt.workspace(desc, None, fqt.FQT_WS_FORWARD)
+    for _ in range(2):                 # a reused workspace gives the same result
+        fqt.fqt_binary_forward(desc, X, W, G, Y, I, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(I.cpu().numpy(), ref.I), "forward integer product"
+        g = Y.float().cpu().numpy().astype(np.float64)
+        rel = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
+        assert (np.abs(g - ref.Y) <= rel * np.abs(ref.Y)).all(), "forward output"
