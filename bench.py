@@ -71,9 +71,11 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="bound on the CPU oracle sample (seconds of work)")
     p.add_argument("--no-graph", action="store_true", help="time eager launches only")
-    p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep"),
+    p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
-                        "layer backwards, or the dW binary GEMM sweep (one JSON line each)")
+                        "layer backwards, the dW binary GEMM sweep, or the binary forward of "
+                        "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer "
+                        "(one JSON line each)")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="first run a plain device copy of this many MiB (three times), so that "
                         "a counter run can scale FETCH_SIZE / WRITE_SIZE by a known byte count")
@@ -128,6 +130,36 @@ def suite(name, reps=10):
         e1.record(st)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k
+
+    if name == "forward":
+        for wname in (WORKLOAD, "resnet18_32px", "vgg16_224_bf16"):
+            wl = WORKLOADS[wname]
+            tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+            tot_ms, tot_ops = 0.0, 0.0
+            for li, L in enumerate(wl.layers):
+                X = _gen(torch, L.x_shape, tdt, dev)
+                W = _gen(torch, L.w_shape, torch.float32, dev)
+                G = _gen(torch, (L.D,), torch.float32, dev)
+                Y = torch.empty(L.dy_shape, dtype=tdt, device=dev)
+                dt = fqt.FQT_BF16 if tdt == torch.bfloat16 else fqt.FQT_F32
+                desc = fqt.layer_desc(L, dt, dt, fqt.FQT_F32, dt)
+                ws = fqt.workspace(desc, None, fqt.FQT_WS_FORWARD, device=dev)
+                step = lambda: fqt.fqt_binary_forward(desc, X, W, G, Y, None, ws, st)
+                for _ in range(3):
+                    step()
+                ms = timed(step, reps)
+                ops = 2.0 * L.binary_macs()
+                tot_ms += ms
+                tot_ops += ops
+                print(json.dumps({"suite": name, "workload": wname, "layer": li, "name": L.name,
+                                  "ms": round(ms, 4), "binary_TOPS": round(ops / ms / 1e9, 1),
+                                  "mfma_frac": round(ops / ms / 1e9 / MFMA_I8_PEAK_TOPS, 4)}),
+                      flush=True)
+                del X, W, G, Y, ws
+                torch.cuda.empty_cache()
+            print(json.dumps({"suite": name, "workload": wname, "total_ms": round(tot_ms, 3),
+                              "binary_TOPS": round(tot_ops / tot_ms / 1e9, 1)}), flush=True)
+        return
 
     if name == "gemm_sweep":
         from paper_2408_14267_amd.workloads import gemm_sweep_points

@@ -823,16 +823,16 @@ __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa,
 
 // Binary forward product (Section 5.1; Appendix C, Alg. 1 forward and the Unfolder):
 // I[r][d] = sum_k sign(X_u)[r][k] sign(W)[d][k] over k < Kp, and Y = gamma_d * I.
-// Operands: sign(W) as +-1 bytes, row-major [Dp][Kp] (0 past D and K), the MFMA's src0
-// (rows = output channels); sign(X_u) as bits, k-block-major [Kw][Rp] (word (kb, r) holds
+// Operands: sign(W) as +-1 bytes in 32-line chunks [Kp/32][Dp][32] (0 past D and K), the
+// MFMA's src0 (rows = output channels; a wave's 32 rows of one chunk are 1 KB contiguous); sign(X_u) as bits, k-block-major [Kw][Rp] (word (kb, r) holds
 // lines 64 kb .. 64 kb + 63 of row r), expanded in registers 16 bits at a time into the
 // src1 bytes (columns = rows r of the unfolded input, so output lanes run along pixels).
-// Lines past K are -1 in X and 0 in W, so they add nothing.  Each wave holds 64 channels
-// x 32 rows (two MFMA tiles sharing one expanded X operand); a block's four waves take
-// four consecutive row tiles of the same 64 channels.  Grid: ceil(Dp/64) x ceil(R/128),
-// channel blocks fastest.
+// Lines past K are -1 in X and 0 in W, so they add nothing.  A tile is 64 channels x 32
+// rows (two MFMA tiles sharing one expanded X operand); a block's four waves take
+// consecutive row tiles of the same 64 channels, WPT waves per tile splitting its
+// contraction.  Grid: ceil(Dp/64) x ceil(R/(32 * 4 / WPT)), channel blocks fastest.
 struct FwdArgs {
-  const int8_t *wb;              // [Dp][Kp]
+  const int8_t *wb;              // [Kp/32][Dp][32]
   const uint64_t *xr;            // [Kw][Rp]
   const float *gamma;            // [D]
   void *Y;                       // [N][D][P]
@@ -845,56 +845,121 @@ struct FwdArgs {
 constexpr int FWD_WAVES = 4;
 constexpr int FWD_THREADS = FWD_WAVES * 64;
 
-template <int NB>
+// One batch of a forward wave's operands: FWD_PREF words of its X rows (two 32-line steps
+// each) and, per step, the 16-byte pieces of its two W row tiles.
+constexpr int FWD_PREF = 4;
+struct FwdBatch {
+  uint64_t word[FWD_PREF];
+  v4i A0[FWD_PREF][2], A1[FWD_PREF][2];
+};
+__device__ __forceinline__ void fwd_issue(const FwdArgs &a, __amdgpu_buffer_rsrc_t wrs,
+                                          __amdgpu_buffer_rsrc_t xrs, uint32_t aoff0,
+                                          uint32_t aoff1, uint32_t boff, uint32_t kb0,
+                                          uint32_t kstride, uint32_t kw, FwdBatch &b) {
+#pragma unroll
+  for (int u = 0; u < FWD_PREF; ++u) {
+    const uint32_t kb1 = kb0 + u * kstride;
+    const uint32_t kb = kb1 < kw ? kb1 : kb0;            // past the end: word kb0 again
+    b.word[u] = load8(xrs, boff, kb * a.Rp * 8);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      b.A0[u][h] = load16(wrs, aoff0, (2 * kb + h) * a.Dp * 32);
+      b.A1[u][h] = load16(wrs, aoff1, (2 * kb + h) * a.Dp * 32);
+    }
+  }
+}
+__device__ __forceinline__ void fwd_consume(const FwdBatch &b, uint32_t kb0, uint32_t kstride,
+                                            uint32_t kw, int g, v16i &acc0, v16i &acc1) {
+#pragma unroll
+  for (int u = 0; u < FWD_PREF; ++u) {
+    if (kb0 + u * kstride >= kw) break;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const v4i x = signs16(uint32_t(b.word[u] >> (32 * h + 16 * g)) & 0xFFFFu);
+      acc0 = mfma_i8(b.A0[u][h], x, acc0);
+      acc1 = mfma_i8(b.A1[u][h], x, acc1);
+    }
+  }
+}
+
+// A block's four waves: WPT waves per 64 x 32 tile, each taking every WPT-th word of X
+// (the contraction split over the waves for more waves in flight), 4 / WPT row tiles.
+// The split partial tiles meet in LDS.
+template <int WPT>
+struct FwdLds {
+  int32_t red[WPT > 1 ? FWD_WAVES : 1][2][16][64];
+};
+template <int WPT>
 __global__ __launch_bounds__(FWD_THREADS) void k_mfma_fwd(FwdArgs a) {
+  constexpr int TPB = FWD_WAVES / WPT;                 // row tiles per block
+  __shared__ FwdLds<WPT> sm;
   const int lane = threadIdx.x & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const uint32_t rb = fdiv(blockIdx.x, a.divDb), db = blockIdx.x - rb * a.dblocks;
-  const uint32_t d0 = db * 64, r0 = (rb * FWD_WAVES + wave) * 32;
-  if (r0 >= a.R) return;                               // wave-uniform: no barrier follows
+  const uint32_t tile = wave / WPT, part = wave - tile * WPT;
+  const uint32_t d0 = db * 64, r0 = (rb * TPB + tile) * 32;
+  const bool live = r0 < a.R;                          // wave-uniform
   const __amdgpu_buffer_rsrc_t wrs = buffer_of(a.wb, a.wb_bytes);
   const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xr, a.xr_bytes);
   // src0 rows d0 + i and d0 + 32 + i (always inside Dp), bytes 16 g .. 16 g + 15 of a step.
-  const uint32_t aoff0 = (d0 + uint32_t(i)) * a.Kp + 16 * g, aoff1 = aoff0 + 32 * a.Kp;
+  const uint32_t aoff0 = (d0 + uint32_t(i)) * 32 + 16 * g, aoff1 = aoff0 + 32 * 32;
   const uint32_t boff = (r0 + uint32_t(i)) * 8;        // word (kb, r0 + i) at kb * Rp * 8
-  const uint32_t steps = a.Kp / 32;                    // Kp is a multiple of 64
+  const uint32_t kw = a.Kp / 64;                       // X words per row
+  constexpr uint32_t kstride = WPT;
   v16i acc0 = {0}, acc1 = {0};
-  for (uint32_t s0 = 0; s0 < steps; s0 += 2 * NB) {
-    // NB words of X (two steps each) and their 4 NB byte pieces of W, all issued before
-    // the first product.
-    uint64_t xw[NB];
-    v4i A0[2 * NB], A1[2 * NB];
-#pragma unroll
-    for (int u = 0; u < NB; ++u) {
-      const uint32_t st = s0 + 2 * u;
-      const bool live = st < steps;
-      xw[u] = live ? __builtin_bit_cast(uint64_t, load8(xrs, boff, (st / 2) * a.Rp * 8)) : 0ull;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        A0[2 * u + h] = load16(wrs, live ? aoff0 : BUF_NONE, (st + h) * 32);
-        A1[2 * u + h] = load16(wrs, live ? aoff1 : BUF_NONE, (st + h) * 32);
-      }
+  if (live && part < kw) {
+    // Double-buffered: batch i + 1's loads issue before batch i's products.
+    FwdBatch b0, b1;
+    uint32_t kb0 = part;
+    const uint32_t step = FWD_PREF * kstride;
+    fwd_issue(a, wrs, xrs, aoff0, aoff1, boff, kb0, kstride, kw, b0);
+    for (;;) {
+      if (kb0 + step < kw) fwd_issue(a, wrs, xrs, aoff0, aoff1, boff, kb0 + step, kstride, kw, b1);
+      __builtin_amdgcn_sched_barrier(0);
+      fwd_consume(b0, kb0, kstride, kw, g, acc0, acc1);
+      kb0 += step;
+      if (kb0 >= kw) break;
+      if (kb0 + step < kw) fwd_issue(a, wrs, xrs, aoff0, aoff1, boff, kb0 + step, kstride, kw, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      fwd_consume(b1, kb0, kstride, kw, g, acc0, acc1);
+      kb0 += step;
+      if (kb0 >= kw) break;
     }
-    __builtin_amdgcn_sched_barrier(0);
+  }
+  uint32_t vlo = 0, vhi = 16;                          // accumulator registers this wave ends
+  if constexpr (WPT > 1) {
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
+    for (int v = 0; v < 16; ++v) {
+      sm.red[wave][0][v][lane] = acc0[v];
+      sm.red[wave][1][v][lane] = acc1[v];
+    }
+    __syncthreads();
+    // Part p of the tile sums registers [16 p / WPT, 16 (p + 1) / WPT) over the parts.
+    vlo = 16 * part / WPT;
+    vhi = 16 * (part + 1) / WPT;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const v4i b = signs16(uint32_t(xw[u] >> (32 * h + 16 * g)) & 0xFFFFu);
-        acc0 = mfma_i8(A0[2 * u + h], b, acc0);
-        acc1 = mfma_i8(A1[2 * u + h], b, acc1);
+    for (int v = 0; v < 16; ++v) {
+      if (uint32_t(v) < vlo || uint32_t(v) >= vhi) continue;
+      int s0 = 0, s1 = 0;
+#pragma unroll
+      for (int q = 0; q < WPT; ++q) {
+        s0 += sm.red[tile * WPT + q][0][v][lane];
+        s1 += sm.red[tile * WPT + q][1][v][lane];
       }
+      acc0[v] = s0;
+      acc1[v] = s1;
     }
   }
   const uint32_t r = r0 + uint32_t(i);
-  if (r >= a.R) return;
+  if (!live || r >= a.R) return;
   const uint32_t n = fdiv(r, a.divP), p = r - n * a.P;
   const size_t base = size_t(n) * a.D * a.P + p;
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
+      if (uint32_t(v) < vlo || uint32_t(v) >= vhi) continue;
       const uint32_t d = d0 + 32 * t + uint32_t(acc_row(v, g));
       if (d >= a.D) continue;
       const int I = t ? acc1[v] : acc0[v];
@@ -1129,8 +1194,15 @@ int launch_forward_gemm(const Layer &L, const int8_t *wrows, int64_t Dp, int64_t
   a.wb_bytes = uint32_t(Dp * Kp);
   a.xr_bytes = uint32_t((Kp / 64) * L.Wr * 64 * 8);
   a.divP = make_fastdiv(uint32_t(L.P)); a.divDb = make_fastdiv(a.dblocks);
-  const uint32_t rblocks = uint32_t((L.R + 32 * FWD_WAVES - 1) / (32 * FWD_WAVES));
-  hipLaunchKernelGGL(k_mfma_fwd<4>, dim3(a.dblocks * rblocks), dim3(FWD_THREADS), 0, s, a);
+  // Row tiles per block: four (one wave each, the contraction whole) when the grid still
+  // has four waves per SIMD that way, else fewer with the contraction split over the waves.
+  const int64_t tiles = ((L.R + 31) / 32) * a.dblocks;
+  const int wpt = tiles >= 4096 ? 1 : tiles >= 1024 ? 2 : 4;
+  const uint32_t tpb = uint32_t(FWD_WAVES / wpt);
+  const dim3 grid(a.dblocks * uint32_t((L.R + 32 * tpb - 1) / (32 * tpb)));
+  if (wpt == 1) hipLaunchKernelGGL(k_mfma_fwd<1>, grid, dim3(FWD_THREADS), 0, s, a);
+  else if (wpt == 2) hipLaunchKernelGGL(k_mfma_fwd<2>, grid, dim3(FWD_THREADS), 0, s, a);
+  else hipLaunchKernelGGL(k_mfma_fwd<4>, grid, dim3(FWD_THREADS), 0, s, a);
   return last_launch_status();
 }
 

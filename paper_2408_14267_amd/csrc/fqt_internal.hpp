@@ -125,7 +125,8 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
 // line 64 kb + b of row r; lines past K are 0).
 int launch_transpose_bits(const uint64_t *src, int64_t Wr, int64_t K, uint64_t *dst,
                           hipStream_t s);
-// sign(W) as +-1 bytes [Dp][Kp] in W's own [D][C*kh*kw] order, 0 past D and past K.
+// sign(W) as +-1 bytes in 32-line chunks [Kp/32][Dp][32], lines in W's own [D][C*kh*kw]
+// order, 0 past D and past K.
 int launch_pack_w_rows(const void *W, const Layer &L, int64_t Dp, int64_t Kp, int8_t *dst,
                        hipStream_t s);
 // Y[n][d][p] = gamma[d] * sum_k sign(X_u)[r][k] sign(W)[d][k] from the two packed operands.

@@ -226,12 +226,14 @@ __global__ __launch_bounds__(THREADS) void k_transpose_bits(const uint64_t *__re
   dst[size_t(kb) * Wr * 64 + size_t(w) * 64 + lane] = x;
 }
 
-// sign(W) rows as +-1 bytes, 16 per thread: row d, bytes [16 q, 16 q + 16) of Kp.
+// sign(W) as +-1 bytes in 32-line chunks, chunk-major: byte (d, k) at
+// ((k / 32) * Dp + d) * 32 + k % 32, so that the 32-byte pieces of consecutive channels
+// are adjacent.  16 bytes per thread: channel d, lines [16 q, 16 q + 16).
 template <int DT>
 __global__ __launch_bounds__(THREADS) void k_pack_w_rows(const void *__restrict__ w, uint32_t D,
                                                          uint32_t K, uint32_t Kp, uint32_t Dp,
                                                          int8_t *__restrict__ dst) {
-  const uint32_t qpr = Kp / 16;                          // 16-byte pieces per row
+  const uint32_t qpr = Kp / 16;                          // 16-byte pieces per channel
   const uint32_t e = blockIdx.x * THREADS + threadIdx.x;
   if (e >= Dp * qpr) return;
   const uint32_t d = e / qpr, k0 = (e - d * qpr) * 16;
@@ -243,7 +245,8 @@ __global__ __launch_bounds__(THREADS) void k_pack_w_rows(const void *__restrict_
     if (d < D && k < K) b = load_elem<DT>(w, int64_t(d) * K + k) > 0.0f ? 0x01u : 0xFFu;
     word[j >> 2] |= b << (8 * (j & 3));
   }
-  *reinterpret_cast<uint4 *>(dst + size_t(d) * Kp + k0) = make_uint4(word[0], word[1], word[2], word[3]);
+  const size_t o = (size_t(k0 / 32) * Dp + d) * 32 + k0 % 32;
+  *reinterpret_cast<uint4 *>(dst + o) = make_uint4(word[0], word[1], word[2], word[3]);
 }
 
 }  // namespace
