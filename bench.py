@@ -33,12 +33,12 @@ MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
 # measured on (TRAFFIC_DIGEST: sha256 over the names and contents of every file in csrc/).
 FETCH_SCALE = 262144.0 / 131086.7
 WRITE_SCALE = 1.0
-TRAFFIC_DIGEST = "aed837c6084925b6440cdfb5aa3622f86cec7f089bc29278bc1e7f0c688a991d"
+TRAFFIC_DIGEST = "fe2d073344a81e81fa79f078e939b83d8cfd675efd29148f37aff8c59773df03"
 TRAFFIC = {
     # entry: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch of its kernels
-    "gemm_dx": (2537.5, 8192.0),
-    "pack_x": (4143.1, 2304.0),
-    "pack_w": (1178.5, 585.0),
+    "gemm_dx": (2538.0, 8192.0),
+    "pack_x": (4143.3, 2304.0),
+    "pack_w": (1179.5, 585.0),
 }
 
 
