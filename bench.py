@@ -71,11 +71,13 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="bound on the CPU oracle sample (seconds of work)")
     p.add_argument("--no-graph", action="store_true", help="time eager launches only")
-    p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward"),
+    p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward",
+                                       "table5"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
-                        "layer backwards, the dW binary GEMM sweep, or the binary forward of "
-                        "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer "
-                        "(one JSON line each)")
+                        "layer backwards, the dW binary GEMM sweep, the binary forward of "
+                        "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer, or "
+                        "average-1-bit against 1-bit products at the sizes of the paper's "
+                        "Table 5 (one JSON line each)")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="first run a plain device copy of this many MiB (three times), so that "
                         "a counter run can scale FETCH_SIZE / WRITE_SIZE by a known byte count")
@@ -130,6 +132,47 @@ def suite(name, reps=10):
         e1.record(st)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k
+
+    if name == "table5":
+        # The paper's Table 5 sizes (m, k, n): a gradient of m columns over a k-deep contraction
+        # times k x n signs (reading of its unlabeled rows: m is the pruned side).  Average
+        # 1-bit: b = 4 codes of the m / 4 columns top-k keeps; 1-bit: b = 1 codes of all m, no
+        # pruning.  Both run the dW product entry; only the product is timed.  Then the same
+        # shapes scaled by 8 in every dimension, where the product is no longer latency-bound.
+        paper = {(512, 512, 512): (8.40, 8.01), (512, 512, 1024): (15.92, 14.54),
+                 (1024, 512, 512): (16.61, 15.91), (1024, 512, 1024): (31.03, 29.79),
+                 (2048, 512, 512): (32.22, 29.92), (2048, 512, 1024): (61.33, 59.94)}
+        scaled = {(8 * m, 8 * k, 8 * n): (None, None) for (m, k, n) in paper}
+        for (m, k, n), (p_avg, p_one) in list(paper.items()) + list(scaled.items()):
+            L = LayerShape(name="mm", kind="linear", N=k, C=n, D=m)
+            desc = fqt.layer_desc(L)
+            dY = _gen(torch, (k, m), torch.float32, dev)
+            X = _gen(torch, (k, n), torch.float32, dev)
+            xs = torch.empty(((k + 63) // 64) * n, dtype=torch.int64, device=dev)
+            fqt.fqt_pack_input_signs(desc, X, xs, st)
+            dW = torch.empty((m, n), dtype=torch.float32, device=dev)
+            out = {"suite": name, "m_k_n": [m, k, n]}
+            for tag, cfg in (("avg1bit", fqt.quant_cfg(4, fqt.FQT_AGP_TOPK, 0, 0, 0)),
+                             ("1bit", fqt.quant_cfg(1, fqt.FQT_AGP_OFF, 0, 0, 0))):
+                q = fqt.QGrad(desc, cfg, device=dev)
+                qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
+                dws = fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW, device=dev)
+                fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st)
+                gd = lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, dws, None, st)
+                for _ in range(3):
+                    gd()
+                out[tag + "_ms"] = round(timed(gd, 50), 5)
+                out[tag + "_kept"] = int(q.pcq_count.item())
+            out["ratio"] = round(out["avg1bit_ms"] / out["1bit_ms"], 3)
+            if p_avg is not None:
+                out["paper_hygon_ms"] = [p_avg, p_one]
+                out["paper_ratio"] = round(p_avg / p_one, 3)
+            else:
+                out["sizes"] = "the paper's sizes x 8 in each dimension"
+            print(json.dumps(out), flush=True)
+            del dY, X, xs, dW, q, qws, dws
+            torch.cuda.empty_cache()
+        return
 
     if name == "forward":
         for wname in (WORKLOAD, "resnet18_32px", "vgg16_224_bf16"):
