@@ -258,48 +258,72 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   }
 }
 
-// Large dW outputs in one split (DIRECT): each wave holds a 64 x 64 block of the output,
-// 2 x 2 MFMA tiles, so every code chunk it loads feeds two column tiles and every sign
-// piece it expands two row tiles.  A block's four waves take four adjacent 64-column
-// blocks of the same 64 slots (the code rows come from L2 once).  Grid: ceil(D/64) slot
-// blocks x ceil(K/256) column groups, slots slowest.  Double-buffered like the split form.
-constexpr int DWB_PREF = 2;
+// Large dW outputs in one split (DIRECT): each wave holds a (32 DWB_RT) x (32 DWB_CT)
+// block of the output in DWB_RT x DWB_CT MFMA tiles, and a block's four waves take four
+// adjacent column blocks of the same slots (the code rows come from L2 once).  Grid:
+// ceil(D / (32 DWB_RT)) slot blocks x ceil(K / (128 DWB_CT)) column groups, slots slowest.
+// Here the X signs enter the MFMA as 0/1 bytes b (three VALU operations per four signs,
+// shared by the row tiles) instead of +-1, and the signed sum comes back per output as
+// sum q s = 2 sum q b - sum q (s = 2b - 1; b = 0 on the zero tail of the last word, where
+// q = 0 too).  The code sums sum q of the rows are taken from the A fragments with
+// v_dot4_u32_u8 (four per fragment, shared by the column tiles).  For b = 8 the codes
+// enter as q - 128: sum q b = acc + 128 T.  Double-buffered like the split form.
+constexpr int DWB_RT = 2, DWB_CT = 4, DWB_STAGES = 4;
 struct DwBigBatch {
-  uint64_t word[DWB_PREF][2];
-  v4i A[DWB_PREF][2][2];                  // [word][half][row tile]
+  uint64_t word[DWB_CT];
+  v4i A[2][DWB_RT];                       // [half][row tile]
 };
 __device__ __forceinline__ void dwb_issue(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
-                                          __amdgpu_buffer_rsrc_t xrs, const uint32_t (&aoff)[2],
-                                          const uint32_t (&boff)[2], uint32_t c0, DwBigBatch &b) {
-  const uint32_t chunk_bytes = a.D * 32;
+                                          __amdgpu_buffer_rsrc_t xrs,
+                                          const uint32_t (&aoff)[DWB_RT],
+                                          const uint32_t (&boff)[DWB_CT], uint32_t c,
+                                          DwBigBatch &b) {
+  // Word offsets as scalars (kept out of any vector induction variable).
+  const uint32_t xs = __builtin_amdgcn_readfirstlane(c * a.K * 8);
+  const uint32_t cs0 = __builtin_amdgcn_readfirstlane(2 * c * a.D * 32);
+  const uint32_t cs1 = __builtin_amdgcn_readfirstlane((2 * c + 1) * a.D * 32);
 #pragma unroll
-  for (int u = 0; u < DWB_PREF; ++u) {
-    const uint32_t c = c0 + u < a.Wr ? c0 + u : c0;
+  for (int ct = 0; ct < DWB_CT; ++ct) b.word[ct] = load8(xrs, boff[ct], xs);
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct) b.word[u][ct] = load8(xrs, boff[ct], c * a.K * 8);
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) b.A[u][h][rt] = load16(crs, aoff[rt], (2 * c + h) * chunk_bytes);
+  for (int rt = 0; rt < DWB_RT; ++rt) {
+    b.A[0][rt] = load16(crs, aoff[rt], cs0);
+    b.A[1][rt] = load16(crs, aoff[rt], cs1);
   }
 }
+// Four sign bits of `half` from bit `off` (LSB first) as four 0/1 bytes: a nibble times
+// 0x00204081 puts bit m at bit 8m (the cross terms land on other bits, without carries)
+// and the mask keeps those.
+__device__ __forceinline__ int bits01x4(uint32_t half, uint32_t off) {
+  return int((__builtin_amdgcn_ubfe(half, off, 4) * 0x00204081u) & 0x01010101u);
+}
 template <bool B8>
-__device__ __forceinline__ void dwb_consume(const DwArgs &a, const DwBigBatch &b, uint32_t c0,
-                                            int g, v16i (&acc)[2][2], uint32_t (&tpart)[2]) {
+__device__ __forceinline__ void dwb_consume(const DwBigBatch &b, const uint32_t (&off)[4],
+                                            v16i (&acc)[DWB_RT][DWB_CT],
+                                            uint32_t (&tcnt)[DWB_CT], uint32_t (&qsum)[DWB_RT]) {
 #pragma unroll
-  for (int u = 0; u < DWB_PREF; ++u) {
-    if (c0 + u >= a.Wr) break;
+  for (int ct = 0; ct < DWB_CT; ++ct)
+    tcnt[ct] += __popc(uint32_t(b.word[ct])) + __popc(uint32_t(b.word[ct] >> 32));
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+  for (int h = 0; h < 2; ++h) {
+    // For b = 8 the sums are taken of the biased bytes q - 128 (signed), the only form
+    // kept in registers; the epilogue adds 128 per position back.
+    v4i A[DWB_RT];
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const uint32_t bits = uint32_t(b.word[u][ct] >> (32 * h + 16 * g)) & 0xFFFFu;
-        tpart[ct] += __popc(bits);
-        const v4i B = signs16(bits);
+    for (int rt = 0; rt < DWB_RT; ++rt) {
+      A[rt] = B8 ? bias128(b.A[h][rt]) : b.A[h][rt];
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-          acc[rt][ct] = mfma_i8(B8 ? bias128(b.A[u][h][rt]) : b.A[u][h][rt], B, acc[rt][ct]);
-      }
+      for (int k = 0; k < 4; ++k)
+        qsum[rt] = B8 ? uint32_t(__builtin_amdgcn_sdot4(A[rt][k], 0x01010101, int(qsum[rt]), false))
+                      : __builtin_amdgcn_udot4(uint32_t(A[rt][k]), 0x01010101u, qsum[rt], false);
+    }
+#pragma unroll
+    for (int ct = 0; ct < DWB_CT; ++ct) {
+      const uint32_t half = uint32_t(b.word[ct] >> (32 * h));
+      const v4i B = v4i{bits01x4(half, off[0]), bits01x4(half, off[1]), bits01x4(half, off[2]),
+                        bits01x4(half, off[3])};
+#pragma unroll
+      for (int rt = 0; rt < DWB_RT; ++rt) acc[rt][ct] = mfma_i8(A[rt], B, acc[rt][ct]);
+    }
   }
 }
 template <bool B8>
@@ -308,59 +332,99 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
-  const uint32_t kgroups = (a.K + 255) / 256;
+  const uint32_t kgroups = (a.K + DW_WAVES * 32 * DWB_CT - 1) / (DW_WAVES * 32 * DWB_CT);
   const uint32_t rb = bid / kgroups;
-  const uint32_t j0 = rb * 64, k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * 64;
+  const uint32_t j0 = rb * (32 * DWB_RT);
+  const uint32_t k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * (32 * DWB_CT);
   if (k0 >= a.K) return;
-  v16i acc[2][2];
+  v16i acc[DWB_RT][DWB_CT];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt)
+  for (int rt = 0; rt < DWB_RT; ++rt)
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = v16i{0};
-  uint32_t tpart[2] = {0u, 0u};
-  if (int(j0) < count) {
+    for (int ct = 0; ct < DWB_CT; ++ct) acc[rt][ct] = v16i{0};
+  uint32_t tcnt[DWB_CT], qsum[DWB_RT];
+#pragma unroll
+  for (int ct = 0; ct < DWB_CT; ++ct) tcnt[ct] = 0u;
+#pragma unroll
+  for (int rt = 0; rt < DWB_RT; ++rt) qsum[rt] = 0u;
+  if (int(j0) < count && a.Wr > 0) {
     const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
     const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
-    uint32_t aoff[2], boff[2];
+    uint32_t aoff[DWB_RT], boff[DWB_CT], off[4];
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    for (int rt = 0; rt < DWB_RT; ++rt) {
       const uint32_t j = j0 + 32 * rt + i;
       aoff[rt] = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
     }
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct) {
+    for (int ct = 0; ct < DWB_CT; ++ct) {
       const uint32_t kc = k0 + 32 * ct + i;
       boff[ct] = kc < a.K ? kc * 8 : BUF_NONE;
     }
-    DwBigBatch b0, b1;
-    uint32_t c0 = 0;
-    dwb_issue(a, crs, xrs, aoff, boff, c0, b0);
-    for (;;) {
-      if (c0 + DWB_PREF < a.Wr) dwb_issue(a, crs, xrs, aoff, boff, c0 + DWB_PREF, b1);
-      __builtin_amdgcn_sched_barrier(0);
-      dwb_consume<B8>(a, b0, c0, g, acc, tpart);
-      c0 += DWB_PREF;
-      if (c0 >= a.Wr) break;
-      if (c0 + DWB_PREF < a.Wr) dwb_issue(a, crs, xrs, aoff, boff, c0 + DWB_PREF, b0);
-      __builtin_amdgcn_sched_barrier(0);
-      dwb_consume<B8>(a, b1, c0, g, acc, tpart);
-      c0 += DWB_PREF;
-      if (c0 >= a.Wr) break;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) off[k] = uint32_t(16 * g + 4 * k);
+    // A ring of DWB_STAGES words: word c + DWB_STAGES is requested as soon as word c has
+    // been used, so DWB_STAGES - 1 words are in flight during each word's products.  Every
+    // step issues the same loads (a word past the end re-reads the last one), so the
+    // waits count exactly.
+    constexpr int ST = DWB_STAGES;
+    DwBigBatch bs[ST];
+    const uint32_t last = a.Wr - 1;
+#pragma unroll
+    for (int u = 0; u < ST; ++u) dwb_issue(a, crs, xrs, aoff, boff, min(uint32_t(u), last), bs[u]);
+    for (uint32_t c = 0; c < a.Wr; c += ST) {
+#pragma unroll
+      for (int u = 0; u < ST; ++u) {
+        if (c + u >= a.Wr) break;
+        dwb_consume<B8>(bs[u], off, acc, tcnt, qsum);
+        __builtin_amdgcn_sched_barrier(0);
+        dwb_issue(a, crs, xrs, aoff, boff, min(c + u + ST, last), bs[u]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
+  // Lane i (and i + 32) holds half of the code sum of row i of each row tile; the
+  // accumulator rows of a lane are acc_row(v, g), fetched from their lanes.
 #pragma unroll
-  for (int ct = 0; ct < 2; ++ct) {
-    const uint32_t T = tpart[ct] + lane_xor<32>(tpart[ct]);
+  for (int rt = 0; rt < DWB_RT; ++rt) {
+    // Sum of the codes of row i of the tile (b = 8: of q - 128 over all Rp positions).
+    const int qrow = int(qsum[rt] + lane_xor<32>(qsum[rt])) + (B8 ? 128 * int(a.Rp) : 0);
+    int qv[16];
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-      dw_write_direct<B8>(a, j0 + 32 * rt, k0 + 32 * ct + i, count, acc[rt][ct], int(T));
+    for (int v = 0; v < 16; ++v) qv[v] = __shfl(qrow, acc_row(v, g));
+    const uint32_t jt = j0 + 32 * rt;
+#pragma unroll
+    for (int ct = 0; ct < DWB_CT; ++ct) {
+      const uint32_t kc = k0 + 32 * ct + i;
+      if (kc >= a.K) continue;
+      const int T = int(tcnt[ct]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const uint32_t j = jt + uint32_t(acc_row(v, g));
+        if (j >= a.D) continue;
+        const size_t d = size_t(a.kept[j]);
+        int I = 0;
+        float out = 0.0f;
+        if (int(j) < count) {
+          const float2 sz = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[d], a.offset[d]);
+          I = 2 * (acc[rt][ct][v] + (B8 ? 128 * T : 0)) - qv[v];
+          out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
+        }
+        a.dW[d * a.K + kc] = out;
+        if (a.I_out) a.I_out[d * a.K + kc] = I;
+      }
+    }
   }
 }
-// Blocks of the 64 x 64-per-wave form.
-uint32_t dw_big_blocks(uint32_t D, uint32_t K) { return ((D + 63) / 64) * ((K + 255) / 256); }
+// Blocks of the big form.
+uint32_t dw_big_blocks(uint32_t D, uint32_t K) {
+  return ((D + 32 * DWB_RT - 1) / (32 * DWB_RT)) *
+         ((K + DW_WAVES * 32 * DWB_CT - 1) / (DW_WAVES * 32 * DWB_CT));
+}
 
+// Two waves per SIMD: the accumulators and the word ring fit 256 registers.
 template <bool B8>
-__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_big(DwArgs a) {
+__global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_mfma_dw_big(DwArgs a) {
   dw_big_body<B8>(a, blockIdx.x);
 }
 

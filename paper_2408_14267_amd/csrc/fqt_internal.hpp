@@ -161,15 +161,14 @@ __device__ __forceinline__ Ctr4 philox4x32_10(Ctr4 c, uint32_t k0, uint32_t k1) 
       k0 += 0x9E3779B9u;
       k1 += 0xBB67AE85u;
     }
-    const uint32_t lo0 = 0xD2511F53u * c.v[0];
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c.v[0]);
-    const uint32_t lo1 = 0xCD9E8D57u * c.v[2];
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.v[2]);
+    // One 32 x 32 -> 64-bit product gives both halves.
+    const uint64_t p0 = uint64_t(0xD2511F53u) * c.v[0];
+    const uint64_t p1 = uint64_t(0xCD9E8D57u) * c.v[2];
     Ctr4 n;
-    n.v[0] = hi1 ^ c.v[1] ^ k0;
-    n.v[1] = lo1;
-    n.v[2] = hi0 ^ c.v[3] ^ k1;
-    n.v[3] = lo0;
+    n.v[0] = uint32_t(p1 >> 32) ^ c.v[1] ^ k0;
+    n.v[1] = uint32_t(p1);
+    n.v[2] = uint32_t(p0 >> 32) ^ c.v[3] ^ k1;
+    n.v[3] = uint32_t(p0);
     c = n;
   }
   return c;

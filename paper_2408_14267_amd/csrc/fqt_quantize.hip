@@ -76,6 +76,7 @@ __device__ __forceinline__ int wave_max(int v) { return wave_max_all(v); }
 struct StatsGeom {
   TileGeom g;
   uint32_t nrt, SL, rs;
+  uint32_t chan_fast;   // grid x walks the channel tiles, y the row blocks
 };
 
 // Load the quads of tile rows [r0, r0 + 64) x channels [d0, d0 + 64) into x (element 0 of
@@ -111,7 +112,7 @@ __device__ __forceinline__ int2 merged_key(uint2 u) {
 // in the tile.
 // With mks / mkc set (merged keys), the sample and channel keys are combined into them
 // with atomics instead of being stored as partials: channel keys into replica
-// blockIdx.x % MKEY_REP, sample keys into replica blockIdx.y % MKEY_REP.
+// (row block) % MKEY_REP, sample keys into replica (channel tile) % MKEY_REP.
 template <int MODE, int DT>
 __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, StatsGeom sg,
                                                    int2 *__restrict__ part_c,
@@ -124,8 +125,10 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
   const TileGeom &g = sg.g;
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
-  const uint32_t d0 = blockIdx.y * TILE;
-  const uint32_t rt0 = blockIdx.x * sg.rs;
+  const uint32_t bxr = sg.chan_fast ? blockIdx.y : blockIdx.x;   // row block
+  const uint32_t byc = sg.chan_fast ? blockIdx.x : blockIdx.y;   // channel tile
+  const uint32_t d0 = byc * TILE;
+  const uint32_t rt0 = bxr * sg.rs;
   int clo[TILE / WAVES], chi[TILE / WAVES];      // channel rows wave + WAVES * i
 #pragma unroll
   for (int i = 0; i < TILE / WAVES; ++i) {
@@ -192,10 +195,10 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
       // sample n_first + k.
       const uint32_t n_first = fdiv(r0, g.divP);
       const uint32_t slot = row_ok ? fdiv(r0 + lane, g.divP) - n_first : 0xFFFFFFFFu;
-      int2 *ps = part_s + (size_t(blockIdx.y) * sg.nrt + rt) * sg.SL;
+      int2 *ps = part_s + (size_t(byc) * sg.nrt + rt) * sg.SL;
       if (g.P == 1) {
         if (mks) {
-          if (row_ok) merge_key(mks + (blockIdx.y % MKEY_REP) * MKEY_GROUPS + r0 + lane, lo, hi);
+          if (row_ok) merge_key(mks + (byc % MKEY_REP) * MKEY_GROUPS + r0 + lane, lo, hi);
         } else {
           ps[lane] = row_ok ? make_int2(lo, hi) : make_int2(INT_MAX, INT_MIN);
         }
@@ -206,7 +209,7 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
           if (mks) {
             // A slot holds data only for a sample that the tile meets (then n < N).
             if (lane == 0 && l <= h)
-              merge_key(mks + (blockIdx.y % MKEY_REP) * MKEY_GROUPS + n_first + k, l, h);
+              merge_key(mks + (byc % MKEY_REP) * MKEY_GROUPS + n_first + k, l, h);
           } else if (lane == 0) {
             ps[k] = make_int2(l, h);
           }
@@ -224,9 +227,9 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
   __syncthreads();
   if (wave == 1 && d0 + lane < g.D) {
     if (mkc)
-      merge_key(mkc + (blockIdx.x % MKEY_REP) * MKEY_GROUPS + d0 + lane, cpart[lane].x,
+      merge_key(mkc + (bxr % MKEY_REP) * MKEY_GROUPS + d0 + lane, cpart[lane].x,
                 cpart[lane].y);
-    else part_c[size_t(blockIdx.x) * g.D + d0 + lane] = cpart[lane];
+    else part_c[size_t(bxr) * g.D + d0 + lane] = cpart[lane];
   }
 }
 
@@ -998,14 +1001,29 @@ constexpr size_t select_signs_static_lds(int GP) {
 
 // ----------------------------------------------------------------------------- quantize + pack
 
+// The 24-bit uniform of a Philox word as the float u24 * 2^-24 (exact).
+__device__ __forceinline__ float unit24(uint32_t u) {
+  return __fmul_rn(static_cast<float>(u >> 8), 5.9604644775390625e-8f);
+}
+
 // b-bit stochastic rounding code of x (Section 3.2): v = clamp((x - Z) * inv, 0, B),
-// q = floor(v) + [u24 < frac(v) * 2^24].  inv = 0 (R = 0) gives q = 0.
-__device__ __forceinline__ uint32_t sr_code(float x, float z, float inv, float Bf, uint32_t u) {
+// q = floor(v) + [u < v - floor(v)] for the uniform u = u24 * 2^-24 (the same test as
+// u24 < frac(v) * 2^24: both sides scale by a power of two).  inv = 0 (R = 0) gives q = 0.
+__device__ __forceinline__ uint32_t sr_code(float x, float z, float inv, float Bf, float u) {
   float v = __fmul_rn(__fsub_rn(x, z), inv);
   v = fminf(fmaxf(v, 0.0f), Bf);
   const float fl = floorf(v);
-  const float fr = v - fl;
-  return static_cast<uint32_t>(fl) + (static_cast<float>(u >> 8) < fr * 16777216.0f ? 1u : 0u);
+  return static_cast<uint32_t>(fl) + (u < __fsub_rn(v, fl) ? 1u : 0u);
+}
+// b = 1: v is clamped to [0, 1], so q = [u < v]; as u < 1, the test on the unclamped
+// product gives the same bit (true for v >= 1, false for v <= 0 and for NaN).
+__device__ __forceinline__ uint32_t sr_bit(float x, float z, float inv, float u) {
+  return u < __fmul_rn(__fsub_rn(x, z), inv) ? 1u : 0u;
+}
+template <bool ONE>
+__device__ __forceinline__ uint32_t sr_any(float x, const GroupParam &p, float Bf, float u) {
+  const uint32_t c = ONE ? sr_bit(x, p.z, p.inv, u) : sr_code(x, p.z, p.inv, Bf, u);
+  return p.rank >= 0 ? c : 0u;
 }
 
 struct QPackArgs {
@@ -1021,7 +1039,49 @@ struct QPackArgs {
   int bits;
   uint64_t seed;
   uint32_t step, layer;
+  uint32_t eager;       // read every quad of the layer before the parameters
+  uint32_t chan_fast;   // grid x walks the channel tiles (rows of dY read as long runs)
 };
+
+// Codes of a thread's quads into the LDS tiles.  The four codes of a quad share one
+// Philox block (element e takes word e % 4; both encodings use the element's word); the
+// encoding whose lines run along the quad gets them as one 32-bit store.
+template <int MODE, bool ONE>
+__device__ __forceinline__ void qpack_quads(const QPackArgs &a, const TileGeom &g, uint32_t d0,
+                                            uint32_t r0, int t, const float (&x)[QUADS][4],
+                                            const bool (&need)[QUADS], float Bf,
+                                            const GroupParam *spar, const GroupParam *cpar,
+                                            uint8_t (*cs)[PITCH], uint8_t (*cc)[PITCH]) {
+#pragma unroll
+  for (int q = 0; q < QUADS; ++q) {
+    int dd, rr;
+    quad_coord<MODE>(t, q, 0, dd, rr);
+    uint32_t qs[4] = {0, 0, 0, 0}, qc[4] = {0, 0, 0, 0};
+    if (need[q]) {
+      const uint32_t e = elem_index(g, d0 + dd, r0 + rr);
+      const Ctr4 u = philox_block(e >> 2, STREAM_ELEM, a.seed, a.step, a.layer);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int dk = MODE == TILE_CHAN ? dd + k : dd;
+        const int rk = MODE == TILE_PIX ? rr + k : rr;
+        const float uf = unit24(u.v[k]);
+        qs[k] = sr_any<ONE>(x[q][k], spar[rk], Bf, uf);
+        qc[k] = sr_any<ONE>(x[q][k], cpar[dk], Bf, uf);
+      }
+    }
+    const uint32_t ws = qs[0] | (qs[1] << 8) | (qs[2] << 16) | (qs[3] << 24);
+    const uint32_t wc = qc[0] | (qc[1] << 8) | (qc[2] << 16) | (qc[3] << 24);
+    if (MODE == TILE_CHAN) {            // row rr, channels dd .. dd + 3
+      *reinterpret_cast<uint32_t *>(&cs[rr][dd]) = ws;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cc[dd + k][rr] = uint8_t(qc[k]);
+    } else {                            // channel dd, rows rr .. rr + 3
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cs[rr + k][dd] = uint8_t(qs[k]);
+      *reinterpret_cast<uint32_t *>(&cc[dd][rr]) = wc;
+    }
+  }
+}
 
 template <int MODE, int DT>
 __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
@@ -1034,8 +1094,22 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const TileGeom &g = a.g;
-  const uint32_t r0 = blockIdx.x * TILE, d0 = blockIdx.y * TILE;
+  const uint32_t r0 = (a.chan_fast ? blockIdx.y : blockIdx.x) * TILE;
+  const uint32_t d0 = (a.chan_fast ? blockIdx.x : blockIdx.y) * TILE;
   const float Bf = float((1 << a.bits) - 1);
+
+  // Eager form (most elements kept): the dY loads issue before the group parameters
+  // arrive, so the two memory round trips overlap; otherwise only quads with a kept
+  // sample or channel are read, after the parameters.
+  float x[QUADS][4];
+  if (MODE != TILE_SCALAR && a.eager) {
+    for (int q = 0; q < QUADS; ++q) {
+      int dd, rr;
+      quad_coord<MODE>(t, q, 0, dd, rr);
+      const bool in = d0 + dd < g.D && r0 + rr < g.R;
+      load_quad<DT>(a.dy, in ? elem_index(g, d0 + dd, r0 + rr) : 0, x[q]);
+    }
+  }
 
   if (t < TILE) {
     const uint32_t r = r0 + t;
@@ -1059,7 +1133,6 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   __syncthreads();
 
   if (MODE != TILE_SCALAR) {
-    float x[QUADS][4];
     bool need[QUADS];
     for (int q = 0; q < QUADS; ++q) {
       int dd, rr;
@@ -1075,31 +1148,10 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
         }
       }
       need[q] = nd;
-      load_quad<DT>(a.dy, nd ? elem_index(g, d0 + dd, r0 + rr) : 0, x[q]);
+      if (!a.eager) load_quad<DT>(a.dy, nd ? elem_index(g, d0 + dd, r0 + rr) : 0, x[q]);
     }
-    for (int q = 0; q < QUADS; ++q) {
-      int dd, rr;
-      quad_coord<MODE>(t, q, 0, dd, rr);
-      uint32_t qs[4] = {0, 0, 0, 0}, qc[4] = {0, 0, 0, 0};
-      if (need[q]) {
-        const uint32_t e = elem_index(g, d0 + dd, r0 + rr);
-        const Ctr4 u = philox_block(e >> 2, STREAM_ELEM, a.seed, a.step, a.layer);
-        for (int k = 0; k < 4; ++k) {
-          const int dk = MODE == TILE_CHAN ? dd + k : dd;
-          const int rk = MODE == TILE_PIX ? rr + k : rr;
-          const float xv = x[q][k] + 0.0f;
-          const GroupParam ps = spar[rk], pc = cpar[dk];
-          if (ps.rank >= 0) qs[k] = sr_code(xv, ps.z, ps.inv, Bf, u.v[k]);
-          if (pc.rank >= 0) qc[k] = sr_code(xv, pc.z, pc.inv, Bf, u.v[k]);
-        }
-      }
-      for (int k = 0; k < 4; ++k) {
-        int dk, rk;
-        quad_coord<MODE>(t, q, k, dk, rk);
-        cs[rk][dk] = uint8_t(qs[k]);
-        cc[dk][rk] = uint8_t(qc[k]);
-      }
-    }
+    if (a.bits == 1) qpack_quads<MODE, true>(a, g, d0, r0, t, x, need, Bf, spar, cpar, cs, cc);
+    else qpack_quads<MODE, false>(a, g, d0, r0, t, x, need, Bf, spar, cpar, cs, cc);
   } else {
     for (int m = 0; m < 4 * QUADS; ++m) {
       int dd, rr;
@@ -1111,9 +1163,9 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
         const uint32_t e = elem_index(g, d, r);
         const float xv = load_elem<DT>(a.dy, e) + 0.0f;
         const Ctr4 u = philox_block(e >> 2, STREAM_ELEM, a.seed, a.step, a.layer);
-        const uint32_t uw = ctr_word(u, e & 3u);
-        if (ps.rank >= 0) qs = sr_code(xv, ps.z, ps.inv, Bf, uw);
-        if (pc.rank >= 0) qc = sr_code(xv, pc.z, pc.inv, Bf, uw);
+        const float uf = unit24(ctr_word(u, e & 3u));
+        qs = sr_any<false>(xv, ps, Bf, uf);
+        qc = sr_any<false>(xv, pc, Bf, uf);
       }
       cs[rr][dd] = uint8_t(qs);
       cc[dd][rr] = uint8_t(qc);
@@ -1204,10 +1256,13 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
                     const QuantWs &w, hipStream_t s, SignJob *signs) {
   TileGeom g{uint32_t(L.D), uint32_t(L.P), uint32_t(L.R), make_fastdiv(uint32_t(L.P))};
   const uint32_t nrt = uint32_t(L.Wr), ndt = uint32_t(L.Wd);
-  const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L)};
   const uint32_t nrb = uint32_t(stats_row_blocks(L));
-  const dim3 grid(nrb, ndt);
   const int mode = (L.P % 4 == 0) ? TILE_PIX : (L.P == 1 && L.D % 4 == 0) ? TILE_CHAN : TILE_SCALAR;
+  // With channels contiguous in dY (P = 1) the channel tiles go fastest, so the blocks in
+  // flight read whole rows of dY in order.
+  const uint32_t chan_fast = (mode == TILE_CHAN && nrb <= 65535) ? 1u : 0u;
+  const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L), chan_fast};
+  const dim3 grid = chan_fast ? dim3(ndt, nrb) : dim3(nrb, ndt);
   const int64_t gmax = L.N > L.D ? L.N : L.D;
   // Large maps with both group sets in one-workgroup selections: per-plane statistics
   // (part_c holds the N * D plane keys: it has D * stats_row_blocks >= D * N entries).
@@ -1334,13 +1389,19 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   }
   if (st != FQT_OK) return st;
 
-  const dim3 qgrid(nrt, ndt);            // one block per 64 x 64 tile
+  // One block per 64 x 64 tile.  With channels contiguous in dY (P = 1), the channel
+  // tiles go fastest, so the blocks in flight read whole rows of dY in order.
   QPackArgs qa;
+  qa.chan_fast = (mode == TILE_CHAN && nrt <= 65535) ? 1u : 0u;
+  const dim3 qgrid = qa.chan_fast ? dim3(ndt, nrt) : dim3(nrt, ndt);
   qa.dy = dY; qa.g = g; qa.sp = w.sp; qa.cp = w.cp;
   qa.psq = q.psq_planes; qa.pcq = q.pcq_planes;
   qa.psq_codes = q.psq_codes; qa.pcq_codes = q.pcq_codes;
   qa.Wd = uint32_t(L.Wd); qa.Wr = uint32_t(L.Wr);
   qa.bits = cfg.bits; qa.seed = cfg.seed; qa.step = cfg.step; qa.layer = cfg.layer_id;
+  // Kept fraction of the elements: 1 without AGP; with AGP about 1 - (1 - 1/b)^2 (G/b
+  // groups of each encoding kept), above 3/4 for b <= 2.
+  qa.eager = (cfg.agp_mode == FQT_AGP_OFF || cfg.bits <= 2) ? 1u : 0u;
   dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
       hipLaunchKernelGGL((k_qpack<TILE_PIX, DT>), qgrid, dim3(THREADS), 0, s, qa);
