@@ -258,34 +258,39 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   }
 }
 
-// Large dW outputs in one split (DIRECT): each wave holds a (32 DWB_RT) x (32 DWB_CT)
-// block of the output in DWB_RT x DWB_CT MFMA tiles, and a block's four waves take four
-// adjacent column blocks of the same slots (the code rows come from L2 once).  Grid:
-// ceil(D / (32 DWB_RT)) slot blocks x ceil(K / (128 DWB_CT)) column groups, slots slowest.
+// Large dW outputs in one split (DIRECT): each wave holds a (32 RT) x (32 CT) block of
+// the output in RT x CT MFMA tiles, and a block's four waves take four adjacent column
+// blocks of the same slots (the code rows come from L2 once).  Grid: ceil(D / (32 RT))
+// slot blocks x ceil(K / (128 CT)) column groups, slots slowest.
 // Here the X signs enter the MFMA as 0/1 bytes b (three VALU operations per four signs,
 // shared by the row tiles) instead of +-1, and the signed sum comes back per output as
 // sum q s = 2 sum q b - sum q (s = 2b - 1; b = 0 on the zero tail of the last word, where
 // q = 0 too).  The code sums sum q of the rows are taken from the A fragments with
 // v_dot4_u32_u8 (four per fragment, shared by the column tiles).  For b = 8 the codes
-// enter as q - 128: sum q b = acc + 128 T.  Double-buffered like the split form.
-constexpr int DWB_RT = 2, DWB_CT = 4, DWB_STAGES = 4;
+// enter as q - 128: sum q b = acc + 128 T.  The words of the contraction stream through a
+// ring of ST register batches.
+// Shapes (row tiles RT, column tiles CT, ring depth ST): long contractions take 2 x 4
+// tiles and a four-word ring at two waves per SIMD; short ones (a few words, where the
+// dW stores dominate) 2 x 2 tiles and two words at the occupancy the registers allow.
+constexpr int DWB_LONG_WORDS = 8;     // contractions of at least this many words: long form
+template <int RT, int CT>
 struct DwBigBatch {
-  uint64_t word[DWB_CT];
-  v4i A[2][DWB_RT];                       // [half][row tile]
+  uint64_t word[CT];
+  v4i A[2][RT];                           // [half][row tile]
 };
+template <int RT, int CT>
 __device__ __forceinline__ void dwb_issue(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
-                                          __amdgpu_buffer_rsrc_t xrs,
-                                          const uint32_t (&aoff)[DWB_RT],
-                                          const uint32_t (&boff)[DWB_CT], uint32_t c,
-                                          DwBigBatch &b) {
+                                          __amdgpu_buffer_rsrc_t xrs, const uint32_t (&aoff)[RT],
+                                          const uint32_t (&boff)[CT], uint32_t c,
+                                          DwBigBatch<RT, CT> &b) {
   // Word offsets as scalars (kept out of any vector induction variable).
   const uint32_t xs = __builtin_amdgcn_readfirstlane(c * a.K * 8);
   const uint32_t cs0 = __builtin_amdgcn_readfirstlane(2 * c * a.D * 32);
   const uint32_t cs1 = __builtin_amdgcn_readfirstlane((2 * c + 1) * a.D * 32);
 #pragma unroll
-  for (int ct = 0; ct < DWB_CT; ++ct) b.word[ct] = load8(xrs, boff[ct], xs);
+  for (int ct = 0; ct < CT; ++ct) b.word[ct] = load8(xrs, boff[ct], xs);
 #pragma unroll
-  for (int rt = 0; rt < DWB_RT; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     b.A[0][rt] = load16(crs, aoff[rt], cs0);
     b.A[1][rt] = load16(crs, aoff[rt], cs1);
   }
@@ -296,20 +301,20 @@ __device__ __forceinline__ void dwb_issue(const DwArgs &a, __amdgpu_buffer_rsrc_
 __device__ __forceinline__ int bits01x4(uint32_t half, uint32_t off) {
   return int((__builtin_amdgcn_ubfe(half, off, 4) * 0x00204081u) & 0x01010101u);
 }
-template <bool B8>
-__device__ __forceinline__ void dwb_consume(const DwBigBatch &b, const uint32_t (&off)[4],
-                                            v16i (&acc)[DWB_RT][DWB_CT],
-                                            uint32_t (&tcnt)[DWB_CT], uint32_t (&qsum)[DWB_RT]) {
+template <bool B8, int RT, int CT>
+__device__ __forceinline__ void dwb_consume(const DwBigBatch<RT, CT> &b, const uint32_t (&off)[4],
+                                            v16i (&acc)[RT][CT], uint32_t (&tcnt)[CT],
+                                            uint32_t (&qsum)[RT]) {
 #pragma unroll
-  for (int ct = 0; ct < DWB_CT; ++ct)
+  for (int ct = 0; ct < CT; ++ct)
     tcnt[ct] += __popc(uint32_t(b.word[ct])) + __popc(uint32_t(b.word[ct] >> 32));
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     // For b = 8 the sums are taken of the biased bytes q - 128 (signed), the only form
     // kept in registers; the epilogue adds 128 per position back.
-    v4i A[DWB_RT];
+    v4i A[RT];
 #pragma unroll
-    for (int rt = 0; rt < DWB_RT; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       A[rt] = B8 ? bias128(b.A[h][rt]) : b.A[h][rt];
 #pragma unroll
       for (int k = 0; k < 4; ++k)
@@ -317,58 +322,57 @@ __device__ __forceinline__ void dwb_consume(const DwBigBatch &b, const uint32_t 
                       : __builtin_amdgcn_udot4(uint32_t(A[rt][k]), 0x01010101u, qsum[rt], false);
     }
 #pragma unroll
-    for (int ct = 0; ct < DWB_CT; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
       const uint32_t half = uint32_t(b.word[ct] >> (32 * h));
       const v4i B = v4i{bits01x4(half, off[0]), bits01x4(half, off[1]), bits01x4(half, off[2]),
                         bits01x4(half, off[3])};
 #pragma unroll
-      for (int rt = 0; rt < DWB_RT; ++rt) acc[rt][ct] = mfma_i8(A[rt], B, acc[rt][ct]);
+      for (int rt = 0; rt < RT; ++rt) acc[rt][ct] = mfma_i8(A[rt], B, acc[rt][ct]);
     }
   }
 }
-template <bool B8>
+template <bool B8, int RT, int CT, int ST>
 __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   const int lane = threadIdx.x & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
-  const uint32_t kgroups = (a.K + DW_WAVES * 32 * DWB_CT - 1) / (DW_WAVES * 32 * DWB_CT);
+  const uint32_t kgroups = (a.K + DW_WAVES * 32 * CT - 1) / (DW_WAVES * 32 * CT);
   const uint32_t rb = bid / kgroups;
-  const uint32_t j0 = rb * (32 * DWB_RT);
-  const uint32_t k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * (32 * DWB_CT);
+  const uint32_t j0 = rb * (32 * RT);
+  const uint32_t k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * (32 * CT);
   if (k0 >= a.K) return;
-  v16i acc[DWB_RT][DWB_CT];
+  v16i acc[RT][CT];
 #pragma unroll
-  for (int rt = 0; rt < DWB_RT; ++rt)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-    for (int ct = 0; ct < DWB_CT; ++ct) acc[rt][ct] = v16i{0};
-  uint32_t tcnt[DWB_CT], qsum[DWB_RT];
+    for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = v16i{0};
+  uint32_t tcnt[CT], qsum[RT];
 #pragma unroll
-  for (int ct = 0; ct < DWB_CT; ++ct) tcnt[ct] = 0u;
+  for (int ct = 0; ct < CT; ++ct) tcnt[ct] = 0u;
 #pragma unroll
-  for (int rt = 0; rt < DWB_RT; ++rt) qsum[rt] = 0u;
+  for (int rt = 0; rt < RT; ++rt) qsum[rt] = 0u;
   if (int(j0) < count && a.Wr > 0) {
     const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
     const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
-    uint32_t aoff[DWB_RT], boff[DWB_CT], off[4];
+    uint32_t aoff[RT], boff[CT], off[4];
 #pragma unroll
-    for (int rt = 0; rt < DWB_RT; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       const uint32_t j = j0 + 32 * rt + i;
       aoff[rt] = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
     }
 #pragma unroll
-    for (int ct = 0; ct < DWB_CT; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
       const uint32_t kc = k0 + 32 * ct + i;
       boff[ct] = kc < a.K ? kc * 8 : BUF_NONE;
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) off[k] = uint32_t(16 * g + 4 * k);
-    // A ring of DWB_STAGES words: word c + DWB_STAGES is requested as soon as word c has
-    // been used, so DWB_STAGES - 1 words are in flight during each word's products.  Every
+    // A ring of ST words: word c + ST is requested as soon as word c has
+    // been used, so ST - 1 words are in flight during each word's products.  Every
     // step issues the same loads (a word past the end re-reads the last one), so the
     // waits count exactly.
-    constexpr int ST = DWB_STAGES;
-    DwBigBatch bs[ST];
+    DwBigBatch<RT, CT> bs[ST];
     const uint32_t last = a.Wr - 1;
 #pragma unroll
     for (int u = 0; u < ST; ++u) dwb_issue(a, crs, xrs, aoff, boff, min(uint32_t(u), last), bs[u]);
@@ -376,7 +380,7 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
 #pragma unroll
       for (int u = 0; u < ST; ++u) {
         if (c + u >= a.Wr) break;
-        dwb_consume<B8>(bs[u], off, acc, tcnt, qsum);
+        dwb_consume<B8, RT, CT>(bs[u], off, acc, tcnt, qsum);
         __builtin_amdgcn_sched_barrier(0);
         dwb_issue(a, crs, xrs, aoff, boff, min(c + u + ST, last), bs[u]);
         __builtin_amdgcn_sched_barrier(0);
@@ -386,7 +390,7 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   // Lane i (and i + 32) holds half of the code sum of row i of each row tile; the
   // accumulator rows of a lane are acc_row(v, g), fetched from their lanes.
 #pragma unroll
-  for (int rt = 0; rt < DWB_RT; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     // Sum of the codes of row i of the tile (b = 8: of q - 128 over all Rp positions).
     const int qrow = int(qsum[rt] + lane_xor<32>(qsum[rt])) + (B8 ? 128 * int(a.Rp) : 0);
     int qv[16];
@@ -394,7 +398,7 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
     for (int v = 0; v < 16; ++v) qv[v] = __shfl(qrow, acc_row(v, g));
     const uint32_t jt = j0 + 32 * rt;
 #pragma unroll
-    for (int ct = 0; ct < DWB_CT; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
       const uint32_t kc = k0 + 32 * ct + i;
       if (kc >= a.K) continue;
       const int T = int(tcnt[ct]);
@@ -416,16 +420,21 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
     }
   }
 }
-// Blocks of the big form.
-uint32_t dw_big_blocks(uint32_t D, uint32_t K) {
-  return ((D + 32 * DWB_RT - 1) / (32 * DWB_RT)) *
-         ((K + DW_WAVES * 32 * DWB_CT - 1) / (DW_WAVES * 32 * DWB_CT));
+// Blocks of the big form with CT column tiles per wave (two row tiles).
+uint32_t dw_big_blocks(uint32_t D, uint32_t K, int ct) {
+  return ((D + 63) / 64) * ((K + DW_WAVES * 32 * ct - 1) / (DW_WAVES * 32 * ct));
 }
 
-// Two waves per SIMD: the accumulators and the word ring fit 256 registers.
+// Long contractions: two waves per SIMD (the accumulators and the word ring fit 256
+// registers).
 template <bool B8>
 __global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_mfma_dw_big(DwArgs a) {
-  dw_big_body<B8>(a, blockIdx.x);
+  dw_big_body<B8, 2, 4, 4>(a, blockIdx.x);
+}
+// Short contractions: three waves per SIMD, for the stores.
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) void k_mfma_dw_short(DwArgs a) {
+  dw_big_body<B8, 2, 2, 2>(a, blockIdx.x);
 }
 
 template <bool B8, bool DIRECT>
@@ -1144,6 +1153,16 @@ bool dw_big(const Layer &L, const DwArgs &a) {
 }
 
 template <bool B8>
+void launch_dw_big(const DwArgs &a, hipStream_t s) {
+  if (a.Wr >= uint32_t(DWB_LONG_WORDS))
+    hipLaunchKernelGGL(k_mfma_dw_big<B8>, dim3(dw_big_blocks(a.D, a.K, 4)), dim3(DW_THREADS), 0,
+                       s, a);
+  else
+    hipLaunchKernelGGL(k_mfma_dw_short<B8>, dim3(dw_big_blocks(a.D, a.K, 2)), dim3(DW_THREADS),
+                       0, s, a);
+}
+
+template <bool B8>
 void launch_dw_finish(const Layer &L, const DwArgs &a, hipStream_t s) {
   if (a.S > DWF_WIDE) {
     const uint32_t qblocks = uint32_t((dw_kp(L) + 63) / 64);
@@ -1162,8 +1181,7 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   const dim3 grid(dw_part_blocks(L, a));
   auto go = [&]<bool B8>() {
     if (dw_big(L, a)) {
-      hipLaunchKernelGGL(k_mfma_dw_big<B8>, dim3(dw_big_blocks(a.D, a.K)), dim3(DW_THREADS), 0,
-                         s, a);
+      launch_dw_big<B8>(a, s);
     } else if (a.S == 1) {
       hipLaunchKernelGGL((k_mfma_dw_part<B8, true>), grid, dim3(DW_THREADS), 0, s, a);
     } else {
@@ -1211,12 +1229,8 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   // launch then holds only dX blocks.
   const bool big = dw_big(L, dwa);
   if (big) {
-    if (cfg.bits == 8)
-      hipLaunchKernelGGL(k_mfma_dw_big<true>, dim3(dw_big_blocks(dwa.D, dwa.K)), dim3(DW_THREADS),
-                         0, s, dwa);
-    else
-      hipLaunchKernelGGL(k_mfma_dw_big<false>, dim3(dw_big_blocks(dwa.D, dwa.K)),
-                         dim3(DW_THREADS), 0, s, dwa);
+    if (cfg.bits == 8) launch_dw_big<true>(dwa, s);
+    else launch_dw_big<false>(dwa, s);
   }
   const uint32_t ndw = big ? 0u : dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);

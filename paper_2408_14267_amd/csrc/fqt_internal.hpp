@@ -52,6 +52,7 @@ struct QuantWs {
   int2 *part_c;            // [stats_row_blocks][D]  channel partials of each row block
   int2 *part_s;            // [ceil(D/64)][ceil(R/64)][stats_slots]  sample partials of
                            //   each 64 x 64 tile, one slot per sample the tile meets
+                           //   (P = 1: [R][ceil(D/64)], one per sample and tile)
   int2 *skey;              // [N] (min, max) ordered-int keys of each sample
   int2 *ckey;              // [D] (min, max) keys of each output channel
   GroupParam *sp;          // [N]

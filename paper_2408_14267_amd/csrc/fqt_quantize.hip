@@ -73,10 +73,13 @@ __device__ __forceinline__ int wave_max(int v) { return wave_max_all(v); }
 // (rs = stats_rows_per_block: enough blocks to cover the chip, few partials).  Sample partials: part_s[(dt * nrt + rt) * SL + k] for the 64-row tile rt and
 // 64-channel tile dt, slot k holding sample n_first(rt) + k, n_first(rt) = rt * 64 / P, and
 // SL = min(64, ceil(63 / P) + 1) slots (a 64-row tile meets at most that many samples).
+// With P = 1 (a sample per row) they are part_s[r * ndt + dt] instead, so that the partials
+// of one sample are contiguous for the reduction.
 struct StatsGeom {
   TileGeom g;
   uint32_t nrt, SL, rs;
   uint32_t chan_fast;   // grid x walks the channel tiles, y the row blocks
+  uint32_t ndt;         // channel tiles
 };
 
 // Load the quads of tile rows [r0, r0 + 64) x channels [d0, d0 + 64) into x (element 0 of
@@ -121,7 +124,6 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
                                                    uint2 *__restrict__ mkc) {
   __shared__ int32_t key[TILE][TILE + 1];
   __shared__ int32_t pmin[WAVES][TILE], pmax[WAVES][TILE];
-  __shared__ int2 cpart[TILE];
   const TileGeom &g = sg.g;
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
@@ -129,19 +131,17 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
   const uint32_t byc = sg.chan_fast ? blockIdx.x : blockIdx.y;   // channel tile
   const uint32_t d0 = byc * TILE;
   const uint32_t rt0 = bxr * sg.rs;
-  int clo[TILE / WAVES], chi[TILE / WAVES];      // channel rows wave + WAVES * i
-#pragma unroll
-  for (int i = 0; i < TILE / WAVES; ++i) {
-    clo[i] = INT_MAX;
-    chi[i] = INT_MIN;
+  int clo = INT_MAX, chi = INT_MIN;             // channel d0 + lane over this wave's rows
+  // Two register sets of row tiles: two tiles' loads are in flight behind each reduction.
+  float xa[QUADS][4], xb[QUADS][4];
+  bool oka[QUADS], okb[QUADS];
+  if (MODE != TILE_SCALAR) {
+    stats_load<MODE, DT>(dy, g, rt0 * TILE, d0, t, xa, oka);
+    if (sg.rs > 1 && rt0 + 1 < sg.nrt) stats_load<MODE, DT>(dy, g, (rt0 + 1) * TILE, d0, t, xb, okb);
   }
-  float x[QUADS][4];
-  bool ok[QUADS];
-  if (MODE != TILE_SCALAR) stats_load<MODE, DT>(dy, g, rt0 * TILE, d0, t, x, ok);
-
-  for (uint32_t s = 0; s < sg.rs; ++s) {
+  auto tile = [&](uint32_t s, float (&x)[QUADS][4], bool (&ok)[QUADS]) -> bool {
     const uint32_t rt = rt0 + s;
-    if (rt >= sg.nrt) break;
+    if (rt >= sg.nrt) return false;
     const uint32_t r0 = rt * TILE;
     if (MODE != TILE_SCALAR) {
       for (int q = 0; q < QUADS; ++q) {
@@ -152,9 +152,9 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
           key[dk][rk] = f2key(x[q][k] + 0.0f);
         }
       }
-      // The next row tile's loads fly while this one is reduced.
-      if (s + 1 < sg.rs && rt + 1 < sg.nrt)
-        stats_load<MODE, DT>(dy, g, r0 + TILE, d0, t, x, ok);
+      // The row tile two ahead loads into these registers while this one is reduced.
+      if (s + 2 < sg.rs && rt + 2 < sg.nrt)
+        stats_load<MODE, DT>(dy, g, r0 + 2 * TILE, d0, t, x, ok);
     } else {
       for (int q = 0; q < 4 * QUADS; ++q) {
         int dd, rr;
@@ -166,13 +166,15 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
     __syncthreads();
 
     const bool row_ok = r0 + lane < g.R;
-    // Channel rows of the tile: reduce over the tile's 64 rows r.
+    // Channels of the tile: lane d0 + lane reduces the wave's rows (read across the key
+    // rows; the odd pitch keeps them on distinct banks), no cross-lane step.
 #pragma unroll
     for (int i = 0; i < TILE / WAVES; ++i) {
-      const int dd = wave + WAVES * i;
-      const int k = key[dd][lane];
-      clo[i] = min(clo[i], wave_min(row_ok ? k : INT_MAX));
-      chi[i] = max(chi[i], wave_max(row_ok ? k : INT_MIN));
+      const int rr = (TILE / WAVES) * wave + i;
+      if (r0 + rr >= g.R) break;
+      const int k = key[lane][rr];
+      clo = min(clo, k);
+      chi = max(chi, k);
     }
     // Columns r of the tile: reduce over the tile's channels.
     int lo = INT_MAX, hi = INT_MIN;
@@ -197,10 +199,11 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
       const uint32_t slot = row_ok ? fdiv(r0 + lane, g.divP) - n_first : 0xFFFFFFFFu;
       int2 *ps = part_s + (size_t(byc) * sg.nrt + rt) * sg.SL;
       if (g.P == 1) {
+        // One sample per row: its partials are stored sample-major, [R][ndt].
         if (mks) {
           if (row_ok) merge_key(mks + (byc % MKEY_REP) * MKEY_GROUPS + r0 + lane, lo, hi);
-        } else {
-          ps[lane] = row_ok ? make_int2(lo, hi) : make_int2(INT_MAX, INT_MIN);
+        } else if (row_ok) {
+          part_s[size_t(r0 + lane) * sg.ndt + byc] = make_int2(lo, hi);
         }
       } else {
         for (uint32_t k = 0; k < sg.SL; ++k) {
@@ -218,18 +221,25 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
     }
     // (The next tile's key stores wait for every read of this one.)
     __syncthreads();
+      return true;
+  };
+  for (uint32_t s = 0; s < sg.rs; s += 2) {
+    if (!tile(s, xa, oka) || s + 1 >= sg.rs || !tile(s + 1, xb, okb)) break;
   }
-  // Channel partials of this row block, [row block][D]: one coalesced store.
-  if (lane == 0) {
-#pragma unroll
-    for (int i = 0; i < TILE / WAVES; ++i) cpart[wave + WAVES * i] = make_int2(clo[i], chi[i]);
-  }
+  // Channel partials of this row block, [row block][D]: the waves' partials combined,
+  // then one coalesced store.
+  pmin[wave][lane] = clo;
+  pmax[wave][lane] = chi;
   __syncthreads();
   if (wave == 1 && d0 + lane < g.D) {
-    if (mkc)
-      merge_key(mkc + (bxr % MKEY_REP) * MKEY_GROUPS + d0 + lane, cpart[lane].x,
-                cpart[lane].y);
-    else part_c[size_t(bxr) * g.D + d0 + lane] = cpart[lane];
+    int lo = pmin[0][lane], hi = pmax[0][lane];
+#pragma unroll
+    for (int v = 1; v < WAVES; ++v) {
+      lo = min(lo, pmin[v][lane]);
+      hi = max(hi, pmax[v][lane]);
+    }
+    if (mkc) merge_key(mkc + (bxr % MKEY_REP) * MKEY_GROUPS + d0 + lane, lo, hi);
+    else part_c[size_t(bxr) * g.D + d0 + lane] = make_int2(lo, hi);
   }
 }
 
@@ -302,7 +312,14 @@ __global__ __launch_bounds__(RED_THREADS) void k_stats_reduce(const int2 *__rest
   const uint32_t b = blockIdx.x;
   const uint32_t N = g.R / g.P;
   int lo = INT_MAX, hi = INT_MIN;
-  if (b < N) {
+  if (b < N && g.P == 1) {
+#pragma unroll 8
+    for (uint32_t i = threadIdx.x; i < ndt; i += RED_THREADS) {
+      const int2 v = part_s[size_t(b) * ndt + i];
+      lo = min(lo, v.x);
+      hi = max(hi, v.y);
+    }
+  } else if (b < N) {
     const uint32_t rt_lo = (b * g.P) / TILE, rt_hi = min(sg.nrt - 1, (b * g.P + g.P - 1) / TILE);
     const uint32_t cnt = rt_hi - rt_lo + 1;
 #pragma unroll 8
@@ -603,6 +620,32 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
     }
   }
 #undef GROUP_KEY
+}
+
+// AGP off (Section 5.2: every group kept, p = 1) over large group sets: one thread per
+// group writes what the one-workgroup selection writes for it (rank = group id), so the
+// whole chip takes the per-group work.  Grid: ceil(max G / 256) x 2 sets.
+__global__ __launch_bounds__(256) void k_select_off(SelectArgs a) {
+  const SetArgs &S = blockIdx.y ? a.set[1] : a.set[0];
+  const int i = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (i == 0) *S.count = S.G;
+  if (i >= S.G) return;
+  const int B = (1 << a.bits) - 1;
+  const int2 k = S.key[i];
+  const float R = group_range(k);
+  const float Z = key2f(k.x);
+  const float Sc = static_cast<float>(static_cast<double>(R) / static_cast<double>(B));
+  S.prob[i] = 1.0f;
+  S.scale[i] = Sc;
+  S.offset[i] = Z + 0.0f;
+  S.slot[i] = make_float2(Sc, Z + 0.0f);
+  GroupParam gp;
+  gp.z = Z;
+  gp.inv = R > 0.0f ? __fdiv_rn(float(B), R) : 0.0f;
+  gp.rank = i;
+  gp.pad = 0;
+  S.gp[i] = gp;
+  S.kept[i] = i;
 }
 
 // Select for group sets of at most GP <= 1024 groups, one 1024-thread workgroup per set,
@@ -1261,7 +1304,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   // With channels contiguous in dY (P = 1) the channel tiles go fastest, so the blocks in
   // flight read whole rows of dY in order.
   const uint32_t chan_fast = (mode == TILE_CHAN && nrb <= 65535) ? 1u : 0u;
-  const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L), chan_fast};
+  const StatsGeom sg{g, nrt, stats_slots(L), stats_rows_per_block(L), chan_fast, ndt};
   const dim3 grid = chan_fast ? dim3(ndt, nrb) : dim3(nrb, ndt);
   const int64_t gmax = L.N > L.D ? L.N : L.D;
   // Large maps with both group sets in one-workgroup selections: per-plane statistics
@@ -1384,7 +1427,10 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     hipLaunchKernelGGL(k_stats_reduce, dim3(unsigned(L.N + L.D)), dim3(RED_THREADS), 0, s,
                        w.part_c, w.part_s, sg, nrb, ndt, w.skey, w.ckey);
     if (last_launch_status() != FQT_OK) return FQT_E_HIP;
-    if (gmax <= 4096) st = launch_select<4096, 1024>(sa, s);
+    if (cfg.agp_mode == FQT_AGP_OFF) {
+      hipLaunchKernelGGL(k_select_off, dim3(unsigned((gmax + 255) / 256), 2), dim3(256), 0, s, sa);
+      st = last_launch_status();
+    } else if (gmax <= 4096) st = launch_select<4096, 1024>(sa, s);
     else st = launch_select<16384, 1024>(sa, s);
   }
   if (st != FQT_OK) return st;

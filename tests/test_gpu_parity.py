@@ -87,6 +87,18 @@ CASES = [
      Recipe("channel_lognormal", sigma=1.5), "f32"),
     ("linear_bigdw_ragged_b8", LayerShape("fc", "linear", 100, 2100, 2050), 8, 0,
      Recipe("sample_lognormal", sigma=1.0), "f32"),
+    # AGP off with more than 1024 samples: the per-group selection over the whole chip;
+    # channel-fast statistics and codes; one-bit codes; the big dW form with AGP off.
+    ("linear_off_large_b1", LayerShape("fc", "linear", 2048, 96, 1300), 1, 2,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("linear_bigdw_off_b1", LayerShape("fc", "linear", 256, 2048, 2112), 1, 2,
+     Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # Big dW forms over contractions of 8 words and more (the long form's word ring, with
+    # a ragged last word and the b = 8 bias).
+    ("linear_bigdw_long_b2", LayerShape("fc", "linear", 520, 2048, 2048), 2, 0,
+     Recipe("channel_lognormal", sigma=1.5), "f32"),
+    ("linear_bigdw_long_ragged_b8", LayerShape("fc", "linear", 600, 2100, 2050), 8, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
 ]
 
 
