@@ -433,6 +433,21 @@ __device__ float block_max_f(float v, float *scratch) {
   return r;
 }
 
+template <int NT>
+__device__ uint64_t block_max_u64(uint64_t v, uint64_t *scratch) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = __shfl_xor(v, o);
+    v = v > y ? v : y;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  uint64_t r = scratch[0];
+  for (int i = 1; i < NT / 64; ++i) r = r > scratch[i] ? r : scratch[i];
+  __syncthreads();
+  return r;
+}
+
 // Exclusive prefix of `v` over thread order; `total` receives the block total.
 template <int NT, typename T>
 __device__ T block_exscan(T v, T *scratch, T &total) {
@@ -487,7 +502,64 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
   uint64_t w_thr = 0;          // weight of the last saturated group
   uint64_t w_rem = 0;          // weight of the unsaturated groups
   uint64_t key_thr = 0;        // TOPK: smallest kept sort key
-  if (a.mode != FQT_AGP_OFF) {
+  bool need_sort = a.mode == FQT_AGP_TOPK;
+  if (a.mode == FQT_AGP_BERNOULLI) {
+    // Saturation by rounds, as in the one-key-per-thread selection: with s groups
+    // saturated and W the weight of the others, every unsaturated group with
+    // (G - b s) w >= b W saturates; the rounds end (at s_sat) when none does, else the
+    // sort below decides.  Equal weights pass or fail together, so the saturated groups
+    // are exactly those with w >= w_thr, the smallest saturated weight.
+    constexpr int SAT_ROUNDS = 8;
+    const int c0 = t * ((G + NT - 1) / NT);
+    const int c1 = min(c0 + (G + NT - 1) / NT, G);
+    uint64_t wsum = 0;
+    for (int i = c0; i < c1; ++i) {
+      const uint64_t w = agp_weight(group_range(GROUP_KEY(i)), rmax);
+      skey[i] = w;                        // this thread's weights, kept in LDS
+      wsum += w;
+    }
+    uint64_t W = block_sum<NT, uint64_t>(wsum, scr_u);
+    uint32_t satbits = 0;                 // groups c0 + m saturated
+    int64_t sc = 0;
+    bool done = false;
+    for (int round = 0; round < SAT_ROUNDS; ++round) {
+      const int64_t A = int64_t(G) - int64_t(b) * sc;
+      uint64_t rs = 0;
+      int32_t rc = 0;
+      for (int i = c0; i < c1; ++i) {
+        const uint64_t w = skey[i];
+        const bool pass = !((satbits >> (i - c0)) & 1u) && w > 0 &&
+                          A * int64_t(w) >= int64_t(b) * int64_t(W);
+        if (pass) {
+          satbits |= 1u << (i - c0);
+          rs += w;
+          ++rc;
+        }
+      }
+      const int32_t cnt = block_sum<NT, int32_t>(rc, scr_i);
+      const uint64_t sum = block_sum<NT, uint64_t>(rs, scr_u);
+      if (cnt == 0) {
+        done = true;
+        break;
+      }
+      sc += cnt;
+      W -= sum;
+    }
+    if (done) {
+      s_sat = sc;
+      w_rem = sc < G ? W : 0;
+      uint64_t wmin = ~0ull;
+      for (int i = c0; i < c1; ++i)
+        if ((satbits >> (i - c0)) & 1u) wmin = min(wmin, skey[i]);
+      // Smallest saturated weight: a block minimum as the negated maximum.
+      const uint64_t neg = block_max_u64<NT>(~wmin, scr_u);
+      w_thr = sc > 0 ? ~neg : 0;
+    } else {
+      need_sort = true;
+    }
+    __syncthreads();                      // the weights in skey are read; the sort reuses it
+  }
+  if (need_sort) {
     for (int i = t; i < GP; i += NT)
       skey[i] = i < G ? sort_key(agp_weight(group_range(GROUP_KEY(i)), rmax), i) : 0ull;
     __syncthreads();

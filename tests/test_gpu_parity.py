@@ -99,6 +99,12 @@ CASES = [
      Recipe("channel_lognormal", sigma=1.5), "f32"),
     ("linear_bigdw_long_ragged_b8", LayerShape("fc", "linear", 600, 2100, 2050), 8, 0,
      Recipe("sample_lognormal", sigma=1.0), "f32"),
+    # More than 1024 samples with geometrically decaying ranges: the many-group selection
+    # saturates in 6 rounds, and (9 rounds needed) falls back to its sort.
+    ("linear_geometric_large_6_rounds_b2", LayerShape("fc", "linear", 1500, 8, 40), 2, 0,
+     Recipe("sample_geometric", ratio=0.99), "f32"),
+    ("linear_geometric_large_sorted_b3", LayerShape("fc", "linear", 1500, 8, 40), 3, 0,
+     Recipe("sample_geometric", ratio=0.97), "f32"),
 ]
 
 
