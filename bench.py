@@ -33,7 +33,7 @@ MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
 # measured on (TRAFFIC_DIGEST: sha256 over the names and contents of every file in csrc/).
 FETCH_SCALE = 262144.0 / 131086.7
 WRITE_SCALE = 1.0
-TRAFFIC_DIGEST = "fe2d073344a81e81fa79f078e939b83d8cfd675efd29148f37aff8c59773df03"
+TRAFFIC_DIGEST = "b81c5dce1922ea7f5cfba9ab8a13e3e2c1f1dc1b4a5b04d26ac63e5243dde3e5"
 TRAFFIC = {
     # entry: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch of its kernels
     "gemm_dx": (2538.0, 8192.0),
