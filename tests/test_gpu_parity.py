@@ -273,6 +273,56 @@ def test_full_vgg_cifar_conv_layer():
     assert 0 < ref.qgrad.samples.count < layer.N and 0 < ref.qgrad.channels.count < layer.D
 
 
+def test_dw_product_16384_cube_sampled():
+    """The dW product at 16384 x 16384 over a 16384-deep contraction (the large GEMM sweep's
+    largest point: the long big-dW form, a 256-word contraction), b = 1, AGP off, on sampled
+    outputs: the integer I of 8 channels x 64 columns from the oracle's own quantizer steps on
+    those channels (statistics, Philox words, stochastic rounding) and the sign bits of those
+    columns of X; dW within the rescale tolerance."""
+    from oracle.philox import STREAM_ELEM, uniform_words
+    fqt = _fqt()
+    N = C = D = 16384
+    seed, step, lid = 7, 1, 2
+    layer = LayerShape("fc", "linear", N, C, D)
+    _announce(f"[gpu parity] sampled dW {layer}")
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    dY = torch.randn((N, D), device="cuda", generator=gen)
+    X = torch.randn((N, C), device="cuda", generator=gen)
+    desc = fqt.layer_desc(layer)
+    cfg = fqt.quant_cfg(1, fqt.FQT_AGP_OFF, seed, step, lid)
+    q = fqt.QGrad(desc, cfg)
+    fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE))
+    xs = torch.empty(((N + 63) // 64) * C, dtype=torch.int64, device="cuda")
+    fqt.fqt_pack_input_signs(desc, X, xs)
+    dW = torch.empty((D, C), dtype=torch.float32, device="cuda")
+    I_dw = torch.empty((D, C), dtype=torch.int32, device="cuda")
+    fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW), I_dw)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    chans = np.concatenate([[0, D - 1], rng.choice(D, 6, replace=False)])
+    cols = np.concatenate([[0, C - 1], rng.choice(C, 62, replace=False)])
+    y = dY[:, torch.from_numpy(chans).cuda()].cpu().numpy()           # [N][8]
+    xb = (X[:, torch.from_numpy(cols).cuda()].cpu().numpy() > 0)       # [N][64]
+    s = np.where(xb, 1, -1).astype(np.int64)
+    I_got = I_dw[torch.from_numpy(chans).cuda()][:, torch.from_numpy(cols).cuda()].cpu().numpy()
+    W_got = dW[torch.from_numpy(chans).cuda()][:, torch.from_numpy(cols).cuda()].cpu().numpy()
+    n = np.arange(N, dtype=np.uint64)
+    for a, d in enumerate(chans):
+        col = y[:, a].astype(np.float32)
+        Z = col.min()
+        R = np.float32(col.max() - Z)
+        u32 = uniform_words(n * np.uint64(D) + np.uint64(d), STREAM_ELEM, seed, step, lid)
+        qd = ofqt.sr_codes(col, Z, R, 1, u32).astype(np.int64)
+        I_ref = qd @ s                                                 # [64]
+        assert np.array_equal(I_got[a], I_ref), f"I of channel {d}"
+        # AGP off: S = R / B, Z' = Z; c = 2 T - N over the column's set bits.
+        S = np.float32(np.float64(R) / 1.0)
+        c = (2 * xb.sum(axis=0) - N).astype(np.float64)
+        t1, t2 = np.float64(S) * I_ref, np.float64(Z) * c
+        bad = np.abs(W_got[a].astype(np.float64) - (t1 + t2)) > 1e-5 * (np.abs(t1) + np.abs(t2)) + 1e-30
+        assert not bad.any(), f"dW of channel {d}"
+
+
 def test_layer_backward_graph_replays_match_eager():
     """fqt_layer_backward captured in a HIP graph (forked second stream included) and
     replayed several times, with eager calls on other data and synchronizations between
