@@ -331,13 +331,25 @@ __device__ __forceinline__ void dwb_consume(const DwBigBatch<RT, CT> &b, const u
     }
   }
 }
-template <bool B8, int RT, int CT, int ST>
+// SPLIT: the same tiles over the word slice [s wps, (s + 1) wps) of a split-R product,
+// writing the slice's partial sums (in the split kernel's form, sum over the slice of
+// A_r s_r with A_r the MFMA code byte: 2 sum A b - sum A) and its set-bit counts for the
+// finish pass.  Grid: S slices (fastest) x slot blocks x column groups.
+template <bool B8, int RT, int CT, int ST, bool SPLIT = false>
 __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   const int lane = threadIdx.x & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
   const uint32_t kgroups = (a.K + DW_WAVES * 32 * CT - 1) / (DW_WAVES * 32 * CT);
+  uint32_t sp = 0;
+  if (SPLIT) {
+    const uint32_t rest = fdiv(bid, a.divS);
+    sp = bid - rest * a.S;
+    bid = rest;
+  }
+  const uint32_t cb = SPLIT ? sp * a.wps : 0u;
+  const uint32_t ce = SPLIT ? min(a.Wr, cb + a.wps) : a.Wr;
   const uint32_t rb = bid / kgroups;
   const uint32_t j0 = rb * (32 * RT);
   const uint32_t k0 = ((bid - rb * kgroups) * DW_WAVES + wave) * (32 * CT);
@@ -352,7 +364,7 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   for (int ct = 0; ct < CT; ++ct) tcnt[ct] = 0u;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) qsum[rt] = 0u;
-  if (int(j0) < count && a.Wr > 0) {
+  if (int(j0) < count && ce > cb) {
     const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
     const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
     uint32_t aoff[RT], boff[CT], off[4];
@@ -373,13 +385,13 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
     // step issues the same loads (a word past the end re-reads the last one), so the
     // waits count exactly.
     DwBigBatch<RT, CT> bs[ST];
-    const uint32_t last = a.Wr - 1;
+    const uint32_t last = ce - 1;
 #pragma unroll
-    for (int u = 0; u < ST; ++u) dwb_issue(a, crs, xrs, aoff, boff, min(uint32_t(u), last), bs[u]);
-    for (uint32_t c = 0; c < a.Wr; c += ST) {
+    for (int u = 0; u < ST; ++u) dwb_issue(a, crs, xrs, aoff, boff, min(cb + uint32_t(u), last), bs[u]);
+    for (uint32_t c = cb; c < ce; c += ST) {
 #pragma unroll
       for (int u = 0; u < ST; ++u) {
-        if (c + u >= a.Wr) break;
+        if (c + u >= ce) break;
         dwb_consume<B8, RT, CT>(bs[u], off, acc, tcnt, qsum);
         __builtin_amdgcn_sched_barrier(0);
         dwb_issue(a, crs, xrs, aoff, boff, min(c + u + ST, last), bs[u]);
@@ -389,6 +401,32 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
   }
   // Lane i (and i + 32) holds half of the code sum of row i of each row tile; the
   // accumulator rows of a lane are acc_row(v, g), fetched from their lanes.
+  if (SPLIT) {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const uint32_t kc = k0 + 32 * ct + i;
+      if (rb == 0 && g == 0 && kc < a.K) a.partT[size_t(sp) * a.Kp + kc] = int32_t(tcnt[ct]);
+    }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int qrow = int(qsum[rt] + lane_xor<32>(qsum[rt]));   // sum of A over the slice
+      int qv[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) qv[v] = __shfl(qrow, acc_row(v, g));
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const uint32_t kc = k0 + 32 * ct + i;
+        if (kc >= a.K) continue;
+        int32_t *out = a.part + (size_t(sp) * a.D + j0 + 32 * rt) * a.Kp + kc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = acc_row(v, g);
+          if (int(j0) + 32 * rt + row < count) out[size_t(row) * a.Kp] = 2 * acc[rt][ct][v] - qv[v];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     // Sum of the codes of row i of the tile (b = 8: of q - 128 over all Rp positions).
@@ -424,6 +462,13 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
 uint32_t dw_big_blocks(uint32_t D, uint32_t K, int ct) {
   return ((D + 63) / 64) * ((K + DW_WAVES * 32 * ct - 1) / (DW_WAVES * 32 * ct));
 }
+
+// Split-R partials in the big form (long slices of the contraction, wide outputs).
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) void k_mfma_dw_split(DwArgs a) {
+  dw_big_body<B8, 2, 2, 2, true>(a, blockIdx.x);
+}
+uint32_t dw_split_blocks(const DwArgs &a) { return a.S * dw_big_blocks(a.D, a.K, 2); }
 
 // Long contractions: two waves per SIMD (the accumulators and the word ring fit 256
 // registers).
@@ -1152,6 +1197,17 @@ bool dw_big(const Layer &L, const DwArgs &a) {
   return a.S == 1 && ((L.D + 63) / 64) * ((L.K + 63) / 64) >= 1024;
 }
 
+// Split-R products over very long contractions (N*Ho*Wo of 2^19 rows and more, slices of
+// 16 words and more): the partials in the big form's 64 x 64 wave tiles.  Shorter ones stay
+// in the products launch, where their partial blocks overlap the dX blocks.
+bool dw_split_big(const Layer &L, const DwArgs &a) {
+  return a.S > 1 && L.Wr >= 8192 && a.wps >= 16;
+}
+template <bool B8>
+void launch_dw_split(const DwArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(k_mfma_dw_split<B8>, dim3(dw_split_blocks(a)), dim3(DW_THREADS), 0, s, a);
+}
+
 template <bool B8>
 void launch_dw_big(const DwArgs &a, hipStream_t s) {
   if (a.Wr >= uint32_t(DWB_LONG_WORDS))
@@ -1182,6 +1238,9 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   auto go = [&]<bool B8>() {
     if (dw_big(L, a)) {
       launch_dw_big<B8>(a, s);
+    } else if (dw_split_big(L, a)) {
+      launch_dw_split<B8>(a, s);
+      launch_dw_finish<B8>(L, a, s);
     } else if (a.S == 1) {
       hipLaunchKernelGGL((k_mfma_dw_part<B8, true>), grid, dim3(DW_THREADS), 0, s, a);
     } else {
@@ -1227,12 +1286,17 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   dxa.slot_sz = sslot;
   // A large one-split dW runs as its own launch in the 2 x 2-tile form; the products
   // launch then holds only dX blocks.
+  // Long split-R contractions likewise run their partials as their own launch.
   const bool big = dw_big(L, dwa);
+  const bool split_big = !big && dw_split_big(L, dwa);
   if (big) {
     if (cfg.bits == 8) launch_dw_big<true>(dwa, s);
     else launch_dw_big<false>(dwa, s);
+  } else if (split_big) {
+    if (cfg.bits == 8) launch_dw_split<true>(dwa, s);
+    else launch_dw_split<false>(dwa, s);
   }
-  const uint32_t ndw = big ? 0u : dw_part_blocks(L, dwa);
+  const uint32_t ndw = (big || split_big) ? 0u : dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const int nb = dx_batch(dxa);
   auto go = [&]<bool B8, bool DIRECT, bool WIDE>() {
