@@ -505,11 +505,23 @@ __global__ __launch_bounds__(256) void k_dw_finish(DwArgs a) {
   float out[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (int(slot) < count) {
     int4 acc = make_int4(0, 0, 0, 0), T4 = make_int4(0, 0, 0, 0);
-    for (uint32_t s = 0; s < a.S; ++s) {
-      const int4 v = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
-      const int4 t4 = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-      T4.x += t4.x; T4.y += t4.y; T4.z += t4.z; T4.w += t4.w;
+    // Eight slices' loads issue together (a slice past S re-reads the last one and is not
+    // added), so the sum costs one memory latency per eight slices.
+    constexpr uint32_t U = 8;
+    for (uint32_t s0 = 0; s0 < a.S; s0 += U) {
+      int4 v[U], t4[U];
+#pragma unroll
+      for (uint32_t u = 0; u < U; ++u) {
+        const uint32_t s = min(s0 + u, a.S - 1);
+        v[u] = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
+        t4[u] = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < U; ++u) {
+        const int m = s0 + u < a.S ? 1 : 0;
+        acc.x += m * v[u].x; acc.y += m * v[u].y; acc.z += m * v[u].z; acc.w += m * v[u].w;
+        T4.x += m * t4[u].x; T4.y += m * t4[u].y; T4.z += m * t4[u].z; T4.w += m * t4[u].w;
+      }
     }
     const int T[4] = {T4.x, T4.y, T4.z, T4.w};
     I[0] = acc.x; I[1] = acc.y; I[2] = acc.z; I[3] = acc.w;
