@@ -556,11 +556,23 @@ __global__ __launch_bounds__(256) void k_dw_finish_wide(DwArgs a) {
   const bool live = int(slot) < count && k < a.Kp;
   int4 acc = make_int4(0, 0, 0, 0), T4 = make_int4(0, 0, 0, 0);
   if (live) {
-    for (uint32_t s = chunk; s < a.S; s += DWF_CHUNKS) {
-      const int4 v = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
-      const int4 t4 = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-      T4.x += t4.x; T4.y += t4.y; T4.z += t4.z; T4.w += t4.w;
+    // Four of this chunk's slices load together (a slice past S re-reads the last one and
+    // is not added).
+    constexpr uint32_t U = 4;
+    for (uint32_t s0 = chunk; s0 < a.S; s0 += U * DWF_CHUNKS) {
+      int4 v[U], t4[U];
+#pragma unroll
+      for (uint32_t u = 0; u < U; ++u) {
+        const uint32_t s = min(s0 + u * DWF_CHUNKS, a.S - 1);
+        v[u] = *reinterpret_cast<const int4 *>(a.part + (size_t(s) * a.D + slot) * a.Kp + k);
+        t4[u] = *reinterpret_cast<const int4 *>(a.partT + size_t(s) * a.Kp + k);
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < U; ++u) {
+        const int m = s0 + u * DWF_CHUNKS < a.S ? 1 : 0;
+        acc.x += m * v[u].x; acc.y += m * v[u].y; acc.z += m * v[u].z; acc.w += m * v[u].w;
+        T4.x += m * t4[u].x; T4.y += m * t4[u].y; T4.z += m * t4[u].z; T4.w += m * t4[u].w;
+      }
     }
   }
   red[chunk][quad] = acc;
