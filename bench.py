@@ -33,7 +33,7 @@ MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
 # measured on (TRAFFIC_DIGEST: sha256 over the names and contents of every file in csrc/).
 FETCH_SCALE = 262144.0 / 131086.7
 WRITE_SCALE = 1.0
-TRAFFIC_DIGEST = "be5ef19397e89f9b9c538d8a23baa4e437885b6b2dd5e9bc26787f7ff10998f7"
+TRAFFIC_DIGEST = "44a2b213ef2730474d4b393662918398bd0843d8c2cdcf0dcb3d3f939fde34e1"
 TRAFFIC = {
     # entry: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch of its kernels
     "gemm_dx": (2538.0, 8192.0),
