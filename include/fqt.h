@@ -17,8 +17,10 @@
  *    dY [N][D][Ho][Wo], dX like X, dW like W (fp32).  A linear layer is the
  *    case H = W = kh = kw = 1 (X [N][C], W [D][C], dY [N][D]).
  *  - Every tensor pointer is a DEVICE pointer on the current HIP device; the
- *    caller owns all memory; the library never allocates, never synchronizes
- *    the stream and keeps no state between calls.  Work is enqueued on
+ *    caller owns all memory; the library never allocates and never synchronizes
+ *    the stream.  It keeps no host-side state; the only state that outlives a
+ *    call is the zeroed first FQT_WS_STATE_BYTES of a quantize or layer
+ *    workspace (see fqt_workspace_init).  Work is enqueued on
  *    `hip_stream` (a hipStream_t; NULL = the null stream); outputs are valid
  *    once that stream has reached the enqueued work.
  *  - Descriptor structs are HOST pointers, read during the call only.
@@ -139,11 +141,16 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
  * fqt_layer_backward (which holds an fqt_qgrad, the packed signs and the partial sums
  * inside it).  The library carves the workspace.  A FQT_WS_QUANTIZE or FQT_WS_LAYER
  * workspace keeps state between calls in its first 128 KiB (FQT_WS_STATE_BYTES): the group
- * keys that the statistics combine with atomics.  Zero-fill those bytes once before the
- * first call that uses the workspace; every call leaves them zero again (and the rest of
- * the workspace garbage).  Such a workspace may serve layers of any shape, one call at a
- * time, but nothing else may write its first 128 KiB (do not share it with a
- * FQT_WS_GEMM_DW workspace).  A FQT_WS_GEMM_DW workspace needs no initialisation. */
+ * keys that the statistics combine with atomics.  Those bytes must be zero when a call
+ * starts: run fqt_workspace_init on the workspace once, after allocating it and before its
+ * first use; every call that returns FQT_OK leaves them zero again (and the rest of the
+ * workspace garbage).  A call that fails after its first launch clears them itself on the
+ * same stream; if that clearing launch fails too, the call returns FQT_E_HIP and the
+ * caller runs fqt_workspace_init again before reusing the workspace.  An uninitialised
+ * workspace gives wrong group ranges, undetected.  Such a workspace may serve layers of
+ * any shape, one call at a time, but nothing else may write its first 128 KiB (do not
+ * share it with a FQT_WS_GEMM_DW workspace).  A FQT_WS_GEMM_DW or FQT_WS_FORWARD
+ * workspace needs no initialisation. */
 #define FQT_WS_STATE_BYTES 131072
 #define FQT_WS_QUANTIZE 0
 #define FQT_WS_LAYER 1
@@ -151,6 +158,13 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
 #define FQT_WS_FORWARD 3   /* fqt_binary_forward; cfg may be NULL for this one */
 int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
                        size_t *bytes);
+
+/* Prepares a FQT_WS_QUANTIZE or FQT_WS_LAYER workspace for use: zero-fills its first
+ * FQT_WS_STATE_BYTES with one small kernel on hip_stream (no memset node, so it may be
+ * captured in a HIP graph).  ws: device pointer, 256-byte aligned; ws_bytes >=
+ * FQT_WS_STATE_BYTES (FQT_E_WORKSPACE otherwise).  Not a statement of the paper: the
+ * statistics combine group keys with atomics, which need a zeroed target. */
+int fqt_workspace_init(void *ws, size_t ws_bytes, void *hip_stream);
 
 /* AGP + SCQ quantization of dY (Section 5.2 AGP; Section 5.3 SCQ; Appendix C Alg. 1
  * pruner, PSQ/PCQ, row/column encoders).  Per-sample and per-channel range R = max - min
@@ -192,9 +206,11 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
  *   with c_X[k] = sum_r s_X[r][k] (the zero-point term).
  * Computed on int8 MFMA from q->pcq_codes and the packed signs, which are expanded to
  * +-1 bytes in registers, in slices of N*Ho*Wo whose partial sums meet in the workspace.
- * xsign: the output of fqt_pack_input_signs for the layer's X.  dW: float [D][C*kh*kw].  I_out (optional): int32 [D][C*kh*kw] receives
- * I (0 in pruned rows).  ws: >= fqt_workspace_size(FQT_WS_GEMM_DW) bytes, 256-byte
- * aligned. */
+ * xsign: the output of fqt_pack_input_signs for the layer's X.  dW: float [D][C*kh*kw].
+ * I_out (optional): int32 [D][C*kh*kw] receives I (0 in pruned rows).
+ * ws: >= fqt_workspace_size(FQT_WS_GEMM_DW) bytes, 256-byte aligned.
+ * I is exact in int32 only while (2^b - 1) * N*Ho*Wo < 2^31: larger layers return
+ * FQT_E_SHAPE (here and in fqt_layer_backward). */
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
                        const fqt_qgrad *q, const uint64_t *xsign, float *dW, int32_t *I_out,
                        void *ws, size_t ws_bytes, void *hip_stream);

@@ -431,7 +431,7 @@ class Backward:
 
 
 def layer_backward(x, w, dy, bits, mode=AGP_BERNOULLI, seed=0, step=0, layer_id=0,
-                   stride=(1, 1), pad=(0, 0)):
+                   stride=(1, 1), pad=(0, 0), dw_channels=None):
     """Backward of a binary linear/conv layer under 1-bit FQT (Section 5.2 Eq. 21 with
     Section 5.3's SCQ form; Appendix C, Alg. 1 backward).
 
@@ -444,6 +444,10 @@ def layer_backward(x, w, dy, bits, mode=AGP_BERNOULLI, seed=0, step=0, layer_id=
     dW has w's shape, dX has x's shape (both float64 here).  Pruned channels give
     zero rows of dW and pruned samples zero samples of dX.  The conv dX goes
     through the paper's route: unfolded product, then the folder.
+
+    dw_channels (optional): output-channel ids; dW, I_dw and their terms are then returned
+    for those channels only, as [len(dw_channels)][C*kh*kw] rows in that order (for layers
+    whose full D x C*kh*kw float64 arrays would not fit a test's budget).
     """
     linear = np.asarray(x).ndim == 2
     x4, w4, dy4 = as_nchw(x), as_nchw(w), as_nchw(dy)
@@ -463,15 +467,19 @@ def layer_backward(x, w, dy, bits, mode=AGP_BERNOULLI, seed=0, step=0, layer_id=
 
     # dW: PCQ codes of kept channels against sign(unfold(X)), rescaled per channel.
     ch = qg.channels
-    kc = ch.kept_ids[:ch.count]
-    I_dw = np.zeros((D, K), dtype=np.int64)
-    I_dw[kc] = int_matmul(qg.pcq_rows, sx.T)
-    dW = np.zeros((D, K), dtype=np.float64)
-    t1w = np.zeros((D, K))
-    t2w = np.zeros((D, K))
-    t1w[kc] = ch.scale[kc, None].astype(np.float64) * I_dw[kc]
-    t2w[kc] = ch.offset[kc, None].astype(np.float64) * cx[None, :]
-    dW[kc] = t1w[kc] + t2w[kc]
+    rows = np.arange(D) if dw_channels is None else np.asarray(dw_channels, dtype=np.int64)
+    slot_of = {int(d): j for j, d in enumerate(ch.kept_ids[:ch.count])}   # row of pcq_rows
+    live = np.array([int(d) in slot_of for d in rows], dtype=bool)        # kept channels
+    kept_rows = np.array([slot_of[int(d)] for d in rows[live]], dtype=np.int64)
+    kd = rows[live]
+    I_dw = np.zeros((rows.size, K), dtype=np.int64)
+    I_dw[live] = int_matmul(qg.pcq_rows[kept_rows], sx.T)
+    dW = np.zeros((rows.size, K), dtype=np.float64)
+    t1w = np.zeros((rows.size, K))
+    t2w = np.zeros((rows.size, K))
+    t1w[live] = ch.scale[kd, None].astype(np.float64) * I_dw[live]
+    t2w[live] = ch.offset[kd, None].astype(np.float64) * cx[None, :]
+    dW[live] = t1w[live] + t2w[live]
 
     # dX: PSQ codes of kept samples against sign(Theta), dequantized, unfolded product, fold.
     sm = qg.samples
@@ -491,7 +499,10 @@ def layer_backward(x, w, dy, bits, mode=AGP_BERNOULLI, seed=0, step=0, layer_id=
     t1x[ks] = sm.scale[ks, None, None, None].astype(np.float64) * I_dx[ks]
     t2x[ks] = sm.offset[ks, None, None, None].astype(np.float64) * c_dx[None]
 
-    wshape = (D, C) if linear else (D, C, kh, kw)
+    if dw_channels is None:
+        wshape = (D, C) if linear else (D, C, kh, kw)
+    else:
+        wshape = (rows.size, K)
     xshape = (N, C) if linear else (N, C, H, W)
     return Backward(qgrad=qg, xbits=xbits, wbits=wbits, xsign_colsum=cx, wsign_colsum=cw,
                     I_dw=I_dw, I_dx=I_dx, c_dx=c_dx,

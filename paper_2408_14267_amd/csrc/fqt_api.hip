@@ -171,6 +171,12 @@ int check_cfg(const fqt_quant_cfg *c, const Layer &) {
   return FQT_OK;
 }
 
+// The dW product keeps I = sum_r q s in int32 (MFMA accumulators, code sums, the b = 8
+// bias term): |I| <= (2^b - 1) * N*Ho*Wo must stay below 2^31.
+int check_dw_range(const Layer &L, const fqt_quant_cfg &c) {
+  return int64_t((1 << c.bits) - 1) * L.R > LIMIT31 ? FQT_E_SHAPE : FQT_OK;
+}
+
 size_t quant_ws_bytes(const Layer &L) {
   Carver c{nullptr};
   QuantWs q;
@@ -233,6 +239,13 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
   return FQT_OK;
 }
 
+int fqt_workspace_init(void *ws, size_t ws_bytes, void *hip_stream) {
+  if (!ws) return FQT_E_NULL;
+  if (!aligned(ws, 256)) return FQT_E_ALIGN;
+  if (ws_bytes < FQT_WS_STATE_BYTES) return FQT_E_WORKSPACE;
+  return launch_state_clear(ws, static_cast<hipStream_t>(hip_stream));
+}
+
 int fqt_agp_scq_quantize(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *dY,
                          const fqt_qgrad *out, void *ws, size_t ws_bytes, void *hip_stream) {
   Layer L;
@@ -279,6 +292,7 @@ int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
   FQT_TRY(check_qgrad(q, false, true));
+  FQT_TRY(check_dw_range(L, *cfg));
   if (!xsign || !dW || !ws) return FQT_E_NULL;
   if (!aligned(xsign, 8) || !aligned(dW, 4) || (I_out && !aligned(I_out, 4)) ||
       !aligned(ws, 256))
@@ -332,6 +346,7 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   Layer L;
   FQT_TRY(make_layer(desc, &L));
   FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_dw_range(L, *cfg));
   if (!X || !W || !dY || !dX || !dW || !ws) return FQT_E_NULL;
   if (!aligned(dY, 16) || !aligned(X, dtype_size(L.x_t)) || !aligned(W, dtype_size(L.w_t)) ||
       !aligned(dX, dtype_size(L.dx_t)) || !aligned(dW, 4) || !aligned(ws, 256))

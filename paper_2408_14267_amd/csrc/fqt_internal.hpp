@@ -102,6 +102,8 @@ struct SignJob {
   int32_t *wlsum;
   bool done;
 };
+// Zero-fills the FQT_WS_STATE_BYTES of state at the start of a quantize / layer workspace.
+int launch_state_clear(void *state, hipStream_t s);
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
                     const QuantWs &w, hipStream_t s, SignJob *signs = nullptr);
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,

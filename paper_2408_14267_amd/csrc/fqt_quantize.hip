@@ -1332,6 +1332,14 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
   }
 }
 
+// Zero-fill of a quantize / layer workspace's state bytes (the merged group keys): one
+// 16-byte store per thread.  A kernel, not hipMemsetAsync, so that a captured graph replays
+// it like any other node.
+__global__ __launch_bounds__(256) void k_state_clear(uint4 *state, uint32_t n16) {
+  const uint32_t e = blockIdx.x * 256 + threadIdx.x;
+  if (e < n16) state[e] = make_uint4(0u, 0u, 0u, 0u);
+}
+
 template <int GP, int NT>
 int launch_select(const SelectArgs &sa, hipStream_t s) {
   const size_t lds = size_t(GP) * sizeof(uint64_t);
@@ -1365,6 +1373,13 @@ uint32_t stats_rows_per_block(const Layer &L) {
 int64_t stats_row_blocks(const Layer &L) {
   const int64_t rs = stats_rows_per_block(L);
   return (L.Wr + rs - 1) / rs;
+}
+
+int launch_state_clear(void *state, hipStream_t s) {
+  constexpr uint32_t n16 = FQT_WS_STATE_BYTES / 16;
+  hipLaunchKernelGGL(k_state_clear, dim3((n16 + 255) / 256), dim3(256), 0, s,
+                     static_cast<uint4 *>(state), n16);
+  return last_launch_status();
 }
 
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
@@ -1505,7 +1520,12 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     } else if (gmax <= 4096) st = launch_select<4096, 1024>(sa, s);
     else st = launch_select<16384, 1024>(sa, s);
   }
-  if (st != FQT_OK) return st;
+  if (st != FQT_OK) {
+    // The statistics merged their keys but no selection will read and clear them: clear
+    // them here, so that the workspace stays fit for the next call.
+    if (merged) launch_state_clear(w.mkeys, s);
+    return st;
+  }
 
   // One block per 64 x 64 tile.  With channels contiguous in dY (P = 1), the channel
   // tiles go fastest, so the blocks in flight read whole rows of dY in order.

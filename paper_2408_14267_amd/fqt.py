@@ -28,7 +28,7 @@ FQT_MAX_AGP_GROUPS = 16384
 EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_agp_scq_quantize",
             "fqt_pack_bits", "fqt_pack_input_signs", "fqt_binary_gemm_dw", "fqt_pack_weight_signs",
             "fqt_binary_gemm_dx",
-            "fqt_layer_backward", "fqt_binary_forward")
+            "fqt_layer_backward", "fqt_binary_forward", "fqt_workspace_init")
 
 
 class FqtError(RuntimeError):
@@ -70,6 +70,7 @@ def _load():
         "fqt_qgrad_words": (c_int, [D, Q, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64),
                                     POINTER(c_int64)]),
         "fqt_workspace_size": (c_int, [D, Q, c_int32, POINTER(c_size_t)]),
+        "fqt_workspace_init": (c_int, [c_void_p, c_size_t, c_void_p]),
         "fqt_agp_scq_quantize": (c_int, [D, Q, c_void_p, G, c_void_p, c_size_t, c_void_p]),
         "fqt_pack_bits": (c_int, [c_void_p, c_int32, c_int64, c_int64, c_int64, c_int32, D,
                                   c_void_p, c_void_p, c_void_p]),
@@ -150,6 +151,11 @@ def fqt_workspace_size(desc, cfg, which=FQT_WS_LAYER):
     return n.value
 
 
+def fqt_workspace_init(ws, stream=None):
+    _check(_lib.fqt_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "fqt_workspace_init")
+
+
 def fqt_agp_scq_quantize(desc, cfg, dY, qgrad, ws, stream=None):
     _check(_lib.fqt_agp_scq_quantize(desc, cfg, _ptr(dY), ctypes.byref(qgrad.struct), _ptr(ws),
                                      ws.numel() * ws.element_size(), _stream(stream)),
@@ -221,8 +227,12 @@ class QGrad:
             self.pcq_offset, self.pcq_prob)))
 
 
-def workspace(desc, cfg, which=FQT_WS_LAYER, device="cuda"):
-    """A 256-byte aligned uint8 workspace tensor of the size the library asks for, zero-filled
-    (quantize and layer workspaces keep zeroed state between calls in their first bytes)."""
+def workspace(desc, cfg, which=FQT_WS_LAYER, device="cuda", stream=None):
+    """A 256-byte aligned uint8 workspace tensor of the size the library asks for; quantize
+    and layer workspaces go through fqt_workspace_init (their first bytes hold zeroed state
+    between calls)."""
     n = fqt_workspace_size(desc, cfg, which)
-    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(n, 1), dtype=torch.uint8, device=device)
+    if which in (FQT_WS_QUANTIZE, FQT_WS_LAYER):
+        fqt_workspace_init(ws, stream)
+    return ws

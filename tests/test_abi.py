@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     lib = ctypes.CDLL(fqt.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -138,3 +138,38 @@ def test_forward_workspace_and_validation():
     st = lib.fqt_binary_forward(ctypes.byref(d), fake, fake, ctypes.c_void_p((1 << 20) + 2),
                                 fake, None, fake, n, None)
     assert st == fqt.FQT_E_ALIGN
+
+
+def test_workspace_init_validation():
+    lib = fqt._lib
+    fake = ctypes.c_void_p(1 << 20)          # never dereferenced: validation fails first
+    assert lib.fqt_workspace_init(None, 1 << 20, None) == fqt.FQT_E_NULL
+    assert lib.fqt_workspace_init(ctypes.c_void_p((1 << 20) + 16), 1 << 20, None) == fqt.FQT_E_ALIGN
+    assert lib.fqt_workspace_init(fake, fqt.FQT_WS_STATE_BYTES - 1, None) == fqt.FQT_E_WORKSPACE
+
+
+@pytest.mark.parametrize("bits,n,h,ok", [(8, 128, 65793, True), (8, 5, 1684301, False),
+                                         (7, 8, 2113665, True), (7, 11, 1537211, False)])
+def test_dw_integer_range_rejected_before_launch(bits, n, h, ok):
+    """The dW integer I = sum_r q s reaches (2^b - 1) * N*Ho*Wo; layers where that exceeds
+    2^31 - 1 are refused (FQT_E_SHAPE) by the dW product and the layer backward, before any
+    launch; the quantizer alone still accepts them.  The rows N*Ho*Wo sit on either side of
+    floor((2^31 - 1) / (2^b - 1)): 8421504 / 8421505 for b = 8, 16909320 / 16909321 for
+    b = 7 (1x1 convolutions over h x 1 maps; b <= 6 cannot reach the bound within the
+    code-array size limit)."""
+    lib = fqt._lib
+    d = fqt.layer_desc(LayerShape("c", "conv2d", n, 1, 1, h, 1))
+    R = n * h
+    assert (((1 << bits) - 1) * R <= (1 << 31) - 1) == ok
+    c = fqt.quant_cfg(bits, fqt.FQT_AGP_OFF)
+    fake = ctypes.c_void_p(1 << 20)
+    q = fqt.fqt_qgrad(*([1 << 20] * 14))
+    st_dw = lib.fqt_binary_gemm_dw(ctypes.byref(d), ctypes.byref(c), ctypes.byref(q), fake,
+                                   fake, None, fake, 0, None)
+    st_layer = lib.fqt_layer_backward(ctypes.byref(d), ctypes.byref(c), fake, fake, fake, fake,
+                                      fake, fake, 0, None)
+    if ok:       # past the range check: the zero-byte workspace is what fails
+        assert st_dw == fqt.FQT_E_WORKSPACE and st_layer == fqt.FQT_E_WORKSPACE
+    else:
+        assert st_dw == fqt.FQT_E_SHAPE and st_layer == fqt.FQT_E_SHAPE
+    fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE)       # the quantizer has no such bound

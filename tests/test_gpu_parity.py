@@ -7,6 +7,7 @@ outputs of both products.  Rescaled float32 gradients: |gpu - oracle| <=
 stays meaningful where the two terms cancel.
 """
 import sys
+from dataclasses import replace
 
 import numpy as np
 import pytest
@@ -111,6 +112,32 @@ CASES = [
     ("linear_geometric_large_sorted_b3", LayerShape("fc", "linear", 1500, 8, 40), 3, 0,
      Recipe("sample_geometric", ratio=0.97), "f32"),
 ]
+
+
+# The layers of the benchmarked networks at their real shapes.
+_CH15 = Recipe("channel_lognormal", sigma=1.5)
+_VGG = {L.name: L for L in WORKLOADS["vgg16_224_bf16"].layers}
+WORKLOAD_CASES = [
+    # VGG-16 at 224 x 224 (bf16 x / dy / dx, b = 2, per-channel lognormal(0, 1.5) scale), at
+    # batch 2: maps of 224^2 and 112^2 pixels take the per-plane statistics in bf16.
+    ("vgg16_224_conv1_n2_bf16", replace(_VGG["conv1"], N=2),
+     2, 0, _CH15, "bf16"),
+    ("vgg16_224_conv2_n2_bf16", replace(_VGG["conv2"], N=2),
+     2, 0, _CH15, "bf16"),
+    ("vgg16_224_conv3_n2_bf16", replace(_VGG["conv3"], N=2),
+     2, 0, _CH15, "bf16"),
+    # 16384 dX tiles with bf16 output: the dX product's four-tiles-per-block form in bf16.
+    ("conv_wide_dx_bf16_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2,
+     0, _CH15, "bf16"),
+    # A point of the binary GEMM sweep as a layer (M = N = 1024, K = 2304 rows) at b = 4 with
+    # Bernoulli AGP.
+    ("gemm_sweep_1024x1024x2304_b4", LayerShape("g", "linear", 2304, 1024, 1024), 4, 0,
+     Recipe("sample_lognormal", sigma=1.5), "f32"),
+]
+# Every layer of ResNet-18 (ImageNet stem) at 32 x 32, batch 128, b = 4, Student-t(3) dY drawn
+# with data seed = layer index, as the network suite runs it.
+RESNET_CASES = [(f"resnet18_{i:02d}_{L.name}", L, i) for i, L in
+                enumerate(WORKLOADS["resnet18_32px"].layers)]
 
 
 def _announce(msg):
@@ -229,11 +256,14 @@ def _check_signs(fqt, ref, desc, layer, X, W, x_dt):
 @pytest.mark.parametrize("name,layer,bits,mode,recipe,dtype", CASES, ids=[c[0] for c in CASES])
 def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
     _announce(f"[gpu parity] {name}: {layer} b={bits} mode={mode} {dtype}")
-    fqt, ref, desc, cfg, X, W, dY = _run_case(layer, bits, mode, recipe, dtype)
+    _check_case(layer, bits, mode, recipe, dtype)
+
+
+def _check_case(layer, bits, mode, recipe, dtype, **kw):
+    fqt, ref, desc, cfg, X, W, dY = _run_case(layer, bits, mode, recipe, dtype, **kw)
     x_dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
     q = _check_quantize(fqt, ref, desc, cfg, dY, layer, bits)
     xs, xsum, wsb, wlsum = _check_signs(fqt, ref, desc, layer, X, W, x_dt)
-
     D, K = layer.D, layer.C * layer.kh * layer.kw
     dW = torch.empty(D, K, dtype=torch.float32, device="cuda")
     I_dw = torch.empty(D, K, dtype=torch.int32, device="cuda")
@@ -246,8 +276,8 @@ def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
     assert np.array_equal(I_dx.cpu().numpy(), ref.I_dx), "dX integer product"
     _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
     _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 2.0 ** -8 if dtype == "bf16" else 1e-5, "dX")
-
-    # The whole-layer entry point gives the same bits as the component calls.
+    # The whole-layer entry point (the launch configuration of the network suites) gives the
+    # same bits as the component calls.
     dX2 = torch.empty_like(dX)
     dW2 = torch.empty_like(dW)
     fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX2, dW2, fqt.workspace(desc, cfg))
@@ -255,6 +285,58 @@ def test_kernels_match_oracle(name, layer, bits, mode, recipe, dtype):
     assert torch.equal(dX2.view(torch.int16 if dtype == "bf16" else torch.int32),
                        dX.view(torch.int16 if dtype == "bf16" else torch.int32))
     assert torch.equal(dW2.view(torch.int32), dW.view(torch.int32))
+    return ref
+
+
+@pytest.mark.parametrize("name,layer,bits,mode,recipe,dtype", WORKLOAD_CASES,
+                         ids=[c[0] for c in WORKLOAD_CASES])
+def test_workload_layers_match_oracle(name, layer, bits, mode, recipe, dtype):
+    """Layers of the benchmarked configurations at their real geometry (smaller batch where
+    the oracle needs it), compared element by element as in test_kernels_match_oracle."""
+    _announce(f"[gpu parity] workload layer {name}: {layer} b={bits} {dtype}")
+    _check_case(layer, bits, mode, recipe, dtype)
+
+
+@pytest.mark.parametrize("name,layer,index", RESNET_CASES, ids=[c[0] for c in RESNET_CASES])
+def test_resnet18_layers_match_oracle(name, layer, index):
+    """Every ResNet-18 layer at batch 128 (the network suite's shapes, dY drawn as it draws
+    them: Student-t(3), data seed and layer id = layer index), compared in full."""
+    wl = WORKLOADS["resnet18_32px"]
+    _announce(f"[gpu parity] {name}: {layer}")
+    _check_case(layer, wl.bits, wl.agp_mode, wl.recipe, wl.dtype, seed=wl.philox_seed, step=0,
+                layer_id=index, data_seed=index)
+
+
+def test_vgg16_fc6_bf16_sampled():
+    """VGG-16 fc6 (25088 -> 4096, batch 64, bf16 x / dy / dx, b = 2, per-channel lognormal
+    dY) through fqt_layer_backward: the selection, scales and codes bit for bit, dX in full,
+    and dW on 16 sampled output channels (kept and pruned, first and last), against the
+    oracle's rows for those channels."""
+    fqt = _fqt()
+    wl = WORKLOADS["vgg16_224_bf16"]
+    layer = _VGG["fc6"]
+    _announce(f"[gpu parity] fc6 sampled: {layer}")
+    x, w, dy = draw_layer(layer, wl.recipe, 6, "bf16")
+    bits, seed, step, lid = wl.bits, 3, 1, 13
+    qref = ofqt.agp_scq_quantize(dy, bits, wl.agp_mode, seed, step, lid)
+    ch = qref.channels
+    kept, pruned = ch.kept_ids[:ch.count], ch.kept_ids[ch.count:]
+    assert kept.size >= 7 and pruned.size >= 7
+    chans = np.unique(np.concatenate([[0, layer.D - 1], kept[:7], pruned[:7]]))
+    ref = ofqt.layer_backward(x, w, dy, bits, wl.agp_mode, seed=seed, step=step, layer_id=lid,
+                              dw_channels=chans)
+    desc = fqt.layer_desc(layer, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+    cfg = fqt.quant_cfg(bits, wl.agp_mode, seed, step, lid)
+    X, W, dY = _to_dev(x, "bf16"), _to_dev(w, "f32"), _to_dev(dy, "bf16")
+    _check_quantize(fqt, ref, desc, cfg, dY, layer, bits)
+    dX = torch.empty(X.shape, dtype=torch.bfloat16, device="cuda")
+    dW = torch.empty(W.shape, dtype=torch.float32, device="cuda")
+    fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, fqt.workspace(desc, cfg))
+    torch.cuda.synchronize()
+    _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 2.0 ** -8, "dX")
+    rows = dW[torch.from_numpy(chans).cuda()]
+    _assert_rescaled(rows, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW sampled rows")
+    assert not rows[torch.from_numpy(~np.isin(chans, kept)).cuda()].any(), "pruned dW rows"
 
 
 def test_full_vgg_cifar_conv_layer():
@@ -329,9 +411,9 @@ def test_dw_product_16384_cube_sampled():
 
 
 def test_layer_backward_graph_replays_match_eager():
-    """fqt_layer_backward captured in a HIP graph (forked second stream included) and
-    replayed several times, with eager calls on other data and synchronizations between
-    the replays: every replay equals the eager result bit for bit."""
+    """fqt_layer_backward captured in a HIP graph on a side stream and replayed several
+    times, with eager calls on other data and synchronizations between the replays: every
+    replay equals the eager result bit for bit."""
     wl = WORKLOADS["resnet18_32px"]
     layer = wl.layers[3]
     _announce(f"[gpu parity] graph replay {layer}")
@@ -488,3 +570,28 @@ def test_forward_matches_oracle(name, layer, dtype):
         g = Y.float().cpu().numpy().astype(np.float64)
         rel = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
         assert (np.abs(g - ref.Y) <= rel * np.abs(ref.Y)).all(), "forward output"
+
+
+def test_garbage_workspace_after_init():
+    """A layer workspace filled with garbage bytes, then prepared by fqt_workspace_init, gives
+    the oracle's result; a second call on it (state left by the first) gives the same bits."""
+    fqt = _fqt()
+    layer = WORKLOADS["vgg_cifar_conv3x3_256"].layers[0]
+    wl = WORKLOADS["vgg_cifar_conv3x3_256"]
+    _announce("[gpu parity] garbage workspace + fqt_workspace_init")
+    fqt_, ref, desc, cfg, X, W, dY = _run_case(layer, wl.bits, wl.agp_mode, wl.recipe, wl.dtype,
+                                              seed=wl.philox_seed, step=0, layer_id=0,
+                                              data_seed=wl.seed)
+    n = fqt.fqt_workspace_size(desc, cfg, fqt.FQT_WS_LAYER)
+    ws = torch.full((n,), 0xAB, dtype=torch.uint8, device="cuda")
+    fqt.fqt_workspace_init(ws)
+    dX, dW = torch.empty_like(X), torch.empty_like(W)
+    outs = []
+    for _ in range(2):
+        fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws)
+        torch.cuda.synchronize()
+        _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
+        _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 1e-5, "dX")
+        outs.append((dX.clone(), dW.clone()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    assert torch.count_nonzero(ws[:fqt.FQT_WS_STATE_BYTES]).item() == 0

@@ -112,11 +112,19 @@ def test_linear_products_plain_matmul():
     np.testing.assert_allclose(bw.dX, gs[:, :, 0, 0] @ sw, rtol=1e-12, atol=1e-9)
 
 
-def test_pruned_groups_give_zero_rows():
+@pytest.mark.parametrize("seed", [1, 11])
+def test_pruned_groups_give_zero_rows(seed):
+    """Seed 1 keeps 2 of 8 samples and 3 of 8 channels; seed 11's Bernoulli draws keep no
+    sample at all (a valid outcome of the masks), so every sample of dX is zero."""
     layer = LayerShape("c3", "conv2d", 8, 4, 8, 4, 4, 3, 3, 1, 1, 1, 1)
-    (x, w, dy), bw = _run(layer, 4, seed=11)
+    (x, w, dy), bw = _run(layer, 4, seed=seed)
     qg = bw.qgrad
-    assert 0 < qg.samples.count < 8 or True
+    if seed == 1:
+        assert 0 < qg.samples.count < 8 and 0 < qg.channels.count < 8
+        assert np.any(bw.dX != 0) and np.any(bw.dW != 0)
+    else:
+        assert qg.samples.count == 0 and 0 < qg.channels.count < 8
+        assert not np.any(bw.dX)
     dW = bw.dW.reshape(8, -1)
     for d in range(8):
         if not qg.channels.keep[d]:
@@ -228,3 +236,21 @@ def test_agp_variance_eq24_regime():
     eq24 = D / (4 * B * B) * float((np.sort(st.R_s.astype(np.float64))[-N // b:] ** 2).sum())
     assert exact.sum() <= eq24 * 1.05
     assert exact.sum() < D / 4 * float((st.R_s.astype(np.float64) ** 2).sum())
+
+
+def test_dw_channels_rows_equal_the_full_result():
+    """layer_backward(dw_channels=...) returns exactly the listed rows of the full dW (kept
+    and pruned channels, repeated and out of order), and leaves dX unchanged."""
+    layer = LayerShape("c3", "conv2d", 6, 4, 9, 5, 5, 3, 3, 1, 1, 1, 1)
+    x, w, dy = draw_layer(layer, Recipe("channel_lognormal", sigma=1.5), 3)
+    full = fqt.layer_backward(x, w, dy, 2, seed=4, stride=layer.stride, pad=layer.pad)
+    ch = full.qgrad.channels
+    assert 0 < ch.count < 9
+    rows = np.array([8, 0, int(ch.kept_ids[0]), int(ch.kept_ids[-1]), 8, 3])
+    part = fqt.layer_backward(x, w, dy, 2, seed=4, stride=layer.stride, pad=layer.pad,
+                              dw_channels=rows)
+    K = 4 * 9
+    for got, want in ((part.dW, full.dW), (part.I_dw, full.I_dw), (part.dW_t1, full.dW_t1),
+                      (part.dW_t2, full.dW_t2)):
+        np.testing.assert_array_equal(got, np.asarray(want).reshape(9, K)[rows])
+    np.testing.assert_array_equal(part.dX, full.dX)
