@@ -258,6 +258,23 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
                        const void *W, const void *dY, void *dX, float *dW, void *ws,
                        size_t ws_bytes, void *hip_stream);
 
+/* fqt_layer_backward for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same computation and
+ * results, with the library's own workspace, a static device array of
+ * FQT_NOALLOC_SCRATCH_BYTES that every GPU the library runs on holds until the process
+ * ends.  The call allocates and frees nothing.  Layers whose FQT_WS_LAYER workspace exceeds
+ * that size return FQT_E_WORKSPACE before any launch (at 64 MiB: the 256 -> 256 3x3 conv on
+ * 8x8 maps at batch 128, every ResNet-18 layer at batch 128, VGG-16 conv11-13 and fc7/fc8 at
+ * batch 64 fit; VGG-16 conv1-10 and fc6 at batch 64 do not).  Each call first clears the
+ * array's state bytes with a fill kernel on hip_stream.  All calls on one GPU share its
+ * array: calls that overlap on one GPU (other streams, other host threads) race and give
+ * wrong results; serialise them.  Other arguments, layouts and errors as in
+ * fqt_layer_backward; FQT_E_HIP if the array's device address cannot be obtained. */
+#define FQT_NOALLOC_SCRATCH_BYTES (64u << 20)
+int fqt_layer_backward_noalloc(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                               const void *X, const void *W, const void *dY, void *dX, float *dW,
+                               void *hip_stream);
+
 /* Binary layer forward (Section 5.1: the output is sign(H_prev) times sign(Theta), scaled
  * per output channel by the learnable Gamma; Appendix C, Alg. 1 forward, with the Unfolder
  * for convolutions):

@@ -1,5 +1,7 @@
 // C ABI of libfqt: argument validation, workspace carving and the entry points.
 // Every check runs on the host before anything is launched.
+#include <mutex>
+
 #include "fqt_internal.hpp"
 
 namespace fqt {
@@ -189,6 +191,52 @@ void carve_quant_ws(void *ws, const Layer &L, QuantWs *q) {
   carve_quant_ws(&c, L, q);
 }
 
+namespace {
+
+int layer_backward_run(const Layer &L, const fqt_quant_cfg &cfg, const void *X, const void *W,
+                       const void *dY, void *dX, float *dW, void *ws, hipStream_t s);
+
+// Validation shared by the layer backward entry points (everything but the workspace).
+int check_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
+                         const void *W, const void *dY, const void *dX, const float *dW,
+                         Layer *L) {
+  FQT_TRY(make_layer(desc, L));
+  FQT_TRY(check_cfg(cfg, *L));
+  FQT_TRY(check_dw_range(*L, *cfg));
+  if (!X || !W || !dY || !dX || !dW) return FQT_E_NULL;
+  if (!aligned(dY, 16) || !aligned(X, dtype_size(L->x_t)) || !aligned(W, dtype_size(L->w_t)) ||
+      !aligned(dX, dtype_size(L->dx_t)) || !aligned(dW, 4))
+    return FQT_E_ALIGN;
+  if (L->kh * L->kw > 64) return FQT_E_SHAPE;
+  return FQT_OK;
+}
+
+// The workspace of fqt_layer_backward_noalloc: one array per GPU, held until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device memory: its device
+// address comes from hipGetSymbolAddress, once per device with that device current, and
+// only that address is ever handed to a kernel.
+static __device__ __align__(256) unsigned char scratch[FQT_NOALLOC_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex scratch_mutex;
+void *scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+
+int scratch_of_current_device(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FQT_E_HIP;
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return FQT_E_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FQT_E_HIP;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return FQT_OK;
+}
+
+}  // namespace
+
 }  // namespace fqt
 
 using namespace fqt;
@@ -344,18 +392,38 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
                        const void *W, const void *dY, void *dX, float *dW, void *ws,
                        size_t ws_bytes, void *hip_stream) {
   Layer L;
-  FQT_TRY(make_layer(desc, &L));
-  FQT_TRY(check_cfg(cfg, L));
-  FQT_TRY(check_dw_range(L, *cfg));
-  if (!X || !W || !dY || !dX || !dW || !ws) return FQT_E_NULL;
-  if (!aligned(dY, 16) || !aligned(X, dtype_size(L.x_t)) || !aligned(W, dtype_size(L.w_t)) ||
-      !aligned(dX, dtype_size(L.dx_t)) || !aligned(dW, 4) || !aligned(ws, 256))
-    return FQT_E_ALIGN;
+  FQT_TRY(check_layer_backward(desc, cfg, X, W, dY, dX, dW, &L));
+  if (!ws) return FQT_E_NULL;
+  if (!aligned(ws, 256)) return FQT_E_ALIGN;
   if (ws_bytes < carve_layer_ws(nullptr, L, *cfg, nullptr)) return FQT_E_WORKSPACE;
+  return layer_backward_run(L, *cfg, X, W, dY, dX, dW, ws, static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_layer_backward_noalloc(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                               const void *X, const void *W, const void *dY, void *dX, float *dW,
+                               void *hip_stream) {
+  Layer L;
+  FQT_TRY(check_layer_backward(desc, cfg, X, W, dY, dX, dW, &L));
+  if (carve_layer_ws(nullptr, L, *cfg, nullptr) > FQT_NOALLOC_SCRATCH_BYTES)
+    return FQT_E_WORKSPACE;
+  void *ws = nullptr;
+  FQT_TRY(scratch_of_current_device(&ws));
+  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  // The array keeps whatever the last call on this GPU left in it: clear the state bytes
+  // (the merged group keys) before the statistics combine into them.
+  FQT_TRY(launch_state_clear(ws, s));
+  return layer_backward_run(L, *cfg, X, W, dY, dX, dW, ws, s);
+}
+
+}  // extern "C"
+
+namespace fqt {
+namespace {
+int layer_backward_run(const Layer &L, const fqt_quant_cfg &cfg_, const void *X, const void *W,
+                       const void *dY, void *dX, float *dW, void *ws, hipStream_t s) {
+  const fqt_quant_cfg *cfg = &cfg_;
   LayerWs w;
   carve_layer_ws(ws, L, *cfg, &w);
-  const hipStream_t s = static_cast<hipStream_t>(hip_stream);
-  if (L.kh * L.kw > 64) return FQT_E_SHAPE;
   // Statistics, then the selection (whose launch also packs the sign operands when the
   // layer allows), the quantizer, both products.
   SignJob sj{X, W, w.xsign, w.wsb, w.wlsum, false};
@@ -372,6 +440,10 @@ int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
   return launch_products(L, *cfg, w.q, w.xsign, w.wsb, w.wlsum, dX, dW, w.dw_ws, w.qws.sslot,
                          w.qws.cslot, s);
 }
+}  // namespace
+}  // namespace fqt
+
+extern "C" {
 
 int fqt_binary_forward(const fqt_layer_desc *desc, const void *X, const void *W,
                        const float *gamma, void *Y, int32_t *I_out, void *ws, size_t ws_bytes,

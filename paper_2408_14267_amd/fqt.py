@@ -24,11 +24,13 @@ FQT_PACK_ALONG_ROWS, FQT_PACK_ALONG_COLS, FQT_PACK_IM2COL = 0, 1, 2
 FQT_WS_QUANTIZE, FQT_WS_LAYER, FQT_WS_GEMM_DW, FQT_WS_FORWARD = 0, 1, 2, 3
 FQT_WS_STATE_BYTES = 131072    # zeroed state at the start of quantize and layer workspaces
 FQT_MAX_BITS = 8
+FQT_NOALLOC_SCRATCH_BYTES = 64 << 20   # static workspace of fqt_layer_backward_noalloc
 FQT_MAX_AGP_GROUPS = 16384
 EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_agp_scq_quantize",
             "fqt_pack_bits", "fqt_pack_input_signs", "fqt_binary_gemm_dw", "fqt_pack_weight_signs",
             "fqt_binary_gemm_dx",
-            "fqt_layer_backward", "fqt_binary_forward", "fqt_workspace_init")
+            "fqt_layer_backward", "fqt_binary_forward", "fqt_workspace_init",
+            "fqt_layer_backward_noalloc")
 
 
 class FqtError(RuntimeError):
@@ -82,6 +84,8 @@ def _load():
                                        c_void_p]),
         "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
+        "fqt_layer_backward_noalloc": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p,
+                                               c_void_p, c_void_p]),
         "fqt_binary_forward": (c_int, [D, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
     }
@@ -194,6 +198,12 @@ def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):
     _check(_lib.fqt_layer_backward(desc, cfg, _ptr(X), _ptr(W), _ptr(dY), _ptr(dX), _ptr(dW),
                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "fqt_layer_backward")
+
+
+def fqt_layer_backward_noalloc(desc, cfg, X, W, dY, dX, dW, stream=None):
+    _check(_lib.fqt_layer_backward_noalloc(desc, cfg, _ptr(X), _ptr(W), _ptr(dY), _ptr(dX),
+                                           _ptr(dW), _stream(stream)),
+           "fqt_layer_backward_noalloc")
 
 
 def fqt_binary_forward(desc, X, W, gamma, Y, I_out, ws, stream=None):

@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     lib = ctypes.CDLL(fqt.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -118,6 +118,8 @@ def test_state_bytes_constant_matches_header():
     text = open(HEADER).read()
     m = re.search(r"#define FQT_WS_STATE_BYTES (\d+)", text)
     assert m and int(m.group(1)) == fqt.FQT_WS_STATE_BYTES
+    m = re.search(r"#define FQT_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == fqt.FQT_NOALLOC_SCRATCH_BYTES
     d = _desc()
     c = fqt.quant_cfg(4)
     assert fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE) > fqt.FQT_WS_STATE_BYTES
@@ -173,3 +175,26 @@ def test_dw_integer_range_rejected_before_launch(bits, n, h, ok):
     else:
         assert st_dw == fqt.FQT_E_SHAPE and st_layer == fqt.FQT_E_SHAPE
     fqt.fqt_workspace_size(d, c, fqt.FQT_WS_QUANTIZE)       # the quantizer has no such bound
+
+
+def test_noalloc_rejects_layers_beyond_its_scratch_before_launch():
+    """fqt_layer_backward_noalloc validates like fqt_layer_backward and refuses a layer whose
+    workspace exceeds the static scratch (VGG-16 conv2 at batch 64 needs 742 MiB) with
+    FQT_E_WORKSPACE, before it touches the device."""
+    lib = fqt._lib
+    fake = ctypes.c_void_p(1 << 20)
+    vgg = {L.name: L for L in WORKLOADS["vgg16_224_bf16"].layers}
+    d = fqt.layer_desc(vgg["conv2"], fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+    c = fqt.quant_cfg(2)
+    assert fqt.fqt_workspace_size(d, c) > fqt.FQT_NOALLOC_SCRATCH_BYTES
+    st = lib.fqt_layer_backward_noalloc(ctypes.byref(d), ctypes.byref(c), fake, fake, fake,
+                                        fake, fake, None)
+    assert st == fqt.FQT_E_WORKSPACE
+    d2 = _desc()
+    assert fqt.fqt_workspace_size(d2, fqt.quant_cfg(4)) <= fqt.FQT_NOALLOC_SCRATCH_BYTES
+    st = lib.fqt_layer_backward_noalloc(ctypes.byref(d2), ctypes.byref(c), None, fake, fake,
+                                        fake, fake, None)
+    assert st == fqt.FQT_E_NULL
+    st = lib.fqt_layer_backward_noalloc(ctypes.byref(d2), ctypes.byref(c), fake, fake,
+                                        ctypes.c_void_p((1 << 20) + 4), fake, fake, None)
+    assert st == fqt.FQT_E_ALIGN

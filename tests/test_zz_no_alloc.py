@@ -1,0 +1,63 @@
+"""fqt_layer_backward_noalloc (the entry point that allocates nothing, for callers that
+cannot call hipMalloc) against fqt_layer_backward on the same inputs, bit for bit: two calls
+in a row on the one static scratch array, the second on a smaller layer, then the first
+layer again (the array keeps the previous call's contents)."""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2408_14267_amd.workloads import WORKLOADS, LayerShape, Recipe, draw_layer
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # (layer, bits, agp mode, recipe, dtype)
+    (WORKLOADS["vgg_cifar_conv3x3_256"].layers[0], 4, 0,
+     WORKLOADS["vgg_cifar_conv3x3_256"].recipe, "f32"),
+    (LayerShape("c", "conv2d", 5, 7, 70, 9, 9, 3, 3, 1, 1, 1, 1), 3, 0,
+     Recipe("sample_lognormal", sigma=1.5), "f32"),
+    (WORKLOADS["vgg_cifar_conv3x3_256"].layers[0], 4, 0,
+     WORKLOADS["vgg_cifar_conv3x3_256"].recipe, "f32"),
+    (LayerShape("c", "conv2d", 8, 32, 64, 14, 14, 3, 3, 1, 1, 1, 1), 2, 0,
+     Recipe("channel_lognormal", sigma=1.5), "bf16"),
+    (LayerShape("fc", "linear", 37, 300, 77), 8, 0, Recipe("sample_lognormal", sigma=2.0), "f32"),
+]
+
+
+def _dev(a, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def test_noalloc_matches_layer_backward():
+    from paper_2408_14267_amd import fqt
+    view = {torch.float32: torch.int32, torch.bfloat16: torch.int16}
+    for i, (layer, bits, mode, recipe, dtype) in enumerate(CASES):
+        print(f"[no-alloc] call {i}: {layer} b={bits} {dtype}", flush=True)
+        sys.stdout.flush()
+        x, w, dy = draw_layer(layer, recipe, i, dtype)
+        dt = fqt.FQT_BF16 if dtype == "bf16" else fqt.FQT_F32
+        desc = fqt.layer_desc(layer, dt, dt, fqt.FQT_F32, dt)
+        cfg = fqt.quant_cfg(bits, mode, 5, i, 2)
+        X, W, dY = _dev(x, dtype), _dev(w, "f32"), _dev(dy, dtype)
+        dX_ref, dW_ref = torch.empty_like(X), torch.empty_like(W)
+        fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX_ref, dW_ref, fqt.workspace(desc, cfg))
+        dX, dW = torch.full_like(X, 3.0), torch.full_like(W, 3.0)
+        fqt.fqt_layer_backward_noalloc(desc, cfg, X, W, dY, dX, dW)
+        torch.cuda.synchronize()
+        assert torch.equal(dX.view(view[dX.dtype]), dX_ref.view(view[dX.dtype])), f"dX call {i}"
+        assert torch.equal(dW.view(torch.int32), dW_ref.view(torch.int32)), f"dW call {i}"
+        assert torch.count_nonzero(dW_ref).item() > 0
+
+
+def test_noalloc_refuses_a_layer_beyond_the_scratch():
+    from paper_2408_14267_amd import fqt
+    vgg = {L.name: L for L in WORKLOADS["vgg16_224_bf16"].layers}
+    desc = fqt.layer_desc(vgg["conv2"], fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+    cfg = fqt.quant_cfg(2)
+    t = torch.empty(16, device="cuda")
+    with pytest.raises(fqt.FqtError) as e:
+        fqt.fqt_layer_backward_noalloc(desc, cfg, t, t, t, t, t)
+    assert e.value.status == fqt.FQT_E_WORKSPACE
