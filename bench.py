@@ -3,13 +3,16 @@
 Workload: VGG-16 CIFAR-shaped 3x3 convolution 256 -> 256 on 8x8 maps, batch 128,
 fp32 X / W / dY (dY per-sample lognormal(0, 2) scale with 13 of 128 samples x100),
 AGP Bernoulli keeping 1/4 of the groups (b = 4), Philox seed 0.  A step is one
-fqt_layer_backward: group statistics, AGP selection, SR + bit-plane packing,
-sign packing of X (bit-im2col) and W, and both binary products with rescale.
+fqt_layer_backward: group statistics, AGP selection, SR + code packing, sign packing
+of X (bit-im2col) and W, and both binary products with rescale.
 
 Prints one JSON line: throughput in binary TOPS (2 x D*C*k*k*N*Ho*Wo binary
-multiply-accumulates per product, both products, per step time), the roofline
-of the dominant kernel timed with HIP events on its own stream, and the CPU
-oracle timed on a bounded sample on the host.
+multiply-accumulates per product, both products, per step time); the roofline of the
+step's dominant kernel (the products launch, timed alone with HIP events on its stream)
+and of the whole step; the linear 32x256x128 layer, and the ResNet-18 (32 px, batch 128)
+and VGG-16 (224 px, batch 64, bf16) backward passes over all their layers, eager and as
+one HIP graph; a cold-cache step time; and the CPU oracle timed on a bounded sample on
+the host, on one thread and on all of the process's cores.
 """
 import argparse
 import json
@@ -25,21 +28,17 @@ sys.path.insert(0, ROOT)
 WORKLOAD = "vgg_cifar_conv3x3_256"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
+SCRUB_BYTES = 1 << 30          # cold-cache runs overwrite this much (the last-level cache is 256 MB)
 
-# HBM traffic per launch from rocprofv3 counter runs of this benchmark (FETCH_SIZE and
-# WRITE_SIZE in KiB per dispatch, one run each), scaled by what the same counters read for
-# a 256 MiB device copy in those runs (FETCH_SIZE reads half the copied bytes).  The figures
-# are reported only while the kernel sources are byte-identical to the ones they were
-# measured on (TRAFFIC_DIGEST: sha256 over the names and contents of every file in csrc/).
-FETCH_SCALE = 262144.0 / 131086.7
+# HBM traffic per launch of the products kernel from rocprofv3 counter runs of this benchmark
+# (FETCH_SIZE and WRITE_SIZE in KiB per dispatch, one run each), scaled by what the same
+# counters read for a 256 MiB device copy in those runs.  Reported only while the kernel
+# sources are byte-identical to the ones they were measured on (TRAFFIC_DIGEST: sha256 over
+# the names and contents of every file in csrc/).
+FETCH_SCALE = 1.0
 WRITE_SCALE = 1.0
-TRAFFIC_DIGEST = "44a2b213ef2730474d4b393662918398bd0843d8c2cdcf0dcb3d3f939fde34e1"
-TRAFFIC = {
-    # entry: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch of its kernels
-    "gemm_dx": (2538.0, 8192.0),
-    "pack_x": (4143.3, 2304.0),
-    "pack_w": (1179.5, 585.0),
-}
+TRAFFIC_DIGEST = ""
+TRAFFIC = {}      # kernel: (FETCH_SIZE KiB, WRITE_SIZE KiB) per launch
 
 
 def sources_digest():
@@ -68,9 +67,14 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0,
-                   help="bound on the CPU oracle sample (seconds of work)")
+    p.add_argument("--cpu-seconds", type=float, default=8.0,
+                   help="bound on each CPU oracle leg (seconds of work)")
     p.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    p.add_argument("--no-networks", action="store_true",
+                   help="skip the ResNet-18 and VGG-16 whole-network totals")
+    p.add_argument("--cold", action="store_true",
+                   help="report the cold-cache step time as ms_per_step (1 GiB overwritten "
+                        "before every timed step) instead of the warm one")
     p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward",
                                        "table5"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
@@ -84,25 +88,33 @@ def parse():
     return p.parse_args()
 
 
-def cpu_baseline(x, w, dy, layer, wl, ops_per_step, budget_s):
-    """The oracle, as it stands, on the host cores: full layer backward repeated until
-    about `budget_s` seconds of work have been done (at least once)."""
-    from threadpoolctl import threadpool_info
+def cpu_legs(x, w, dy, layer, wl, ops_per_step, budget_s):
+    """The oracle, as it stands, on the host: a full layer backward repeated until about
+    `budget_s` seconds of work have been done (at least once), first with every thread pool
+    held to one thread (the paper times one core), then with the pools at the process's
+    cores.  Returns (one-thread leg, all-cores leg)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import fqt as ofqt
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        ofqt.layer_backward(x, w, dy, wl.bits, wl.agp_mode, seed=wl.philox_seed,
-                            stride=layer.stride, pad=layer.pad)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s:
-            break
-    threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
-    return {"value": ops_per_step * reps / el / 1e12, "unit": "TOPS", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{reps} full layer backward(s) of {WORKLOAD} in {el:.1f} s "
-                      f"({el / reps * 1e3:.0f} ms each; numpy, BLAS threads={threads})"}
+    cores = len(os.sched_getaffinity(0))
+
+    def run(threads):
+        with threadpool_limits(limits=threads):
+            used = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+            reps, t0 = 0, time.perf_counter()
+            while True:
+                ofqt.layer_backward(x, w, dy, wl.bits, wl.agp_mode, seed=wl.philox_seed,
+                                    stride=layer.stride, pad=layer.pad)
+                reps += 1
+                el = time.perf_counter() - t0
+                if el >= budget_s:
+                    break
+        return {"value": ops_per_step * reps / el / 1e12, "unit": "TOPS", "cores": used,
+                "kind": "oracle", "ms_per_step": el / reps * 1e3,
+                "sample": f"{reps} full layer backward(s) of {WORKLOAD} in {el:.1f} s "
+                          f"({el / reps * 1e3:.0f} ms each; numpy, thread pools at {used} "
+                          f"of the process's {cores} cores)"}
+    return run(1), run(cores)
 
 
 def _gen(torch, shape, dtype, dev, scale=None):
@@ -112,9 +124,114 @@ def _gen(torch, shape, dtype, dev, scale=None):
     return x.to(dtype)
 
 
+def _timed(torch, stream, fn, k):
+    """Mean ms of k calls of fn between two HIP events recorded on `stream`."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(k):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / k
+
+
+def _graph_of(torch, stream, fn, reps):
+    """A HIP graph of `reps` back-to-back calls of fn(stream), captured on a side stream."""
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        fn(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(reps):
+                fn(side)
+    torch.cuda.synchronize()
+    return g
+
+
+def network_layers(name, dev, stream, reps=10, graph=True, per_layer=None):
+    """Every layer backward of a network (inputs drawn on the GPU with the workload's recipe
+    distributions, one workspace shared by all layers): per-layer eager ms, the eager total,
+    and one HIP graph of the whole network's layer calls replayed (ms per pass)."""
+    import torch
+
+    from paper_2408_14267_amd import fqt
+    from paper_2408_14267_amd.workloads import WORKLOADS
+    torch.manual_seed(0)
+    wl = WORKLOADS[name]
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    calls, ws_bytes, rows = [], 0, []
+    for li, L in enumerate(wl.layers):
+        X = _gen(torch, L.x_shape, tdt, dev)
+        W = _gen(torch, L.w_shape, torch.float32, dev)
+        nd = len(L.dy_shape)
+        r = wl.recipe
+        if r.kind == "sample_lognormal":
+            sc = torch.exp(r.sigma * torch.randn((L.N,) + (1,) * (nd - 1), device=dev))
+            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
+        elif r.kind == "channel_lognormal":
+            sc = torch.exp(r.sigma * torch.randn((1, L.D) + (1,) * (nd - 2), device=dev))
+            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
+        else:
+            dY = torch.distributions.StudentT(r.df).sample(L.dy_shape).to(dev).to(tdt)
+        dX, dW = torch.empty_like(X), torch.empty_like(W)
+        if tdt == torch.bfloat16:
+            desc = fqt.layer_desc(L, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+        else:
+            desc = fqt.layer_desc(L)
+        cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, wl.philox_seed, 0, li)
+        ws_bytes = max(ws_bytes, fqt.fqt_workspace_size(desc, cfg))
+        calls.append((L, desc, cfg, X, W, dY, dX, dW))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    fqt.fqt_workspace_init(ws, stream)
+
+    def layer_fn(c, st):
+        L, desc, cfg, X, W, dY, dX, dW = c
+        fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st)
+
+    total_eager, ops = 0.0, 0.0
+    es = 2 if tdt == torch.bfloat16 else 4
+    for li, c in enumerate(calls):
+        L = c[0]
+        step = lambda: layer_fn(c, stream)
+        for _ in range(3):
+            step()
+        ms = _timed(torch, stream, step, reps)
+        total_eager += ms
+        ops += 4.0 * L.binary_macs()
+        mbytes = (L.N * L.D * L.Ho * L.Wo + 2 * L.N * L.C * L.H * L.W) * es + \
+            2 * L.D * L.C * L.kh * L.kw * 4
+        rows.append({"layer": li, "name": L.name, "ms": round(ms, 4),
+                     "binary_TOPS": round(4.0 * L.binary_macs() / ms / 1e9, 1),
+                     "min_bytes_MB": round(mbytes / 1e6, 2),
+                     "GBps_of_min_bytes": round(mbytes / ms / 1e6, 1)})
+        if per_layer:
+            per_layer({"suite": name, **rows[-1]})
+    out = {"layers": len(calls), "ms_eager": round(total_eager, 4),
+           "binary_TOPS_eager": round(ops / total_eager / 1e9, 1)}
+    if graph:
+        g = _graph_of(torch, stream, lambda st: [layer_fn(c, st) for c in calls], 1)
+        for _ in range(3):
+            g.replay()
+        ms_g = _timed(torch, stream, g.replay, reps)
+        out.update({"ms_graph": round(ms_g, 4), "binary_TOPS_graph": round(ops / ms_g / 1e9, 1)})
+    out["min_bytes_MB"] = round(sum(r["min_bytes_MB"] for r in rows), 1)
+    if name.startswith("resnet18"):
+        # The layers the paper quantizes: all but the stem conv, the fc and the 1x1 shortcuts.
+        sub = [r for r in rows if r["name"] not in ("conv1", "fc") and not r["name"].endswith(".down")]
+        out["quantized_subset"] = {"layers": len(sub),
+                                   "ms_eager": round(sum(r["ms"] for r in sub), 4)}
+    del calls, ws
+    torch.cuda.empty_cache()
+    return out, rows
+
+
 def suite(name, reps=10):
-    """Per-layer eager times of the layer backward over a whole network (inputs drawn on the
-    GPU with the workload's recipe distributions), or the dW binary GEMM sweep."""
+    """One JSON line per layer / point: a whole network's layer backwards (per-layer eager
+    times, then the totals eager and as one graph), the dW binary GEMM sweep, the binary
+    forward, or the Table 5 analogue."""
     import torch
 
     from paper_2408_14267_amd import fqt
@@ -212,7 +329,9 @@ def suite(name, reps=10):
             L = LayerShape(name="gemm", kind="linear", N=K, C=M, D=M)
             desc = fqt.layer_desc(L)
             cfg = fqt.quant_cfg(1, fqt.FQT_AGP_OFF, 0, 0, 0)
-            dY = _gen(torch, (K, M), torch.float32, dev)
+            # dY [K][M] ~ N(0,1) scaled per row by lognormal(0, 1.5)
+            dY = _gen(torch, (K, M), torch.float32, dev,
+                      torch.exp(1.5 * torch.randn((K, 1), device=dev)))
             X = _gen(torch, (K, M), torch.float32, dev)
             q = fqt.QGrad(desc, cfg, device=dev)
             qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
@@ -226,6 +345,13 @@ def suite(name, reps=10):
                 f()
             k = 3 if M * M * K > 2 ** 36 else reps
             tq, tp, tg = timed(qz, k), timed(px, k), timed(gd, k)
+            # the quantizer at b = 4 with Bernoulli AGP on the same dY
+            cfg4 = fqt.quant_cfg(4, fqt.FQT_AGP_BERNOULLI, 0, 0, 0)
+            q4 = fqt.QGrad(desc, cfg4, device=dev)
+            qws4 = fqt.workspace(desc, cfg4, fqt.FQT_WS_QUANTIZE, device=dev)
+            qz4 = lambda: fqt.fqt_agp_scq_quantize(desc, cfg4, dY, q4, qws4, st)
+            qz4()
+            tq4 = timed(qz4, k)
             ops = 2.0 * M * M * K
             # quantize: dY read twice (statistics, codes) + 1-byte codes and b-bit planes of
             # both encodings written
@@ -235,52 +361,17 @@ def suite(name, reps=10):
                               "mfma_frac": round(ops / tg / 1e9 / MFMA_I8_PEAK_TOPS, 4),
                               "quantize_ms": round(tq, 4),
                               "quantize_GBps": round(qbytes / tq / 1e6, 1),
+                              "quantize_b4_agp_ms": round(tq4, 4),
+                              "quantize_b4_agp_GBps_of_dY_twice": round(K * M * 8 / tq4 / 1e6, 1),
                               "pack_x_ms": round(tp, 4)}), flush=True)
-            del dY, X, q, qws, dws, xs, dW
+            del dY, X, q, qws, dws, xs, dW, q4, qws4
             torch.cuda.empty_cache()
         return
 
-    wl = WORKLOADS[name]
-    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
-    tot_ms, tot_ops = 0.0, 0.0
-    for li, L in enumerate(wl.layers):
-        X = _gen(torch, L.x_shape, tdt, dev)
-        W = _gen(torch, L.w_shape, torch.float32, dev)
-        nd = len(L.dy_shape)
-        r = wl.recipe
-        if r.kind == "sample_lognormal":
-            sc = torch.exp(r.sigma * torch.randn((L.N,) + (1,) * (nd - 1), device=dev))
-            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
-        elif r.kind == "channel_lognormal":
-            sc = torch.exp(r.sigma * torch.randn((1, L.D) + (1,) * (nd - 2), device=dev))
-            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
-        else:
-            dY = torch.distributions.StudentT(r.df).sample(L.dy_shape).to(dev).to(tdt)
-        dX, dW = torch.empty_like(X), torch.empty_like(W)
-        if tdt == torch.bfloat16:
-            desc = fqt.layer_desc(L, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
-        else:
-            desc = fqt.layer_desc(L)
-        cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, wl.philox_seed, 0, li)
-        ws = fqt.workspace(desc, cfg, device=dev)
-        step = lambda: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st)
-        for _ in range(3):
-            step()
-        ms = timed(step, reps)
-        ops = 4.0 * L.binary_macs()
-        es = 2 if tdt == torch.bfloat16 else 4
-        # each tensor crossing HBM once: dY, X, W read; dX, dW written
-        mbytes = (L.N * L.D * L.Ho * L.Wo + 2 * L.N * L.C * L.H * L.W) * es + 2 * L.D * L.C * L.kh * L.kw * 4
-        tot_ms += ms
-        tot_ops += ops
-        print(json.dumps({"suite": name, "layer": li, "name": L.name, "ms": round(ms, 4),
-                          "binary_TOPS": round(ops / ms / 1e9, 1),
-                          "min_bytes_MB": round(mbytes / 1e6, 2),
-                          "GBps_of_min_bytes": round(mbytes / ms / 1e6, 1)}), flush=True)
-        del X, W, dY, dX, dW, ws
-        torch.cuda.empty_cache()
-    print(json.dumps({"suite": name, "total_ms": round(tot_ms, 3),
-                      "binary_TOPS": round(tot_ops / tot_ms / 1e9, 1)}), flush=True)
+    out, _ = network_layers(name, dev, st, reps=reps, graph=True,
+                            per_layer=lambda row: print(json.dumps(row), flush=True))
+    print(json.dumps({"suite": name, "total_ms": out["ms_eager"],
+                      "binary_TOPS": out["binary_TOPS_eager"], **out}), flush=True)
 
 
 def main():
@@ -304,6 +395,7 @@ def main():
     wl = WORKLOADS[WORKLOAD]
     layer = wl.layers[0]
     dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
     if args.calib_copy_mib:
         src = torch.ones(args.calib_copy_mib << 18, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -317,69 +409,65 @@ def main():
     desc = fqt.layer_desc(layer)
     cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, wl.philox_seed, 0, 0)
     ws = fqt.workspace(desc, cfg, device=dev)
-    stream = torch.cuda.current_stream()
     macs = layer.binary_macs()
     ops_per_step = 2 * 2 * macs            # two products, 2 ops per binary MAC
 
     def step():
         fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream)
 
-    def timed(fn, k):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(k):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / k
-
     for _ in range(args.warmup):
         step()
-    ms_eager = timed(step, args.steps)
-
-    def graph_of(fn, reps):
-        """A HIP graph of `reps` back-to-back calls of fn(stream), captured on a side stream."""
-        g = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            fn(side)
-            torch.cuda.synchronize()
-            with torch.cuda.graph(g, stream=side):
-                for _ in range(reps):
-                    fn(side)
-        torch.cuda.synchronize()
-        return g
-
+    ms_eager = _timed(torch, stream, step, args.steps)
     ms_graph = None
     if not args.no_graph:
-        g = graph_of(lambda st: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st), 1)
+        g = _graph_of(torch, stream,
+                      lambda st: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st), 1)
         for _ in range(args.warmup):
             g.replay()
-        ms_graph = timed(g.replay, args.steps)
-    # The step is reported in the faster of the two launch modes (same work either way).
-    ms = ms_eager if ms_graph is None else min(ms_eager, ms_graph)
+        ms_graph = _timed(torch, stream, g.replay, args.steps)
 
-    # Single-kernel entry points, each timed as a graph of REPS back-to-back launches replayed
-    # on `stream` between two HIP events (eager launches of a few-microsecond kernel would
-    # time the host instead).
+    # Cold cache: before each timed step, overwrite 1 GiB (four times the last-level cache),
+    # then time the step alone between two events.
+    scrub = torch.empty(SCRUB_BYTES // 4, dtype=torch.float32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cold_reps, cold_ms = max(5, min(50, args.steps // 4)), 0.0
+    for r in range(cold_reps):
+        scrub.fill_(float(r))
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        cold_ms += e0.elapsed_time(e1)
+    ms_cold = cold_ms / cold_reps
+    del scrub
+
+    warm = ms_eager if ms_graph is None else min(ms_eager, ms_graph)
+    ms = ms_cold if args.cold else warm
+
+    # The step's kernels through the entry points that launch them: the quantizer (statistics,
+    # selection, codes), the two sign packers, and both products in one launch, the step's
+    # longest kernel.  Each timed as a graph of REPS back-to-back launches replayed on
+    # `stream` between two HIP events.
     q = fqt.QGrad(desc, cfg, device=dev)
     qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
     dws = fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW, device=dev)
     K = layer.C * layer.kh * layer.kw
     P = layer.Ho * layer.Wo
     R = layer.N * P
+    HW = layer.H * layer.W
     Wd, Wr = (layer.D + 63) // 64, (R + 63) // 64
     xs = torch.empty(Wr * K, dtype=torch.int64, device=dev)
     wsb = torch.empty(K, 64 * Wd, dtype=torch.int8, device=dev)
     wls = torch.empty(K, dtype=torch.int32, device=dev)
+    fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, stream)
+    fqt.fqt_pack_input_signs(desc, X, xs, stream)
+    fqt.fqt_pack_weight_signs(desc, W, wsb, wls, stream)
     entries = {
         "quantize": lambda st: fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st),
         "pack_x": lambda st: fqt.fqt_pack_input_signs(desc, X, xs, st),
         "pack_w": lambda st: fqt.fqt_pack_weight_signs(desc, W, wsb, wls, st),
-        "gemm_dw": lambda st: fqt.fqt_binary_gemm_dw(desc, cfg, q, xs, dW, dws, None, st),
-        "gemm_dx": lambda st: fqt.fqt_binary_gemm_dx(desc, cfg, q, wsb, wls, dX, None, st),
+        "products": lambda st: fqt.fqt_binary_products(desc, cfg, q, xs, wsb, wls, dX, dW, dws,
+                                                       st),
     }
     REPS = 20
     per = {}
@@ -387,41 +475,75 @@ def main():
         if args.no_graph:
             for _ in range(args.warmup):
                 fn(stream)
-            per[name] = timed(lambda: fn(stream), args.steps)
+            per[name] = _timed(torch, stream, lambda: fn(stream), args.steps)
             continue
-        gk = graph_of(fn, REPS)
+        gk = _graph_of(torch, stream, fn, REPS)
         for _ in range(max(1, args.warmup // REPS)):
             gk.replay()
-        per[name] = timed(gk.replay, max(1, args.steps // REPS)) / REPS
+        per[name] = _timed(torch, stream, gk.replay, max(1, args.steps // REPS)) / REPS
+    torch.cuda.synchronize()
     ks, kc = int(q.psq_count.item()), int(q.pcq_count.item())
     b = wl.bits
-    # Algorithmic bytes (each tensor crosses HBM once; codes at b bits, signs at 1 bit) and
-    # int8 MFMA ops (2 * M * N * K over the kept rows) of each single-kernel entry.
-    work = {
-        "pack_x": (X.numel() * 4 + K * Wr * 8, 0),
-        "pack_w": (W.numel() * 4 + K * Wd * 8, 0),
-        "gemm_dw": (kc * R * b // 8 + K * Wr * 8 + dW.numel() * 4, 2 * kc * K * R),
-        "gemm_dx": (ks * P * layer.D * b // 8 + K * Wd * 8 + dX.numel() * 4,
-                    2 * ks * layer.H * layer.W * layer.C * K * layer.D // layer.C),
-    }
-    # The roofline is taken on the longest entry point that launches a single kernel (the
-    # dW entry launches two: split partials and their sum; the quantizer three).
-    dom = max(("gemm_dx", "pack_x", "pack_w"), key=lambda k: per[k])
-    nbytes, nops = work[dom]
-    t_s = per[dom] * 1e-3
-    if nbytes / (HBM_PEAK_GBS * 1e9) >= nops / (MFMA_I8_PEAK_TOPS * 1e12):
-        roofline = {"bound": "hbm", "achieved": nbytes / t_s / 1e9, "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": nbytes / t_s / 1e9 / HBM_PEAK_GBS}
+    # Algorithmic bytes of the products launch: every operand crossing memory once at the
+    # width the method needs (codes at b bits, signs at 1 bit) and the outputs.  Ops: the
+    # int8 MFMA work over the kept rows (dX contracts D per kernel tap).
+    code_bytes = (ks * P * layer.D + kc * R) * b / 8
+    sign_bytes = (K * R + K * layer.D) / 8
+    out_bytes = X.numel() * 4 + W.numel() * 4
+    prod_bytes = code_bytes + sign_bytes + out_bytes
+    prod_ops = 2 * ks * HW * K * layer.D + 2 * kc * K * R
+    t_s = per["products"] * 1e-3
+    if prod_bytes / (HBM_PEAK_GBS * 1e9) >= prod_ops / (MFMA_I8_PEAK_TOPS * 1e12):
+        roofline = {"bound": "hbm", "achieved": prod_bytes / t_s / 1e9, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": prod_bytes / t_s / 1e9 / HBM_PEAK_GBS}
     else:
-        roofline = {"bound": "mfma", "achieved": nops / t_s / 1e12, "peak": MFMA_I8_PEAK_TOPS,
-                    "unit": "TOPS", "frac": nops / t_s / 1e12 / MFMA_I8_PEAK_TOPS}
-    roofline.update({"traffic": measured_traffic(dom), "kernel": dom, "kernel_ms": per[dom],
-                     "algorithmic_bytes": nbytes, "int8_ops": nops,
+        roofline = {"bound": "mfma", "achieved": prod_ops / t_s / 1e12,
+                    "peak": MFMA_I8_PEAK_TOPS, "unit": "TOPS",
+                    "frac": prod_ops / t_s / 1e12 / MFMA_I8_PEAK_TOPS}
+    roofline.update({"traffic": measured_traffic("products"), "kernel": "k_products",
+                     "entry": "fqt_binary_products", "kernel_ms": per["products"],
+                     "algorithmic_bytes": prod_bytes,
+                     "algorithmic_bytes_parts": {"codes_b_bits": code_bytes,
+                                                 "signs_1_bit": sign_bytes,
+                                                 "dX_dW": out_bytes},
+                     "int8_ops": prod_ops, "int8_frac": prod_ops / t_s / 1e12 / MFMA_I8_PEAK_TOPS,
                      "kept_samples": ks, "kept_channels": kc})
+    # The whole step against HBM: dY, X, W read and dX, dW written once each.
+    step_bytes = (dY.numel() + X.numel() + W.numel() + X.numel() + W.numel()) * 4
+    step_roofline = {"bound": "hbm", "algorithmic_bytes": step_bytes,
+                     "achieved": step_bytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "ms_at_peak": step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3}
+
+    # The single linear layer (32 x 256 -> 128, b = 2): launch-bound, eager and as a graph.
+    wl1 = WORKLOADS["linear_32x256x128"]
+    l1 = wl1.layers[0]
+    x1, w1, dy1 = (torch.from_numpy(a).to(dev) for a in draw_layer(l1, wl1.recipe, wl1.seed))
+    dx1, dw1 = torch.empty_like(x1), torch.empty_like(w1)
+    d1 = fqt.layer_desc(l1)
+    c1 = fqt.quant_cfg(wl1.bits, wl1.agp_mode, wl1.philox_seed, 0, 0)
+    ws1 = fqt.workspace(d1, c1, device=dev)
+    f1 = lambda st: fqt.fqt_layer_backward(d1, c1, x1, w1, dy1, dx1, dw1, ws1, st)
+    for _ in range(args.warmup):
+        f1(stream)
+    cfg1 = {"workload": "linear_32x256x128", "ms_eager": _timed(torch, stream, lambda: f1(stream),
+                                                                 args.steps)}
+    if not args.no_graph:
+        g1 = _graph_of(torch, stream, f1, 1)
+        for _ in range(args.warmup):
+            g1.replay()
+        cfg1["ms_graph"] = _timed(torch, stream, g1.replay, args.steps)
+
+    networks = None
+    if not args.no_networks:
+        networks = {n: network_layers(n, dev, stream, graph=not args.no_graph)[0]
+                    for n in ("resnet18_32px", "vgg16_224_bf16")}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(x, w, dy, layer, wl, ops_per_step, args.cpu_seconds)
+        one, allc = cpu_legs(x, w, dy, layer, wl, ops_per_step, args.cpu_seconds)
+        cpu = dict(one)
+        cpu["all_cores"] = allc
 
     out = {
         "metric": "binary backward TOPS + layer-backward ms (VGG16/ResNet18 shapes), % roofline",
@@ -439,10 +561,14 @@ def main():
         "config": {"workload": WORKLOAD, "layer": "conv3x3 256->256, 8x8, stride 1, pad 1",
                    "batch": layer.N, "bits": wl.bits, "agp": "bernoulli", "inputs": "f32",
                    "accumulate": "i32",
-                   "timed_as": "hip_graph" if ms_graph is not None and ms_graph <= ms_eager else "eager",
+                   "timed_as": "cold" if args.cold else (
+                       "hip_graph" if ms_graph is not None and ms_graph <= ms_eager else "eager"),
                    "ms_per_step_eager": ms_eager, "ms_per_step_graph": ms_graph,
-                   "per_kernel_ms": per, "binary_ops_per_step": ops_per_step},
+                   "ms_per_step_cold": ms_cold, "per_entry_ms": per,
+                   "binary_ops_per_step": ops_per_step,
+                   "linear_32x256x128": cfg1, "networks": networks},
         "roofline": roofline,
+        "step_roofline": step_roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))

@@ -249,6 +249,18 @@ int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
                        const fqt_qgrad *q, const int8_t *wsign, const int32_t *wsign_linesum,
                        void *dX, int32_t *I_out, void *hip_stream);
 
+/* Both products of the layer backward from one quantized gradient (Section 5.3, SCQ;
+ * Appendix C Alg. 1 binary products, dequantization and Folder): the dW of
+ * fqt_binary_gemm_dw and the dX of fqt_binary_gemm_dx, computed in one launch whose dW and
+ * dX workgroups run side by side (the form fqt_layer_backward uses).  Arguments as in those
+ * two calls: q from fqt_agp_scq_quantize, xsign from fqt_pack_input_signs, wsign and
+ * wsign_linesum from fqt_pack_weight_signs; ws >= fqt_workspace_size(FQT_WS_GEMM_DW), 256-byte
+ * aligned, no initialisation.  Layers whose dW contraction needs split partials over many
+ * rows add a second launch that sums them. */
+int fqt_binary_products(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
+                        const uint64_t *xsign, const int8_t *wsign, const int32_t *wsign_linesum,
+                        void *dX, float *dW, void *ws, size_t ws_bytes, void *hip_stream);
+
 /* Whole layer backward (Appendix C Alg. 1 backward; Section 5.3's final form):
  * quantize dY, pack sign(X) (im2col for conv), expand sign(W) to bytes, then both
  * products.

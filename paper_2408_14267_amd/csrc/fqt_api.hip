@@ -388,6 +388,24 @@ int fqt_binary_gemm_dx(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
                         static_cast<hipStream_t>(hip_stream));
 }
 
+int fqt_binary_products(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const fqt_qgrad *q,
+                        const uint64_t *xsign, const int8_t *wsign, const int32_t *wsign_linesum,
+                        void *dX, float *dW, void *ws, size_t ws_bytes, void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_qgrad(q, true, true));
+  FQT_TRY(check_dw_range(L, *cfg));
+  if (!xsign || !wsign || !wsign_linesum || !dX || !dW || !ws) return FQT_E_NULL;
+  if (!aligned(xsign, 8) || !aligned(wsign, 16) || !aligned(wsign_linesum, 4) ||
+      !aligned(dX, dtype_size(L.dx_t)) || !aligned(dW, 4) || !aligned(ws, 256))
+    return FQT_E_ALIGN;
+  if (L.kh * L.kw > 64) return FQT_E_SHAPE;
+  if (ws_bytes < gemm_dw_ws_bytes(L, *cfg)) return FQT_E_WORKSPACE;
+  return launch_products(L, *cfg, *q, xsign, wsign, wsign_linesum, dX, dW, ws, nullptr, nullptr,
+                         static_cast<hipStream_t>(hip_stream));
+}
+
 int fqt_layer_backward(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, const void *X,
                        const void *W, const void *dY, void *dX, float *dW, void *ws,
                        size_t ws_bytes, void *hip_stream) {
@@ -427,7 +445,9 @@ int layer_backward_run(const Layer &L, const fqt_quant_cfg &cfg_, const void *X,
   // Statistics, then the selection (whose launch also packs the sign operands when the
   // layer allows), the quantizer, both products.
   SignJob sj{X, W, w.xsign, w.wsb, w.wlsum, false};
-  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s, &sj));
+  // The products read the byte codes; the bit planes (the paper's packed form) are left to
+  // fqt_agp_scq_quantize callers.
+  FQT_TRY(launch_quantize(L, *cfg, dY, w.q, w.qws, s, &sj, false));
   if (!sj.done) {
     if (L.kind == FQT_LINEAR)
       FQT_TRY(launch_pack_bits(X, L.x_t, L.N, L.C, L.C, FQT_PACK_ALONG_ROWS, nullptr, w.xsign,

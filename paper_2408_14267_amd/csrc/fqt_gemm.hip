@@ -108,37 +108,41 @@ struct DwArgs {
   int32_t *part;                 // [S][D][Kp] partial sums of each split (slots < count)
   int32_t *partT;                // [S][Kp] set bits of each split of each sign line
   uint32_t D, K, Kp, R, Rp, Wr, ktiles, kgroups, codes_bytes, xsign_bytes, S, wps;
+  uint32_t wpw;                  // in-block reduction form: words of the contraction per wave
   FastDiv divS, divKg, divQ;    // divQ: Kp / 4
+  FastDiv divKt;                 // ktiles
 };
 
 constexpr int DW_WAVES = 4;                 // column tiles per block, one per wave
 constexpr int DW_THREADS = DW_WAVES * 64;
 constexpr int DW_PREF = 4;                  // 64-bit words of the contraction per batch
 
-// One batch of a wave's operands: DW_PREF words of its sign column and the two 32-byte
+// One batch of a wave's operands: PREF words of its sign column and the two 32-byte
 // code chunks of each word.
+template <int PREF>
 struct DwBatch {
-  uint64_t word[DW_PREF];
-  v4i A[DW_PREF][2];
+  uint64_t word[PREF];
+  v4i A[PREF][2];
 };
+template <int PREF>
 __device__ __forceinline__ void dw_issue(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
                                          __amdgpu_buffer_rsrc_t xrs, uint32_t aoff,
                                          uint32_t boff, uint32_t c0, uint32_t w_end,
-                                         DwBatch &b) {
+                                         DwBatch<PREF> &b) {
   const uint32_t chunk_bytes = a.D * 32;      // one 32-position chunk of every PCQ row
 #pragma unroll
-  for (int u = 0; u < DW_PREF; ++u) {
+  for (int u = 0; u < PREF; ++u) {
     const uint32_t c = c0 + u < w_end ? c0 + u : c0;   // past the end: word c0 again
     b.word[u] = load8(xrs, boff, c * a.K * 8);
 #pragma unroll
     for (int h = 0; h < 2; ++h) b.A[u][h] = load16(crs, aoff, (2 * c + h) * chunk_bytes);
   }
 }
-template <bool B8>
-__device__ __forceinline__ void dw_consume(const DwBatch &b, uint32_t c0, uint32_t w_end,
+template <bool B8, int PREF>
+__device__ __forceinline__ void dw_consume(const DwBatch<PREF> &b, uint32_t c0, uint32_t w_end,
                                            int g, v16i &acc, uint32_t &tpart) {
 #pragma unroll
-  for (int u = 0; u < DW_PREF; ++u) {
+  for (int u = 0; u < PREF; ++u) {
     if (c0 + u >= w_end) break;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -153,28 +157,31 @@ __device__ __forceinline__ void dw_consume(const DwBatch &b, uint32_t c0, uint32
 // double-buffered: the loads of batch i + 1 issue before the products of batch i (a
 // sched_barrier keeps the compiler from sinking them), so a long contraction costs one
 // exposed memory latency.
-template <bool B8>
+template <bool B8, int PREF = DW_PREF>
 __device__ __forceinline__ void dw_accumulate(const DwArgs &a, __amdgpu_buffer_rsrc_t crs,
                                               __amdgpu_buffer_rsrc_t xrs, uint32_t aoff,
                                               uint32_t boff, uint32_t c_first, uint32_t w_end,
                                               int g, v16i &acc, uint32_t &tpart) {
   if (c_first >= w_end) return;
-  DwBatch b0, b1;
+  DwBatch<PREF> b0, b1;
   uint32_t c0 = c_first;
-  dw_issue(a, crs, xrs, aoff, boff, c0, w_end, b0);
+  dw_issue<PREF>(a, crs, xrs, aoff, boff, c0, w_end, b0);
   for (;;) {
-    if (c0 + DW_PREF < w_end) dw_issue(a, crs, xrs, aoff, boff, c0 + DW_PREF, w_end, b1);
+    if (c0 + PREF < w_end) dw_issue<PREF>(a, crs, xrs, aoff, boff, c0 + PREF, w_end, b1);
     __builtin_amdgcn_sched_barrier(0);
-    dw_consume<B8>(b0, c0, w_end, g, acc, tpart);
-    c0 += DW_PREF;
+    dw_consume<B8, PREF>(b0, c0, w_end, g, acc, tpart);
+    c0 += PREF;
     if (c0 >= w_end) break;
-    if (c0 + DW_PREF < w_end) dw_issue(a, crs, xrs, aoff, boff, c0 + DW_PREF, w_end, b0);
+    if (c0 + PREF < w_end) dw_issue<PREF>(a, crs, xrs, aoff, boff, c0 + PREF, w_end, b0);
     __builtin_amdgcn_sched_barrier(0);
-    dw_consume<B8>(b1, c0, w_end, g, acc, tpart);
-    c0 += DW_PREF;
+    dw_consume<B8, PREF>(b1, c0, w_end, g, acc, tpart);
+    c0 += PREF;
     if (c0 >= w_end) break;
   }
 }
+// Words per batch of the in-block reduction form (8 was measured slower at the 256 -> 256
+// conv on 8x8 maps: the products launch it shares with the dX blocks lost occupancy).
+constexpr int DW_KRED_PREF = 4;
 
 // dW rows of the slot tile [j0, j0 + 32) of one wave's 32 columns written directly (one
 // split, S = 1): I, T, the rescale S_d I + Z'_d (2T - N*Ho*Wo) (b = 8 adds back
@@ -255,6 +262,69 @@ __device__ __forceinline__ void dw_part_body(const DwArgs &a, uint32_t bid) {
   for (int v = 0; v < 16; ++v) {
     const int row = acc_row(v, g);
     if (int(j0) + row < count) out[size_t(row) * a.Kp] = acc[v];
+  }
+}
+
+// dW with the contraction split over the four waves of a block and reduced in LDS (no
+// partial sums leave the workgroup, no finish pass).  Grid: ceil(D/32) slot tiles x
+// ceil(K/32) column tiles over the slot capacity, column tiles fastest (a column tile keeps
+// its XCD across slot tiles when the number of column tiles is a multiple of eight, so its
+// sign words are fetched into one L2).  Wave w contracts the 32 x 32 tile over the words
+// [w wpw, (w + 1) wpw) of N*Ho*Wo; the four partial tiles and set-bit counts meet in LDS,
+// and wave w finishes accumulator registers 4w .. 4w + 3 (slot rows 8w + 4g + u): the sum
+// over the waves, the b = 8 bias term, the rescale and the dW stores.  Slot tiles past the
+// kept channels write their rows of zeros.
+struct DwRedLds {
+  int32_t red[DW_WAVES][16][64];
+  uint32_t tred[DW_WAVES][32];
+};
+template <bool B8>
+__device__ __forceinline__ void dw_kred_body(const DwArgs &a, uint32_t bid, DwRedLds &sm) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t wave = wave_id();
+  const int i = lane & 31, g = lane >> 5;
+  const int count = *a.count;
+  const uint32_t rt = fdiv(bid, a.divKt);
+  const uint32_t kt = bid - rt * a.ktiles;
+  const uint32_t j0 = rt * 32, kc = kt * 32 + uint32_t(i);
+  const bool live = int(j0) < count;            // uniform over the block
+  if (live) {
+    const __amdgpu_buffer_rsrc_t crs = buffer_of(a.codes, a.codes_bytes);
+    const __amdgpu_buffer_rsrc_t xrs = buffer_of(a.xsign, a.xsign_bytes);
+    const uint32_t j = j0 + uint32_t(i);
+    const uint32_t aoff = int(j) < count ? j * 32 + 16 * g : BUF_NONE;
+    const uint32_t boff = kc < a.K ? kc * 8 : BUF_NONE;
+    const uint32_t cb = wave * a.wpw;
+    const uint32_t ce = min(a.Wr, cb + a.wpw);
+    v16i acc = v16i{0};
+    uint32_t tpart = 0;
+    dw_accumulate<B8, DW_KRED_PREF>(a, crs, xrs, aoff, boff, cb, ce, g, acc, tpart);
+    const uint32_t T = tpart + lane_xor<32>(tpart);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sm.red[wave][v][lane] = acc[v];
+    if (g == 0) sm.tred[wave][i] = T;
+  }
+  __syncthreads();
+  int T = 0;
+  if (live) T = int(sm.tred[0][i] + sm.tred[1][i] + sm.tred[2][i] + sm.tred[3][i]);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int v = 4 * int(wave) + u;
+    const uint32_t j = j0 + uint32_t(acc_row(v, g));
+    if (j >= a.D) continue;
+    const size_t d = size_t(a.kept[j]);
+    int I = 0;
+    float out = 0.0f;
+    if (int(j) < count) {
+      I = sm.red[0][v][lane] + sm.red[1][v][lane] + sm.red[2][v][lane] + sm.red[3][v][lane];
+      if (B8) I += 128 * (2 * T - int(a.Rp));
+      const float2 sz = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[d], a.offset[d]);
+      out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
+    }
+    if (kc < a.K) {
+      a.dW[d * a.K + kc] = out;
+      if (a.I_out) a.I_out[d * a.K + kc] = I;
+    }
   }
 }
 
@@ -485,6 +555,12 @@ __global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(3, 3
 template <bool B8, bool DIRECT>
 __global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_part(DwArgs a) {
   dw_part_body<B8, DIRECT>(a, blockIdx.x);
+}
+
+template <bool B8>
+__global__ __launch_bounds__(DW_THREADS) void k_mfma_dw_kred(DwArgs a) {
+  __shared__ DwRedLds sm;
+  dw_kred_body<B8>(a, blockIdx.x, sm);
 }
 
 // dW from the split partials: one thread per 4 columns (slot, k .. k + 3) of the slot
@@ -947,16 +1023,27 @@ __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
   else dx_body<B8, NB>(a, blockIdx.x, sm);
 }
 
-// Both products in one launch (the layer backward): blocks [0, ndw) are dW split-R
-// partial blocks (no LDS), the rest dX blocks.
-template <bool B8, int NB, bool DIRECT, bool WIDE>
+// How the dW blocks of the products launch run: split-R partials summed by a finish pass
+// (PARTS), one split writing dW itself (DIRECT), or the contraction split over a block's
+// waves and reduced in LDS (KRED).
+enum DwForm { DWF_PARTS = 0, DWF_DIRECT = 1, DWF_KRED = 2 };
+
+// Both products in one launch (the layer backward): blocks [0, ndw) are dW blocks, the rest
+// dX blocks; the two share one LDS allocation.
+template <bool WIDE>
+union ProductsLds {
+  DxLdsOf<WIDE> dx;
+  DwRedLds dw;
+};
+template <bool B8, int NB, int DWF, bool WIDE>
 __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
-  __shared__ DxLdsOf<WIDE> sm;
+  __shared__ ProductsLds<WIDE> sm;
   if (blockIdx.x < ndw) {
-    dw_part_body<B8, DIRECT>(dwa, blockIdx.x);
+    if constexpr (DWF == DWF_KRED) dw_kred_body<B8>(dwa, blockIdx.x, sm.dw);
+    else dw_part_body<B8, DWF == DWF_DIRECT>(dwa, blockIdx.x);
   } else {
-    if constexpr (WIDE) dx_body_wide<B8, NB>(dxa, blockIdx.x - ndw, sm);
-    else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm);
+    if constexpr (WIDE) dx_body_wide<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
+    else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
   }
 }
 
@@ -1140,12 +1227,17 @@ int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   return int(std::max<int64_t>(S, 1));
 }
 
+// Contractions of at most this many words that would need split-R partials run in the
+// in-block reduction form instead (four waves of at most 64 words each).
+constexpr int64_t DW_KRED_MAX_WORDS = 256;
+bool dw_kred_form(const Layer &L, int64_t S) { return S > 1 && L.Wr <= DW_KRED_MAX_WORDS; }
+
 // dW workspace: partials [S][D][Kp] and set-bit counts [S][Kp] (Kp = K rounded up to 32);
-// none when one split writes dW directly.
+// none when one split or the in-block reduction writes dW directly.
 static size_t dw_kp(const Layer &L) { return size_t((L.K + 31) / 32) * 32; }
 size_t gemm_dw_ws_bytes(const Layer &L, const fqt_quant_cfg &cfg) {
   const size_t S = size_t(gemm_dw_splits(L, cfg));
-  if (S == 1) return 256;
+  if (S == 1 || dw_kred_form(L, int64_t(S))) return 256;
   return align256(S * size_t(L.D) * dw_kp(L) * 4) + align256(S * dw_kp(L) * 4);
 }
 
@@ -1169,8 +1261,14 @@ DwArgs make_dw_args(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   a.xsign_bytes = uint32_t(L.Wr * L.K * 8);
   a.kgroups = (ktiles + DW_WAVES - 1) / DW_WAVES;
   a.S = S; a.wps = uint32_t((L.Wr + S - 1) / S);
+  a.wpw = uint32_t((L.Wr + DW_WAVES - 1) / DW_WAVES);
   a.divS = make_fastdiv(S); a.divKg = make_fastdiv(a.kgroups); a.divQ = make_fastdiv(uint32_t(dw_kp(L) / 4));
+  a.divKt = make_fastdiv(ktiles);
   return a;
+}
+// Blocks of the in-block reduction form: every (slot tile, column tile) of the capacity.
+uint32_t dw_kred_blocks(const Layer &L, const DwArgs &a) {
+  return a.ktiles * uint32_t((L.D + 31) / 32);
 }
 // Split-R partial blocks over the slot capacity: S x ceil(ceil(K/32) / 4) x ceil(D/32).
 uint32_t dw_part_blocks(const Layer &L, const DwArgs &a) {
@@ -1210,7 +1308,8 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
   return a;
 }
 // Contraction steps of one dX wave, rounded to the instantiated batch depths (10 steps
-// per batch still leaves four resident blocks per CU).
+// per batch still leaves four resident blocks per CU; 18 steps in one batch was measured
+// slower at the 256 -> 256 conv on 8x8 maps).
 int dx_batch(const DxArgs &a) {
   const uint32_t per_wave = a.wide ? a.taps * a.nch : (a.taps * a.nch + DX_WAVES - 1) / DX_WAVES;
   return per_wave <= 4 ? 4 : per_wave <= 8 ? 8 : 10;
@@ -1262,6 +1361,9 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   auto go = [&]<bool B8>() {
     if (dw_big(L, a)) {
       launch_dw_big<B8>(a, s);
+    } else if (dw_kred_form(L, a.S) && !dw_split_big(L, a)) {
+      hipLaunchKernelGGL(k_mfma_dw_kred<B8>, dim3(dw_kred_blocks(L, a)), dim3(DW_THREADS), 0, s,
+                         a);
     } else if (dw_split_big(L, a)) {
       launch_dw_split<B8>(a, s);
       launch_dw_finish<B8>(L, a, s);
@@ -1313,6 +1415,7 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
   // Long split-R contractions likewise run their partials as their own launch.
   const bool big = dw_big(L, dwa);
   const bool split_big = !big && dw_split_big(L, dwa);
+  const bool kred = !big && !split_big && dw_kred_form(L, dwa.S);
   if (big) {
     if (cfg.bits == 8) launch_dw_big<true>(dwa, s);
     else launch_dw_big<false>(dwa, s);
@@ -1320,32 +1423,36 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
     if (cfg.bits == 8) launch_dw_split<true>(dwa, s);
     else launch_dw_split<false>(dwa, s);
   }
-  const uint32_t ndw = (big || split_big) ? 0u : dw_part_blocks(L, dwa);
+  const uint32_t ndw = (big || split_big) ? 0u
+                      : kred ? dw_kred_blocks(L, dwa) : dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const int nb = dx_batch(dxa);
-  auto go = [&]<bool B8, bool DIRECT, bool WIDE>() {
+  auto go = [&]<bool B8, int DWF, bool WIDE>() {
     if (nb == 4)
-      hipLaunchKernelGGL((k_products<B8, 4, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+      hipLaunchKernelGGL((k_products<B8, 4, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
                          dwa, ndw);
     else if (nb == 8)
-      hipLaunchKernelGGL((k_products<B8, 8, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+      hipLaunchKernelGGL((k_products<B8, 8, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
                          dwa, ndw);
     else
-      hipLaunchKernelGGL((k_products<B8, 10, DIRECT, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
+      hipLaunchKernelGGL((k_products<B8, 10, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
                          dwa, ndw);
-    if (!DIRECT) launch_dw_finish<B8>(L, dwa, s);
+    if (DWF == DWF_PARTS) launch_dw_finish<B8>(L, dwa, s);
   };
-  auto go2 = [&]<bool B8, bool DIRECT>() {
-    if (dxa.wide) go.template operator()<B8, DIRECT, true>();
-    else go.template operator()<B8, DIRECT, false>();
+  auto go2 = [&]<bool B8, int DWF>() {
+    if (dxa.wide) go.template operator()<B8, DWF, true>();
+    else go.template operator()<B8, DWF, false>();
   };
-  if (cfg.bits == 8) {
-    if (dwa.S == 1) go2.template operator()<true, true>();
-    else go2.template operator()<true, false>();
-  } else {
-    if (dwa.S == 1) go2.template operator()<false, true>();
-    else go2.template operator()<false, false>();
-  }
+  auto go3 = [&]<bool B8>() {
+    // With the dW product in its own launch the products launch has no dW blocks: the big
+    // form (one split) needs no finish, the split_big partials do.
+    if (split_big) go2.template operator()<B8, DWF_PARTS>();
+    else if (big || dwa.S == 1) go2.template operator()<B8, DWF_DIRECT>();
+    else if (kred) go2.template operator()<B8, DWF_KRED>();
+    else go2.template operator()<B8, DWF_PARTS>();
+  };
+  if (cfg.bits == 8) go3.template operator()<true>();
+  else go3.template operator()<false>();
   return last_launch_status();
 }
 

@@ -104,8 +104,10 @@ struct SignJob {
 };
 // Zero-fills the FQT_WS_STATE_BYTES of state at the start of a quantize / layer workspace.
 int launch_state_clear(void *state, hipStream_t s);
+// planes = false: the codes one byte each only (what the products read), no bit planes.
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
-                    const QuantWs &w, hipStream_t s, SignJob *signs = nullptr);
+                    const QuantWs &w, hipStream_t s, SignJob *signs = nullptr,
+                    bool planes = true);
 int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                      const Layer *conv, uint64_t *dst, int32_t *linesum, hipStream_t s,
                      bool word_major = false);

@@ -1156,6 +1156,7 @@ struct QPackArgs {
   uint32_t step, layer;
   uint32_t eager;       // read every quad of the layer before the parameters
   uint32_t chan_fast;   // grid x walks the channel tiles (rows of dY read as long runs)
+  uint32_t planes;      // 1: also write the bit planes (0: the byte codes only)
 };
 
 // Codes of a thread's quads into the LDS tiles.  The four codes of a quad share one
@@ -1299,16 +1300,17 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
     const int rank = cpar[dd].rank;             // -1 for pruned channels and past D
     const uint32_t *src = reinterpret_cast<const uint32_t *>(&cc[dd][8 * lk]);
     const uint32_t lo = src[0], hi = src[1];
-    const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
-#pragma unroll
-    for (int p = 0; p < 8; ++p)
-      if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
-    __builtin_amdgcn_wave_barrier();            // LDS operations of a wave run in order
-    const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
-    if (rank >= 0) {
+    if (rank >= 0)
       *reinterpret_cast<uint2 *>(a.pcq_codes + ((size_t(r0 >> 5) + (lk >> 2)) * g.D + rank) * 32 +
                                  8 * (lk & 3)) = make_uint2(lo, hi);
-      if (lk < a.bits) a.pcq[(size_t(lk) * g.D + rank) * a.Wr + (r0 >> 6)] = pw;
+    if (a.planes) {
+      const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
+      __builtin_amdgcn_wave_barrier();          // LDS operations of a wave run in order
+      const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
+      if (rank >= 0 && lk < a.bits) a.pcq[(size_t(lk) * g.D + rank) * a.Wr + (r0 >> 6)] = pw;
     }
   }
   __builtin_amdgcn_wave_barrier();
@@ -1318,16 +1320,17 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
     const int row = prow[rr];                   // -1 for pruned samples and past R
     const uint32_t *src = reinterpret_cast<const uint32_t *>(&cs[rr][8 * lk]);
     const uint32_t lo = src[0], hi = src[1];
-    const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
-#pragma unroll
-    for (int p = 0; p < 8; ++p)
-      if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
-    __builtin_amdgcn_wave_barrier();
-    const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
-    if (row >= 0) {
+    if (row >= 0)
       *reinterpret_cast<uint2 *>(a.psq_codes + ((size_t(d0 >> 5) + (lk >> 2)) * g.R + row) * 32 +
                                  8 * (lk & 3)) = make_uint2(lo, hi);
-      if (lk < a.bits) a.psq[(size_t(lk) * g.R + row) * a.Wd + (d0 >> 6)] = pw;
+    if (a.planes) {
+      const uint64_t y = bit_transpose8((uint64_t(hi) << 32) | lo);
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        if (p < a.bits) pbuf[wave][li][p][lk] = uint8_t(y >> (8 * p));
+      __builtin_amdgcn_wave_barrier();
+      const uint64_t pw = *reinterpret_cast<const uint64_t *>(&pbuf[wave][li][lk][0]);
+      if (row >= 0 && lk < a.bits) a.psq[(size_t(lk) * g.R + row) * a.Wd + (d0 >> 6)] = pw;
     }
   }
 }
@@ -1383,7 +1386,7 @@ int launch_state_clear(void *state, hipStream_t s) {
 }
 
 int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, const fqt_qgrad &q,
-                    const QuantWs &w, hipStream_t s, SignJob *signs) {
+                    const QuantWs &w, hipStream_t s, SignJob *signs, bool write_planes) {
   TileGeom g{uint32_t(L.D), uint32_t(L.P), uint32_t(L.R), make_fastdiv(uint32_t(L.P))};
   const uint32_t nrt = uint32_t(L.Wr), ndt = uint32_t(L.Wd);
   const uint32_t nrb = uint32_t(stats_row_blocks(L));
@@ -1540,6 +1543,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   // Kept fraction of the elements: 1 without AGP; with AGP about 1 - (1 - 1/b)^2 (G/b
   // groups of each encoding kept), above 3/4 for b <= 2.
   qa.eager = (cfg.agp_mode == FQT_AGP_OFF || cfg.bits <= 2) ? 1u : 0u;
+  qa.planes = write_planes ? 1u : 0u;
   dispatch_dtype(L.dy_t, [&]<int DT>() {
     if (mode == TILE_PIX)
       hipLaunchKernelGGL((k_qpack<TILE_PIX, DT>), qgrid, dim3(THREADS), 0, s, qa);

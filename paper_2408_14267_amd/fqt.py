@@ -30,7 +30,7 @@ EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_a
             "fqt_pack_bits", "fqt_pack_input_signs", "fqt_binary_gemm_dw", "fqt_pack_weight_signs",
             "fqt_binary_gemm_dx",
             "fqt_layer_backward", "fqt_binary_forward", "fqt_workspace_init",
-            "fqt_layer_backward_noalloc")
+            "fqt_layer_backward_noalloc", "fqt_binary_products")
 
 
 class FqtError(RuntimeError):
@@ -84,6 +84,8 @@ def _load():
                                        c_void_p]),
         "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
+        "fqt_binary_products": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p,
+                                        c_void_p, c_void_p, c_size_t, c_void_p]),
         "fqt_layer_backward_noalloc": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p,
                                                c_void_p, c_void_p]),
         "fqt_binary_forward": (c_int, [D, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
@@ -192,6 +194,13 @@ def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, wsign_linesum, dX, I_out=None, s
     _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign),
                                    _ptr(wsign_linesum), _ptr(dX), _ptr(I_out), _stream(stream)),
            "fqt_binary_gemm_dx")
+
+
+def fqt_binary_products(desc, cfg, qgrad, xsign, wsign, wsign_linesum, dX, dW, ws, stream=None):
+    _check(_lib.fqt_binary_products(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign),
+                                    _ptr(wsign), _ptr(wsign_linesum), _ptr(dX), _ptr(dW),
+                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "fqt_binary_products")
 
 
 def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):

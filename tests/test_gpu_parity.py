@@ -276,6 +276,14 @@ def _check_case(layer, bits, mode, recipe, dtype, **kw):
     assert np.array_equal(I_dx.cpu().numpy(), ref.I_dx), "dX integer product"
     _assert_rescaled(dW, ref.dW, ref.dW_t1, ref.dW_t2, 1e-5, "dW")
     _assert_rescaled(dX, ref.dX, ref.dX_t1, ref.dX_t2, 2.0 ** -8 if dtype == "bf16" else 1e-5, "dX")
+    # Both products in one launch (fqt_binary_products) give the same bits as the two calls.
+    dX3, dW3 = torch.full_like(dX, 7.0), torch.full_like(dW, 7.0)
+    fqt.fqt_binary_products(desc, cfg, q, xs, wsb, wlsum, dX3, dW3,
+                            fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW))
+    torch.cuda.synchronize()
+    assert torch.equal(dX3.view(torch.int16 if dtype == "bf16" else torch.int32),
+                       dX.view(torch.int16 if dtype == "bf16" else torch.int32)), "products dX"
+    assert torch.equal(dW3.view(torch.int32), dW.view(torch.int32)), "products dW"
     # The whole-layer entry point (the launch configuration of the network suites) gives the
     # same bits as the component calls.
     dX2 = torch.empty_like(dX)
