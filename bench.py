@@ -76,7 +76,7 @@ def parse():
                    help="report the cold-cache step time as ms_per_step (1 GiB overwritten "
                         "before every timed step) instead of the warm one")
     p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward",
-                                       "table5"),
+                                       "table5", "train"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
                         "layer backwards, the dW binary GEMM sweep, the binary forward of "
                         "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer, or "
@@ -249,6 +249,36 @@ def suite(name, reps=10):
         e1.record(st)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k
+
+    if name == "train":
+        # A Table 3 analogue: one training step (forward, cross-entropy, backward, Adam) of
+        # VGG-16 and ResNet-18 at 32 x 32 (batch 128) and 224 x 224 (batch 64), random data:
+        # the binary network under 1-bit FQT (b = 4, AGP Bernoulli) against the same network
+        # in float32 and in bf16 autocast on the same GPU.
+        from paper_2408_14267_amd import train
+        for net, res, nb in (("vgg16", 32, 128), ("resnet18", 32, 128), ("vgg16", 224, 64),
+                             ("resnet18", 224, 64)):
+            out = {"suite": name, "net": net, "res": res, "batch": nb}
+            for mode in ("binary_fqt", "fp32", "bf16_autocast"):
+                torch.manual_seed(0)
+                binary = mode == "binary_fqt"
+                classes = 10 if res == 32 else 1000
+                model = (train.VGG16(classes, res, binary=binary, bits=4) if net == "vgg16"
+                         else train.ResNet18(classes, binary=binary, bits=4)).to(dev)
+                opt = torch.optim.Adam(model.parameters(), lr=1e-3)
+                x = torch.randn(nb, 3, res, res, device=dev)
+                y = torch.randint(0, classes, (nb,), device=dev)
+                ac = torch.bfloat16 if mode == "bf16_autocast" else None
+                stepf = lambda: train.train_step(model, opt, x, y, ac)
+                for _ in range(3):
+                    stepf()
+                out[mode + "_ms"] = round(timed(stepf, reps), 4)
+                del model, opt
+                torch.cuda.empty_cache()
+            out["speedup_vs_fp32"] = round(out["fp32_ms"] / out["binary_fqt_ms"], 3)
+            out["speedup_vs_bf16"] = round(out["bf16_autocast_ms"] / out["binary_fqt_ms"], 3)
+            print(json.dumps(out), flush=True)
+        return
 
     if name == "table5":
         # The paper's Table 5 sizes (m, k, n): a gradient of m columns over a k-deep contraction
