@@ -76,7 +76,7 @@ def parse():
                    help="report the cold-cache step time as ms_per_step (1 GiB overwritten "
                         "before every timed step) instead of the warm one")
     p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward",
-                                       "table5", "train"),
+                                       "table5", "train", "variance", "baselines"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
                         "layer backwards, the dW binary GEMM sweep, the binary forward of "
                         "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer, or "
@@ -124,6 +124,42 @@ def _gen(torch, shape, dtype, dev, scale=None):
     return x.to(dtype)
 
 
+def _dequantized(torch, q, N, D, P):
+    """(PSQ estimate, PCQ estimate) of dY as float64 [N][D][P], from the codes, kept lists,
+    scales and offsets of a quantized gradient (the estimate g_hat = S q + Z' of the kept
+    groups, 0 elsewhere)."""
+    R = N * P
+    Wd, Wr = (D + 63) // 64, (R + 63) // 64
+    out = []
+    for side in ("psq", "pcq"):
+        count = int(getattr(q, side + "_count").item())
+        kept = getattr(q, side + "_kept")[:count].long()
+        S = getattr(q, side + "_scale").double()[kept]
+        Z = getattr(q, side + "_offset").double()[kept]
+        g = torch.zeros((N, D, P), dtype=torch.float64, device=q.psq_codes.device)
+        if side == "psq":
+            codes = q.psq_codes.view(2 * Wd, R, 32).permute(1, 0, 2).reshape(R, 64 * Wd)[:, :D]
+            rows = codes[:count * P].double().view(count, P, D).permute(0, 2, 1)
+            g[kept] = S[:, None, None] * rows + Z[:, None, None]
+        else:
+            codes = q.pcq_codes.view(2 * Wr, D, 32).permute(1, 0, 2).reshape(D, 64 * Wr)[:, :R]
+            rows = codes[:count].double().view(count, N, P).permute(1, 0, 2)
+            g[:, kept] = S[None, :, None] * rows + Z[None, :, None]
+        out.append(g)
+    return out
+
+
+def _draw_dy(torch, L, recipe, dtype, dev):
+    nd = len(L.dy_shape)
+    if recipe.kind == "sample_lognormal":
+        sc = torch.exp(recipe.sigma * torch.randn((L.N,) + (1,) * (nd - 1), device=dev))
+        return _gen(torch, L.dy_shape, dtype, dev, sc)
+    if recipe.kind == "channel_lognormal":
+        sc = torch.exp(recipe.sigma * torch.randn((1, L.D) + (1,) * (nd - 2), device=dev))
+        return _gen(torch, L.dy_shape, dtype, dev, sc)
+    return torch.distributions.StudentT(recipe.df).sample(L.dy_shape).to(dev).to(dtype)
+
+
 def _timed(torch, stream, fn, k):
     """Mean ms of k calls of fn between two HIP events recorded on `stream`."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -151,7 +187,8 @@ def _graph_of(torch, stream, fn, reps):
     return g
 
 
-def network_layers(name, dev, stream, reps=10, graph=True, per_layer=None):
+def network_layers(name, dev, stream, reps=10, graph=True, per_layer=None, bits=None,
+                   agp_mode=None):
     """Every layer backward of a network (inputs drawn on the GPU with the workload's recipe
     distributions, one workspace shared by all layers): per-layer eager ms, the eager total,
     and one HIP graph of the whole network's layer calls replayed (ms per pass)."""
@@ -166,22 +203,14 @@ def network_layers(name, dev, stream, reps=10, graph=True, per_layer=None):
     for li, L in enumerate(wl.layers):
         X = _gen(torch, L.x_shape, tdt, dev)
         W = _gen(torch, L.w_shape, torch.float32, dev)
-        nd = len(L.dy_shape)
-        r = wl.recipe
-        if r.kind == "sample_lognormal":
-            sc = torch.exp(r.sigma * torch.randn((L.N,) + (1,) * (nd - 1), device=dev))
-            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
-        elif r.kind == "channel_lognormal":
-            sc = torch.exp(r.sigma * torch.randn((1, L.D) + (1,) * (nd - 2), device=dev))
-            dY = _gen(torch, L.dy_shape, tdt, dev, sc)
-        else:
-            dY = torch.distributions.StudentT(r.df).sample(L.dy_shape).to(dev).to(tdt)
+        dY = _draw_dy(torch, L, wl.recipe, tdt, dev).contiguous()
         dX, dW = torch.empty_like(X), torch.empty_like(W)
         if tdt == torch.bfloat16:
             desc = fqt.layer_desc(L, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
         else:
             desc = fqt.layer_desc(L)
-        cfg = fqt.quant_cfg(wl.bits, wl.agp_mode, wl.philox_seed, 0, li)
+        cfg = fqt.quant_cfg(wl.bits if bits is None else bits,
+                            wl.agp_mode if agp_mode is None else agp_mode, wl.philox_seed, 0, li)
         ws_bytes = max(ws_bytes, fqt.fqt_workspace_size(desc, cfg))
         calls.append((L, desc, cfg, X, W, dY, dX, dW))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -278,6 +307,108 @@ def suite(name, reps=10):
             out["speedup_vs_fp32"] = round(out["fp32_ms"] / out["binary_fqt_ms"], 3)
             out["speedup_vs_bf16"] = round(out["bf16_autocast_ms"] / out["binary_fqt_ms"], 3)
             print(json.dumps(out), flush=True)
+        return
+
+    if name == "variance":
+        # Quantizer variance (Section 4.2; the paper's per-layer variance figure for
+        # ResNet-18): E sum (g_hat - dY)^2 of the estimate that feeds each product, estimated
+        # from the GPU quantizer over 32 Philox steps, for 1-bit per-group quantization
+        # without AGP (the PSQ baseline) and for AGP + b-bit codes, b = 2, 4, 8.  Relative to
+        # sum dY^2, and as a fraction of the 1-bit baseline.
+        from paper_2408_14267_amd.workloads import WORKLOADS as WL
+        steps = 32
+        points = [("vgg_cifar_conv3x3_256", 0, WL["vgg_cifar_conv3x3_256"].layers[0])] + \
+                 [("resnet18_32px", i, L) for i, L in enumerate(WL["resnet18_32px"].layers)]
+        for wname, li, L in points:
+            wl = WL[wname]
+            dY = _draw_dy(torch, L, wl.recipe, torch.float32, dev).contiguous()
+            N, D, P = L.N, L.D, L.Ho * L.Wo
+            x = dY.double().view(N, D, P)
+            norm = float((x * x).sum())
+            desc = fqt.layer_desc(L)
+            row = {"suite": name, "workload": wname, "layer": li, "name": L.name,
+                   "sum_dY2": norm, "steps": steps}
+            for tag, bits, mode in (("psq1_no_agp", 1, fqt.FQT_AGP_OFF),
+                                    ("agp_b2", 2, fqt.FQT_AGP_BERNOULLI),
+                                    ("agp_b4", 4, fqt.FQT_AGP_BERNOULLI),
+                                    ("agp_b8", 8, fqt.FQT_AGP_BERNOULLI)):
+                ts, tc = 0.0, 0.0
+                for step in range(steps):
+                    cfg = fqt.quant_cfg(bits, mode, 0, step, li)
+                    q = fqt.QGrad(desc, cfg, device=dev)
+                    fqt.fqt_agp_scq_quantize(desc, cfg, dY, q,
+                                             fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE,
+                                                           device=dev), st)
+                    gs, gc = _dequantized(torch, q, N, D, P)
+                    ts += float(((gs - x) ** 2).sum())
+                    tc += float(((gc - x) ** 2).sum())
+                row[tag] = {"psq_rel_var": ts / steps / norm, "pcq_rel_var": tc / steps / norm}
+            for tag in ("agp_b2", "agp_b4", "agp_b8"):
+                row[tag]["psq_vs_1bit"] = row[tag]["psq_rel_var"] / row["psq1_no_agp"]["psq_rel_var"]
+                row[tag]["pcq_vs_1bit"] = row[tag]["pcq_rel_var"] / row["psq1_no_agp"]["pcq_rel_var"]
+            print(json.dumps(row), flush=True)
+            del dY, x
+            torch.cuda.empty_cache()
+        return
+
+    if name == "baselines":
+        # Baseline quantizers on the same kernels (the paper's Table 1 / Table 3 rows), on the
+        # 256 -> 256 conv (8 x 8, batch 128) and the ResNet-18 network: ours (AGP, b = 4),
+        # 1-bit per-group codes without AGP, 8-bit SCQ without AGP; and 8-bit PSQ for both
+        # products, where dW cannot use the integer kernels (its per-sample scale varies along
+        # the contraction, Section 5.3): the dX product on the kernels, dW as a float32
+        # product of the dequantized PSQ gradient with sign(unfold(X)) (torch, a comparison
+        # system only).
+        from paper_2408_14267_amd.workloads import WORKLOADS as WL
+        variants = (("ours_agp_b4", 4, fqt.FQT_AGP_BERNOULLI), ("scq1_no_agp", 1, fqt.FQT_AGP_OFF),
+                    ("scq8_no_agp", 8, fqt.FQT_AGP_OFF))
+        wl = WL["vgg_cifar_conv3x3_256"]
+        L = wl.layers[0]
+        X = _gen(torch, L.x_shape, torch.float32, dev)
+        W = _gen(torch, L.w_shape, torch.float32, dev)
+        dY = _draw_dy(torch, L, wl.recipe, torch.float32, dev).contiguous()
+        dX, dW = torch.empty_like(X), torch.empty_like(W)
+        desc = fqt.layer_desc(L)
+        row = {"suite": name, "workload": wl.name}
+        for tag, bits, mode in variants:
+            cfg = fqt.quant_cfg(bits, mode, 0, 0, 0)
+            ws = fqt.workspace(desc, cfg, device=dev)
+            f = lambda: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st)
+            for _ in range(5):
+                f()
+            row[tag + "_ms"] = round(timed(f, 50), 5)
+        # 8-bit PSQ for both products.
+        cfg = fqt.quant_cfg(8, fqt.FQT_AGP_OFF, 0, 0, 0)
+        q = fqt.QGrad(desc, cfg, device=dev)
+        qws = fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev)
+        K, P = L.C * L.kh * L.kw, L.Ho * L.Wo
+        Wd = (L.D + 63) // 64
+        wsb = torch.empty(K, 64 * Wd, dtype=torch.int8, device=dev)
+        wls = torch.empty(K, dtype=torch.int32, device=dev)
+
+        def psq8_both():
+            fqt.fqt_agp_scq_quantize(desc, cfg, dY, q, qws, st)
+            fqt.fqt_pack_weight_signs(desc, W, wsb, wls, st)
+            fqt.fqt_binary_gemm_dx(desc, cfg, q, wsb, wls, dX, None, st)
+            gs = _dequantized(torch, q, L.N, L.D, P)[0].float()             # [N][D][P]
+            sx = torch.nn.functional.unfold(X, (L.kh, L.kw), padding=(L.ph, L.pw),
+                                            stride=(L.sh, L.sw))             # [N][K][P]
+            sx = torch.where(sx > 0, 1.0, -1.0)
+            dW.view(L.D, K).copy_(gs.permute(1, 0, 2).reshape(L.D, -1)
+                                  @ sx.permute(1, 0, 2).reshape(K, -1).t())
+        for _ in range(5):
+            psq8_both()
+        row["psq8_both_products_ms"] = round(timed(psq8_both, 50), 5)
+        print(json.dumps(row), flush=True)
+        del X, W, dY, dX, dW
+        torch.cuda.empty_cache()
+        # The ResNet-18 network, per variant (eager totals).
+        for tag, bits, mode in variants:
+            wl18 = WL["resnet18_32px"]
+            out, _ = network_layers("resnet18_32px", dev, st, reps=10, graph=False,
+                                    bits=bits, agp_mode=mode)
+            print(json.dumps({"suite": name, "workload": "resnet18_32px", "variant": tag,
+                              "ms_eager": out["ms_eager"]}), flush=True)
         return
 
     if name == "table5":

@@ -259,6 +259,69 @@ def sr_codes(x, Z, R, bits, u32):
     return q.astype(np.uint8)
 
 
+# --------------------------------------------------------------------------- variance
+
+def agp_probabilities(R, bits, mode):
+    """Keep probabilities p_i of AGP in float64 (Section 5.2; water_fill's reading for
+    p_i > 1): 1 for saturated groups, (G - b s) w_i / (b W_rem) for the others; every
+    group with R > 0 has p = 1 under AGP_OFF; TOPK keeps its k groups with p = 1."""
+    R = np.asarray(R, dtype=F32)
+    G, b = R.size, int(bits)
+    w = agp_weights(R)
+    p = np.zeros(G)
+    if mode == AGP_OFF:
+        p[:] = 1.0
+    elif mode == AGP_TOPK:
+        p[descending_order(w)[:max(1, G // b)]] = 1.0
+    else:
+        order, s, w_rem = water_fill(w, b)
+        p[order[:s]] = 1.0
+        if w_rem > 0:
+            for i in order[s:]:
+                p[i] = (G - b * s) * w[i] / (b * w_rem)
+    return p
+
+
+def quantizer_variance(dy, bits, mode=AGP_BERNOULLI, groups="samples"):
+    """Exact conditional variance, element by element, of the quantized gradient that feeds
+    one product: g_hat = (m/p) Q(x), with Q the b-bit min-max stochastic-rounding quantizer
+    of the element's group (Section 3.2) and m ~ Bern(p) the AGP mask (Section 5.2).
+
+    groups = "samples" (PSQ, the dX operand) or "channels" (PCQ, the dW operand).  With
+    Var_SR = (R/B)^2 f (1 - f), f the fractional part of v = clamp((x - Z) B/R, 0, B) taken
+    in float32 as the quantizer takes it (Proposition B.1's variance of SR, scaled by R/B),
+    E[g_hat] = x and Var[g_hat] = E[g_hat^2] - x^2 = (Var_SR + x^2)/p - x^2
+                                = Var_SR / p + x^2 (1 - p) / p.
+    Under AGP_OFF (p = 1) this is plain per-group quantization's Var_SR.  Groups with
+    p = 0 (R = 0, never kept; reading of the zero-range case) and the groups TOPK prunes
+    contribute 0.  Returns float64 in dy's [N][D][Ho][Wo] layout; the sum over all elements
+    is the quantizer variance of Section 4.2 / Appendix B.
+    """
+    dy4 = canonical_f32(as_nchw(dy))
+    st = group_stats(dy4)
+    if groups == "samples":
+        R, Z = st.R_s, st.Z_s
+        bshape = (-1, 1, 1, 1)
+    elif groups == "channels":
+        R, Z = st.R_c, st.Z_c
+        bshape = (1, -1, 1, 1)
+    else:
+        raise ValueError(groups)
+    B = F32((1 << int(bits)) - 1)
+    p = agp_probabilities(R, bits, mode).reshape(bshape)
+    Rb = R.reshape(bshape)
+    safe_R = np.where(Rb > 0, Rb, F32(1.0))
+    inv = (B / safe_R).astype(F32)
+    v = ((dy4 - Z.reshape(bshape)).astype(F32) * inv).astype(F32)
+    v = np.minimum(np.maximum(v, F32(0.0)), B).astype(np.float64)
+    f = v - np.floor(v)
+    var_sr = np.where(Rb > 0, (Rb.astype(np.float64) / float(B)) ** 2 * f * (1.0 - f), 0.0)
+    x = dy4.astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        out = np.where(p > 0, var_sr / p + x * x * (1.0 - p) / p, 0.0)
+    return out
+
+
 # --------------------------------------------------------------------------- step 5: planes
 
 def bit_planes(q, bits):

@@ -183,14 +183,11 @@ def test_layer_unbiased_over_seeds(layer, bits):
 
 
 def _agp_exact_variance(g, b, p):
-    """Var[(m/p) Q(x)] = Var_SR / p + x^2 (1-p)/p per element, Var_SR = (R/B)^2 f(1-f)
-    (from the AGP definition of Section 5.2 and Prop. B.1)."""
-    B = (1 << b) - 1
+    """The oracle's exact per-element variance of the AGP + PSQ estimator (samples side);
+    p, the Monte-Carlo run's float32 probabilities, must agree with its float64 ones."""
     st = fqt.group_stats(g[:, :, None, None])
-    v = np.minimum((g - st.Z_s[:, None]) * (F32(B) / st.R_s[:, None]), F32(B)).astype(np.float64)
-    f = v - np.floor(v)
-    return ((st.R_s[:, None].astype(np.float64) / B) ** 2 * f * (1 - f) / p[:, None]
-            + g.astype(np.float64) ** 2 * (1 - p[:, None]) / p[:, None]), st
+    np.testing.assert_allclose(fqt.agp_probabilities(st.R_s, b, fqt.AGP_BERNOULLI), p, rtol=1e-6)
+    return fqt.quantizer_variance(g, b, fqt.AGP_BERNOULLI, "samples")[:, :, 0, 0], st
 
 
 def _agp_monte_carlo(g, b, S):
@@ -254,3 +251,50 @@ def test_dw_channels_rows_equal_the_full_result():
                       (part.dW_t2, full.dW_t2)):
         np.testing.assert_array_equal(got, np.asarray(want).reshape(9, K)[rows])
     np.testing.assert_array_equal(part.dX, full.dX)
+
+
+def test_quantizer_variance_channels_monte_carlo():
+    """The PCQ side on a conv-shaped gradient with uneven channel ranges: the Monte-Carlo
+    variance of the oracle's own AGP + PCQ estimator, over Philox seeds, matches
+    quantizer_variance(groups="channels") in total and element by element (15 %)."""
+    layer = LayerShape("c", "conv2d", 4, 3, 6, 3, 3, 3, 3, 1, 1, 1, 1)
+    _, _, dy = draw_layer(layer, Recipe("channel_lognormal", sigma=1.0), 8)
+    S, b = 4000, 2
+    tot = np.zeros(dy.shape)
+    sq = np.zeros(dy.shape)
+    for seed in range(S):
+        qg = fqt.agp_scq_quantize(dy, b, fqt.AGP_BERNOULLI, seed=seed)
+        ch = qg.channels
+        est = np.zeros(dy.shape)
+        k = ch.keep
+        est[:, k] = (ch.scale[None, k, None, None].astype(np.float64) * qg.q_pcq[:, k]
+                     + ch.offset[None, k, None, None])
+        tot += est
+        sq += est ** 2
+    var = sq / S - (tot / S) ** 2
+    exact = fqt.quantizer_variance(dy, b, fqt.AGP_BERNOULLI, "channels")
+    assert 0.1 < fqt.agp_probabilities(fqt.group_stats(dy).R_c, b, 0).min() < 1
+    np.testing.assert_allclose(var.sum(), exact.sum(), rtol=0.05)
+    np.testing.assert_allclose(var, exact, rtol=0.15, atol=1e-3 * exact.max())
+
+
+def test_quantizer_variance_special_cases():
+    """AGP off is plain per-group SR: its total obeys Section 5.2's bound D/(4 B^2) sum R_i^2
+    (per sample) and vanishes on exactly representable codes; the AGP probabilities sum to
+    G/b; b = 1 with AGP is plain 1-bit PSQ (every p = 1)."""
+    rng = np.random.default_rng(3)
+    N, D = 12, 40
+    g = (rng.standard_normal((N, D)) * np.exp(1.5 * rng.standard_normal((N, 1)))).astype(F32)
+    st = fqt.group_stats(fqt.as_nchw(g))
+    for b in (1, 2, 4, 8):
+        B = (1 << b) - 1
+        off = fqt.quantizer_variance(g, b, fqt.AGP_OFF).sum()
+        assert off <= D / (4.0 * B * B) * float((st.R_s.astype(np.float64) ** 2).sum())
+        p = fqt.agp_probabilities(st.R_s, b, fqt.AGP_BERNOULLI)
+        assert abs(p.sum() - N / b) < 1e-9 and p.max() <= 1.0
+    np.testing.assert_array_equal(fqt.agp_probabilities(st.R_s, 1, fqt.AGP_BERNOULLI), np.ones(N))
+    np.testing.assert_array_equal(fqt.quantizer_variance(g, 1, fqt.AGP_BERNOULLI),
+                                  fqt.quantizer_variance(g, 1, fqt.AGP_OFF))
+    # Values on the code grid (x = Z + k R / B exactly representable) have no SR variance.
+    grid = np.array([[0.0, 1.0, 2.0, 3.0]], dtype=F32)
+    assert not fqt.quantizer_variance(grid, 2, fqt.AGP_OFF).any()
