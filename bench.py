@@ -28,6 +28,10 @@ sys.path.insert(0, ROOT)
 WORKLOAD = "vgg_cifar_conv3x3_256"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_I8_PEAK_TOPS = 5000.0     # MI355X dense int8 MFMA
+MFMA_FP4_PEAK_TOPS = 10100.0   # MI355X dense fp4 MFMA
+# VALU popcount: 256 CUs x 64 lanes x 2.4 GHz lane-ops; AND + popcount-accumulate of a 64-bit
+# word pair is 4 lane-ops for 64 binary multiply-accumulates (128 binary ops).
+POPC_PEAK_TOPS = 256 * 64 * 2.4e9 / 4 * 128 / 1e12
 SCRUB_BYTES = 1 << 30          # cold-cache runs overwrite this much (the last-level cache is 256 MB)
 
 # HBM traffic per launch of the products kernel from rocprofv3 counter runs of this benchmark
@@ -76,7 +80,7 @@ def parse():
                    help="report the cold-cache step time as ms_per_step (1 GiB overwritten "
                         "before every timed step) instead of the warm one")
     p.add_argument("--suite", choices=("resnet18_32px", "vgg16_224_bf16", "gemm_sweep", "forward",
-                                       "table5", "train", "variance", "baselines"),
+                                       "table5", "train", "variance", "baselines", "engines"),
                    help="instead of the benchmark line: per-layer times of a whole network's "
                         "layer backwards, the dW binary GEMM sweep, the binary forward of "
                         "the VGG CIFAR conv layer and of every ResNet-18 / VGG-16 layer, or "
@@ -409,6 +413,70 @@ def suite(name, reps=10):
                                     bits=bits, agp_mode=mode)
             print(json.dumps({"suite": name, "workload": "resnet18_32px", "variant": tag,
                               "ms_eager": out["ms_eager"]}), flush=True)
+        return
+
+    if name == "engines":
+        # The dW product on the three engines (Section 5.2 decomposition; Appendix C binary
+        # multiplication): int8 MFMA over the byte codes (the library's), VALU popcount over
+        # the bit planes (the paper's), and gfx950's fp4 MFMA over the planes expanded to
+        # e2m1.  Each against its own peak: int8 ops 2 * kept * K * R; popcount and fp4 issue
+        # one pass per plane, 2 * b * kept * K * R.  The fp4 time includes its expansion
+        # launches; the expansion-free product time is reported beside it.
+        from paper_2408_14267_amd.workloads import WORKLOADS as WL, gemm_sweep_points
+        pts = [("vgg_cifar_conv3x3_256", WL["vgg_cifar_conv3x3_256"].layers[0], 4,
+                fqt.FQT_AGP_BERNOULLI)]
+        pts += [(f"gemm_{M}x{M}x{K}", LayerShape(name="g", kind="linear", N=K, C=M, D=M), 1,
+                 fqt.FQT_AGP_OFF) for M, _, K in gemm_sweep_points() if M <= 8192]
+        for wname, L, bits, mode in pts:
+            desc = fqt.layer_desc(L)
+            cfg = fqt.quant_cfg(bits, mode, 0, 0, 0)
+            X = _gen(torch, L.x_shape, torch.float32, dev)
+            dY = _gen(torch, L.dy_shape, torch.float32, dev).contiguous()
+            K, P = L.C * L.kh * L.kw, L.Ho * L.Wo
+            R = L.N * P
+            Wr = (R + 63) // 64
+            q = fqt.QGrad(desc, cfg, device=dev)
+            fqt.fqt_agp_scq_quantize(desc, cfg, dY, q,
+                                     fqt.workspace(desc, cfg, fqt.FQT_WS_QUANTIZE, device=dev), st)
+            xwm = torch.empty(Wr * K, dtype=torch.int64, device=dev)
+            fqt.fqt_pack_input_signs(desc, X, xwm, st)
+            xb = torch.empty(K * Wr, dtype=torch.int64, device=dev)
+            xs = torch.empty(K, dtype=torch.int32, device=dev)
+            if L.kind == "linear":
+                fqt.fqt_pack_bits(X, fqt.FQT_F32, L.N, L.C, L.C, fqt.FQT_PACK_ALONG_ROWS, None, xb,
+                                  xs, st)
+            else:
+                fqt.fqt_pack_bits(X, fqt.FQT_F32, 0, 0, 0, fqt.FQT_PACK_IM2COL, desc, xb, xs, st)
+            dW = torch.empty((L.D, K), device=dev)
+            kept = int(q.pcq_count.item())
+            macs = kept * K * R
+            reps = 3 if macs > 2 ** 38 else 20
+            row = {"suite": name, "workload": wname, "bits": bits, "kept_channels": kept,
+                   "K": K, "R": R}
+            dws = fqt.workspace(desc, cfg, fqt.FQT_WS_GEMM_DW, device=dev)
+            f8 = lambda: fqt.fqt_binary_gemm_dw(desc, cfg, q, xwm, dW, dws, None, st)
+            f8()
+            t8 = timed(f8, reps)
+            row["int8"] = {"ms": round(t8, 5), "TOPS": round(2 * macs / t8 / 1e9, 1),
+                           "frac_of_peak": round(2 * macs / t8 / 1e9 / MFMA_I8_PEAK_TOPS, 4)}
+            for tag, eng, which, peak in (("popcount", fqt.FQT_ENGINE_POPCOUNT,
+                                           fqt.FQT_WS_DW_POPCOUNT, POPC_PEAK_TOPS),
+                                          ("fp4", fqt.FQT_ENGINE_FP4, fqt.FQT_WS_DW_FP4,
+                                           MFMA_FP4_PEAK_TOPS)):
+                if tag == "fp4" and bits > 4:
+                    continue
+                ws_e = fqt.workspace(desc, cfg, which, device=dev)
+                fe = lambda: fqt.fqt_binary_gemm_dw_planes(desc, cfg, q, xb, xs, dW, eng, ws_e,
+                                                           None, st)
+                fe()
+                te = timed(fe, reps)
+                ops = 2 * bits * macs
+                row[tag] = {"ms": round(te, 5), "TOPS": round(ops / te / 1e9, 1),
+                            "frac_of_peak": round(ops / te / 1e9 / peak, 4)}
+                del ws_e
+            print(json.dumps(row), flush=True)
+            del X, dY, q, xwm, xb, xs, dW, dws
+            torch.cuda.empty_cache()
         return
 
     if name == "table5":

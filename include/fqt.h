@@ -156,6 +156,8 @@ int fqt_qgrad_words(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
 #define FQT_WS_LAYER 1
 #define FQT_WS_GEMM_DW 2
 #define FQT_WS_FORWARD 3   /* fqt_binary_forward; cfg may be NULL for this one */
+#define FQT_WS_DW_POPCOUNT 4   /* fqt_binary_gemm_dw_planes, FQT_ENGINE_POPCOUNT */
+#define FQT_WS_DW_FP4 5        /* fqt_binary_gemm_dw_planes, FQT_ENGINE_FP4 */
 int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int32_t which,
                        size_t *bytes);
 
@@ -214,6 +216,30 @@ int fqt_pack_bits(const void *src, int32_t dtype, int64_t rows, int64_t cols, in
 int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
                        const fqt_qgrad *q, const uint64_t *xsign, float *dW, int32_t *I_out,
                        void *ws, size_t ws_bytes, void *hip_stream);
+
+/* The weight-gradient product from the paper's packed operands (Section 5.2's bit-plane
+ * decomposition; Appendix C, binary multiplication, average 1-bit and the {0,1} <-> {+-1}
+ * conversion): the same I and dW as fqt_binary_gemm_dw, from
+ *   q->pcq_planes  the PCQ code planes written by fqt_agp_scq_quantize, and
+ *   xbits          sign(unfold(X)) packed along N*Ho*Wo, uint64 [C*kh*kw][ceil(N*Ho*Wo/64)]
+ *                  (fqt_pack_bits FQT_PACK_IM2COL for a convolution, FQT_PACK_ALONG_ROWS of
+ *                  X [N][C] for a linear layer), with
+ *   xbits_linesum  its line sums, int32 [C*kh*kw] (fqt_pack_bits' linesum),
+ * I = sum_p 2^p (2 popcount(q_p & t) - popcount(q_p)) over the words.  engine:
+ *   FQT_ENGINE_POPCOUNT  AND + popcount on the vector ALUs (the paper's engine), any b;
+ *   FQT_ENGINE_FP4       both operands expanded once to e2m1 (a set bit 1.0, a clear one 0)
+ *                        and contracted by gfx950's scaled fp4 MFMA, one per plane with
+ *                        the plane weight 2^p as its scale; float32 sums are exact, so
+ *                        b <= 4 and (2^b - 1) * N*Ho*Wo < 2^24 (FQT_E_INVAL / FQT_E_SHAPE
+ *                        otherwise).
+ * ws: >= fqt_workspace_size(FQT_WS_DW_POPCOUNT or FQT_WS_DW_FP4) bytes, 256-byte aligned,
+ * no initialisation.  dW: float [D][C*kh*kw]; I_out (optional) int32 [D][C*kh*kw]. */
+#define FQT_ENGINE_POPCOUNT 1
+#define FQT_ENGINE_FP4 2
+int fqt_binary_gemm_dw_planes(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                              const fqt_qgrad *q, const uint64_t *xbits,
+                              const int32_t *xbits_linesum, float *dW, int32_t *I_out,
+                              int32_t engine, void *ws, size_t ws_bytes, void *hip_stream);
 
 /* sign(X) in the operand form of the dW product (Section 5.1 binarizer; Appendix C Alg. 2
  * and the Unfolder): the bits of fqt_pack_bits IM2COL for a convolution (ALONG_ROWS of X

@@ -9,7 +9,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfqt.so")
-SOURCES = ["fqt_api.hip", "fqt_quantize.hip", "fqt_pack.hip", "fqt_gemm.hip"]
+SOURCES = ["fqt_api.hip", "fqt_quantize.hip", "fqt_pack.hip", "fqt_gemm.hip", "fqt_engines.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -283,6 +283,8 @@ int fqt_workspace_size(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, int
   if (which == FQT_WS_QUANTIZE) *bytes = quant_ws_bytes(L);
   else if (which == FQT_WS_LAYER) *bytes = carve_layer_ws(nullptr, L, *cfg, nullptr);
   else if (which == FQT_WS_GEMM_DW) *bytes = gemm_dw_ws_bytes(L, *cfg);
+  else if (which == FQT_WS_DW_POPCOUNT) *bytes = engine_ws_bytes(L, *cfg, FQT_ENGINE_POPCOUNT);
+  else if (which == FQT_WS_DW_FP4) *bytes = engine_ws_bytes(L, *cfg, FQT_ENGINE_FP4);
   else return FQT_E_INVAL;
   return FQT_OK;
 }
@@ -347,6 +349,25 @@ int fqt_binary_gemm_dw(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg, con
     return FQT_E_ALIGN;
   if (ws_bytes < gemm_dw_ws_bytes(L, *cfg)) return FQT_E_WORKSPACE;
   return launch_gemm_dw(L, *cfg, *q, xsign, dW, I_out, ws, static_cast<hipStream_t>(hip_stream));
+}
+
+int fqt_binary_gemm_dw_planes(const fqt_layer_desc *desc, const fqt_quant_cfg *cfg,
+                              const fqt_qgrad *q, const uint64_t *xbits,
+                              const int32_t *xbits_linesum, float *dW, int32_t *I_out,
+                              int32_t engine, void *ws, size_t ws_bytes, void *hip_stream) {
+  Layer L;
+  FQT_TRY(make_layer(desc, &L));
+  FQT_TRY(check_cfg(cfg, L));
+  FQT_TRY(check_qgrad(q, false, true));
+  FQT_TRY(check_dw_range(L, *cfg));
+  FQT_TRY(check_engine(L, *cfg, engine));
+  if (!xbits || !xbits_linesum || !dW || !ws) return FQT_E_NULL;
+  if (!aligned(xbits, 8) || !aligned(xbits_linesum, 4) || !aligned(dW, 4) ||
+      (I_out && !aligned(I_out, 4)) || !aligned(ws, 256))
+    return FQT_E_ALIGN;
+  if (ws_bytes < engine_ws_bytes(L, *cfg, engine)) return FQT_E_WORKSPACE;
+  return launch_gemm_dw_planes(L, *cfg, *q, xbits, xbits_linesum, dW, I_out, engine, ws,
+                               static_cast<hipStream_t>(hip_stream));
 }
 
 int fqt_pack_input_signs(const fqt_layer_desc *desc, const void *X, uint64_t *dst,

@@ -125,6 +125,13 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
                     float *dW, void *dw_ws, const float2 *sslot, const float2 *cslot,
                     hipStream_t s);
 
+// The dW product from the code planes and line-major sign bits (popcount or fp4 engine).
+size_t engine_ws_bytes(const Layer &L, const fqt_quant_cfg &cfg, int engine);
+int check_engine(const Layer &L, const fqt_quant_cfg &cfg, int engine);
+int launch_gemm_dw_planes(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
+                          const uint64_t *xbits, const int32_t *xsum, float *dW, int32_t *I_out,
+                          int engine, void *ws, hipStream_t s);
+
 // Binary forward (Section 5.1): the operands and the product.
 // Word-major sign words [Wr][K] -> k-block-major [Kw][Wr * 64] (bit b of word (kb, r) is
 // line 64 kb + b of row r; lines past K are 0).

@@ -22,6 +22,8 @@ FQT_LINEAR, FQT_CONV2D = 0, 1
 FQT_AGP_BERNOULLI, FQT_AGP_TOPK, FQT_AGP_OFF = 0, 1, 2
 FQT_PACK_ALONG_ROWS, FQT_PACK_ALONG_COLS, FQT_PACK_IM2COL = 0, 1, 2
 FQT_WS_QUANTIZE, FQT_WS_LAYER, FQT_WS_GEMM_DW, FQT_WS_FORWARD = 0, 1, 2, 3
+FQT_WS_DW_POPCOUNT, FQT_WS_DW_FP4 = 4, 5
+FQT_ENGINE_POPCOUNT, FQT_ENGINE_FP4 = 1, 2
 FQT_WS_STATE_BYTES = 131072    # zeroed state at the start of quantize and layer workspaces
 FQT_MAX_BITS = 8
 FQT_NOALLOC_SCRATCH_BYTES = 64 << 20   # static workspace of fqt_layer_backward_noalloc
@@ -30,7 +32,7 @@ EXPORTED = ("fqt_status_string", "fqt_qgrad_words", "fqt_workspace_size", "fqt_a
             "fqt_pack_bits", "fqt_pack_input_signs", "fqt_binary_gemm_dw", "fqt_pack_weight_signs",
             "fqt_binary_gemm_dx",
             "fqt_layer_backward", "fqt_binary_forward", "fqt_workspace_init",
-            "fqt_layer_backward_noalloc", "fqt_binary_products")
+            "fqt_layer_backward_noalloc", "fqt_binary_products", "fqt_binary_gemm_dw_planes")
 
 
 class FqtError(RuntimeError):
@@ -84,6 +86,8 @@ def _load():
                                        c_void_p]),
         "fqt_layer_backward": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                        c_void_p, c_size_t, c_void_p]),
+        "fqt_binary_gemm_dw_planes": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p,
+                                              c_int32, c_void_p, c_size_t, c_void_p]),
         "fqt_binary_products": (c_int, [D, Q, G, c_void_p, c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, c_size_t, c_void_p]),
         "fqt_layer_backward_noalloc": (c_int, [D, Q, c_void_p, c_void_p, c_void_p, c_void_p,
@@ -178,6 +182,14 @@ def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, ws, I_out=None, stream=None)
     _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign), _ptr(dW),
                                    _ptr(I_out), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream(stream)), "fqt_binary_gemm_dw")
+
+
+def fqt_binary_gemm_dw_planes(desc, cfg, qgrad, xbits, xbits_linesum, dW, engine, ws, I_out=None,
+                              stream=None):
+    _check(_lib.fqt_binary_gemm_dw_planes(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xbits),
+                                          _ptr(xbits_linesum), _ptr(dW), _ptr(I_out), engine,
+                                          _ptr(ws), ws.numel() * ws.element_size(),
+                                          _stream(stream)), "fqt_binary_gemm_dw_planes")
 
 
 def fqt_pack_input_signs(desc, X, dst, stream=None):
