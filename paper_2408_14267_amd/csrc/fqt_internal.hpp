@@ -245,6 +245,24 @@ __device__ __forceinline__ void load_quad(const void *p, int64_t i, float out[4]
   }
 }
 
+// Load eight consecutive elements starting at i (i % 8 == 0, base 16-byte aligned): one
+// 16-byte load for bfloat16, two for float32.
+template <int DT>
+__device__ __forceinline__ void load_oct(const void *p, int64_t i, float out[8]) {
+  if (DT == FQT_BF16) {
+    const uint4 v = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p) + i);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      out[2 * k] = __uint_as_float(w[k] << 16);
+      out[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+    }
+  } else {
+    load_quad<DT>(p, i, out);
+    load_quad<DT>(p, i + 4, out + 4);
+  }
+}
+
 // Calls F.template operator()<DT>() with DT the compile-time dtype code of `dt`.
 template <typename F>
 __host__ void dispatch_dtype(int dt, F &&f) {

@@ -318,6 +318,7 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     BandGeom bg;
     size_t lds = 0;
     if (word_major && bit_geom(L, BITS_THREADS, 512, 48 * 1024, &bt, &lds)) {
+      bit_geom_vec(&bt, src);
       dispatch_dtype(dtype, [&]<int DT>() {
         hipLaunchKernelGGL(k_pack_im2col_bits<DT>, dim3(bit_blocks(bt)), dim3(BITS_THREADS), lds,
                            s, src, bt, dst);

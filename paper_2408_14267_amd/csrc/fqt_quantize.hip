@@ -1476,6 +1476,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     sg.npw = pack_w_blocks(L);
     uint32_t xblocks;
     if (with_bits) {
+      bit_geom_vec(&bt, signs->X);
       sg.bt = bt;
       xblocks = bit_blocks(bt);
     } else {

@@ -192,6 +192,8 @@ struct BitGeom {
   uint32_t own;               // 1: only the block's own words are loaded (whole samples)
   uint32_t cgroups, wgroups;
   FastDiv divP, divW, divTaps, divKw, divWB, divWg;
+  uint32_t vec;               // 1: X is 16-byte aligned and every word lies in one sample,
+                              //    so a lane loads 8 consecutive elements at once
 };
 
 constexpr int BIT_U = 8;        // sign words a wave loads back to back
@@ -250,9 +252,13 @@ inline bool bit_geom(const Layer &L, int nt, int64_t target_blocks, size_t lds_m
                uint32_t(cgroups), uint32_t(wgroups),
                make_fastdiv(uint32_t(L.P)), make_fastdiv(uint32_t(L.W)),
                make_fastdiv(uint32_t(L.kh * L.kw)), make_fastdiv(uint32_t(L.kw)),
-               make_fastdiv(uint32_t(WB)), make_fastdiv(uint32_t(wgroups))};
+               make_fastdiv(uint32_t(WB)), make_fastdiv(uint32_t(wgroups)), 0u};
   *lds = bytes;
   return true;
+}
+// The 8-elements-per-lane staging: words that never straddle samples and a 16-byte aligned X.
+inline void bit_geom_vec(BitGeom *g, const void *x) {
+  g->vec = (g->P % 64 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0) ? 1u : 0u;
 }
 inline uint32_t bit_blocks(const BitGeom &g) { return g.cgroups * g.wgroups; }
 
@@ -289,7 +295,30 @@ __device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, cons
   // Words the block loads: its own [w0, w0 + nw), or everything in the layer.
   const int32_t lo_w = g.own ? int32_t(w0) : 0;
   const int32_t hi_w = g.own ? int32_t(w0 + nw) : int32_t(g.Wr);
-  for (uint32_t it = wave; it < nch * nb; it += NW) {
+  if (g.vec) {
+    // Lane l takes positions 8 (l % 8) .. 8 (l % 8) + 7 of word l / 8 of the item with one
+    // 16-byte load (bf16; two for float32) and stores their 8 sign bits as one byte of the
+    // staged word: byte m of a word holds its positions 8 m .. 8 m + 7, least significant
+    // bit first, the same bits the per-position ballots give.
+    static_assert(U == 8, "one word per 8 lanes");
+    uint8_t *bytes = reinterpret_cast<uint8_t *>(bits);
+    const uint32_t k = uint32_t(lane) >> 3, m = uint32_t(lane) & 7u;
+    for (uint32_t it = wave; it < nch * nb; it += NW) {
+      const uint32_t c = it / nb, j0 = g.jl0 + (it - c * nb) * U;
+      const int32_t wa = int32_t(w0 + j0 + k) - int32_t(g.dlo);
+      const bool inw = wa >= lo_w && wa < hi_w;
+      const uint32_t u = uint32_t(min(max(wa, lo_w), hi_w - 1));
+      const uint32_t n = fdiv(u * 64, g.divP);
+      const int64_t e = (int64_t(n) * g.C + c0 + c) * g.P + int64_t(u - n * wps) * 64 + 8 * m;
+      float v[8];
+      load_oct<DT>(x, e, v);
+      uint32_t b = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) b |= (v[i] > 0.0f ? 1u : 0u) << i;
+      bytes[size_t(c * g.span + j0 + k) * 8 + m] = uint8_t(inw ? b : 0u);
+    }
+  }
+  for (uint32_t it = g.vec ? nch * nb : uint32_t(wave); it < nch * nb; it += NW) {
     const uint32_t c = it / nb, j0 = g.jl0 + (it - c * nb) * U;
     const int32_t wa0 = int32_t(w0 + j0) - int32_t(g.dlo);
     float v[U];
