@@ -122,6 +122,45 @@ def _check(status, where):
         raise FqtError(status, where)
 
 
+_TORCH_OF = {FQT_F32: torch.float32, FQT_BF16: torch.bfloat16}
+
+
+def _sizes(desc):
+    """Element counts of the layer's tensors and its packed-operand sizes: X, W, dY, the X
+    sign words (Wr * K) and the weight sign bytes (K * 64 * Wd)."""
+    if desc.kind == FQT_LINEAR:
+        P, K = 1, desc.C
+    else:
+        Ho = (desc.H + 2 * desc.ph - desc.kh) // desc.sh + 1
+        Wo = (desc.W + 2 * desc.pw - desc.kw) // desc.sw + 1
+        P, K = Ho * Wo, desc.C * desc.kh * desc.kw
+    HW = 1 if desc.kind == FQT_LINEAR else desc.H * desc.W
+    R = desc.N * P
+    return {"X": desc.N * desc.C * HW, "W": desc.D * K, "dY": R * desc.D,
+            "xsign": (R + 63) // 64 * K, "wsign": K * 64 * ((desc.D + 63) // 64), "K": K}
+
+
+def _need(where, *specs):
+    """Raise before any launch when a tensor cannot hold what the descriptor describes (a
+    kernel would read or write past it): specs are (tensor, dtype, elements, name[,
+    optional]); every shape check runs before the device check."""
+    for t, dtype, numel, name, *opt in specs:
+        what = f"{where}: {name}"
+        if t is None:
+            if opt and opt[0]:
+                continue
+            raise ValueError(f"{what}: a tensor is required")
+        if dtype is not None and t.dtype != dtype:
+            raise ValueError(f"{what}: dtype {t.dtype} does not match the descriptor's {dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{what}: tensor must be contiguous")
+        if t.numel() < numel:
+            raise ValueError(f"{what}: {t.numel()} elements, the descriptor needs {numel}")
+    for t, _, _, name, *opt in specs:
+        if t is not None and not t.is_cuda:
+            raise ValueError(f"{where}: {name}: expected a device tensor, got one on {t.device}")
+
+
 def dtype_code(dt):
     if dt in (torch.float32, "f32"):
         return FQT_F32
@@ -167,6 +206,8 @@ def fqt_workspace_init(ws, stream=None):
 
 
 def fqt_agp_scq_quantize(desc, cfg, dY, qgrad, ws, stream=None):
+    _need("fqt_agp_scq_quantize",
+          (dY, _TORCH_OF.get(desc.dy_dtype), _sizes(desc)["dY"], "dY"))
     _check(_lib.fqt_agp_scq_quantize(desc, cfg, _ptr(dY), ctypes.byref(qgrad.struct), _ptr(ws),
                                      ws.numel() * ws.element_size(), _stream(stream)),
            "fqt_agp_scq_quantize")
@@ -179,6 +220,11 @@ def fqt_pack_bits(src, dtype, rows, cols, ld, axis, conv, dst, linesum=None, str
 
 
 def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, ws, I_out=None, stream=None):
+    z = _sizes(desc)
+    _need("fqt_binary_gemm_dw",
+          (xsign, torch.int64, z["xsign"], "xsign"),
+          (dW, torch.float32, z["W"], "dW"),
+          (I_out, torch.int32, z["W"], "I_out", True))
     _check(_lib.fqt_binary_gemm_dw(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign), _ptr(dW),
                                    _ptr(I_out), _ptr(ws), ws.numel() * ws.element_size(),
                                    _stream(stream)), "fqt_binary_gemm_dw")
@@ -186,6 +232,12 @@ def fqt_binary_gemm_dw(desc, cfg, qgrad, xsign, dW, ws, I_out=None, stream=None)
 
 def fqt_binary_gemm_dw_planes(desc, cfg, qgrad, xbits, xbits_linesum, dW, engine, ws, I_out=None,
                               stream=None):
+    z = _sizes(desc)
+    _need("fqt_binary_gemm_dw_planes",
+          (xbits, torch.int64, z["xsign"], "xbits"),
+          (xbits_linesum, torch.int32, z["K"], "xbits_linesum"),
+          (dW, torch.float32, z["W"], "dW"),
+          (I_out, torch.int32, z["W"], "I_out", True))
     _check(_lib.fqt_binary_gemm_dw_planes(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xbits),
                                           _ptr(xbits_linesum), _ptr(dW), _ptr(I_out), engine,
                                           _ptr(ws), ws.numel() * ws.element_size(),
@@ -193,22 +245,44 @@ def fqt_binary_gemm_dw_planes(desc, cfg, qgrad, xbits, xbits_linesum, dW, engine
 
 
 def fqt_pack_input_signs(desc, X, dst, stream=None):
+    z = _sizes(desc)
+    _need("fqt_pack_input_signs",
+          (X, _TORCH_OF.get(desc.x_dtype), z["X"], "X"),
+          (dst, torch.int64, z["xsign"], "dst"))
     _check(_lib.fqt_pack_input_signs(desc, _ptr(X), _ptr(dst), _stream(stream)),
            "fqt_pack_input_signs")
 
 
 def fqt_pack_weight_signs(desc, W, dst, linesum, stream=None):
+    z = _sizes(desc)
+    _need("fqt_pack_weight_signs",
+          (W, _TORCH_OF.get(desc.w_dtype), z["W"], "W"),
+          (dst, torch.int8, z["wsign"], "dst"),
+          (linesum, torch.int32, z["K"], "linesum"))
     _check(_lib.fqt_pack_weight_signs(desc, _ptr(W), _ptr(dst), _ptr(linesum), _stream(stream)),
            "fqt_pack_weight_signs")
 
 
 def fqt_binary_gemm_dx(desc, cfg, qgrad, wsign, wsign_linesum, dX, I_out=None, stream=None):
+    z = _sizes(desc)
+    _need("fqt_binary_gemm_dx",
+          (wsign, torch.int8, z["wsign"], "wsign"),
+          (wsign_linesum, torch.int32, z["K"], "wsign_linesum"),
+          (dX, _TORCH_OF.get(desc.dx_dtype), z["X"], "dX"),
+          (I_out, torch.int32, z["X"], "I_out", True))
     _check(_lib.fqt_binary_gemm_dx(desc, cfg, ctypes.byref(qgrad.struct), _ptr(wsign),
                                    _ptr(wsign_linesum), _ptr(dX), _ptr(I_out), _stream(stream)),
            "fqt_binary_gemm_dx")
 
 
 def fqt_binary_products(desc, cfg, qgrad, xsign, wsign, wsign_linesum, dX, dW, ws, stream=None):
+    z = _sizes(desc)
+    _need("fqt_binary_products",
+          (xsign, torch.int64, z["xsign"], "xsign"),
+          (wsign, torch.int8, z["wsign"], "wsign"),
+          (wsign_linesum, torch.int32, z["K"], "wsign_linesum"),
+          (dX, _TORCH_OF.get(desc.dx_dtype), z["X"], "dX"),
+          (dW, torch.float32, z["W"], "dW"))
     _check(_lib.fqt_binary_products(desc, cfg, ctypes.byref(qgrad.struct), _ptr(xsign),
                                     _ptr(wsign), _ptr(wsign_linesum), _ptr(dX), _ptr(dW),
                                     _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
@@ -216,18 +290,39 @@ def fqt_binary_products(desc, cfg, qgrad, xsign, wsign, wsign_linesum, dX, dW, w
 
 
 def fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, stream=None):
+    z = _sizes(desc)
+    _need("fqt_layer_backward",
+          (X, _TORCH_OF.get(desc.x_dtype), z["X"], "X"),
+          (W, _TORCH_OF.get(desc.w_dtype), z["W"], "W"),
+          (dY, _TORCH_OF.get(desc.dy_dtype), z["dY"], "dY"),
+          (dX, _TORCH_OF.get(desc.dx_dtype), z["X"], "dX"),
+          (dW, torch.float32, z["W"], "dW"))
     _check(_lib.fqt_layer_backward(desc, cfg, _ptr(X), _ptr(W), _ptr(dY), _ptr(dX), _ptr(dW),
                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "fqt_layer_backward")
 
 
 def fqt_layer_backward_noalloc(desc, cfg, X, W, dY, dX, dW, stream=None):
+    z = _sizes(desc)
+    _need("fqt_layer_backward_noalloc",
+          (X, _TORCH_OF.get(desc.x_dtype), z["X"], "X"),
+          (W, _TORCH_OF.get(desc.w_dtype), z["W"], "W"),
+          (dY, _TORCH_OF.get(desc.dy_dtype), z["dY"], "dY"),
+          (dX, _TORCH_OF.get(desc.dx_dtype), z["X"], "dX"),
+          (dW, torch.float32, z["W"], "dW"))
     _check(_lib.fqt_layer_backward_noalloc(desc, cfg, _ptr(X), _ptr(W), _ptr(dY), _ptr(dX),
                                            _ptr(dW), _stream(stream)),
            "fqt_layer_backward_noalloc")
 
 
 def fqt_binary_forward(desc, X, W, gamma, Y, I_out, ws, stream=None):
+    z = _sizes(desc)
+    _need("fqt_binary_forward",
+          (X, _TORCH_OF.get(desc.x_dtype), z["X"], "X"),
+          (W, _TORCH_OF.get(desc.w_dtype), z["W"], "W"),
+          (gamma, torch.float32, desc.D, "gamma"),
+          (Y, _TORCH_OF.get(desc.dy_dtype), z["dY"], "Y"),
+          (I_out, torch.int32, z["dY"], "I_out", True))
     _check(_lib.fqt_binary_forward(desc, _ptr(X), _ptr(W), _ptr(gamma), _ptr(Y), _ptr(I_out),
                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "fqt_binary_forward")

@@ -198,3 +198,42 @@ def test_noalloc_rejects_layers_beyond_its_scratch_before_launch():
     st = lib.fqt_layer_backward_noalloc(ctypes.byref(d2), ctypes.byref(c), fake, fake,
                                         ctypes.c_void_p((1 << 20) + 4), fake, fake, None)
     assert st == fqt.FQT_E_ALIGN
+
+
+def test_binding_sizes_follow_the_descriptor():
+    # 3x3 conv 256 -> 256 on 8x8, N = 128: R = 8192 rows, K = 2304 lines, Wd = 4 words of D.
+    z = fqt._sizes(_desc())
+    assert z == {"X": 128 * 256 * 64, "W": 256 * 2304, "dY": 128 * 256 * 64,
+                 "xsign": 128 * 2304, "wsign": 2304 * 64 * 4, "K": 2304}
+    lin = fqt._sizes(fqt.layer_desc(LayerShape("fc", "linear", 32, 256, 128)))
+    assert lin == {"X": 32 * 256, "W": 128 * 256, "dY": 32 * 128, "xsign": 256,
+                   "wsign": 256 * 128, "K": 256}
+    # Strided, padded conv: Ho = Wo = (9 + 2 - 3) // 2 + 1 = 5.
+    st = fqt._sizes(fqt.layer_desc(LayerShape("c", "conv2d", 2, 3, 5, 9, 9, 3, 3, 2, 2, 1, 1)))
+    assert st["dY"] == 2 * 5 * 25 and st["xsign"] == 1 * 27 and st["X"] == 2 * 3 * 81
+
+
+def test_binding_rejects_mismatched_tensors_before_launch():
+    torch = pytest.importorskip("torch")
+    L = WORKLOADS["vgg_cifar_conv3x3_256"].layers[0]
+    d = fqt.layer_desc(L, fqt.FQT_BF16, fqt.FQT_BF16, fqt.FQT_F32, fqt.FQT_BF16)
+    c = fqt.quant_cfg(4)
+    z = fqt._sizes(d)
+    X = torch.empty(z["X"], dtype=torch.bfloat16)
+    W = torch.empty(z["W"], dtype=torch.float32)
+    dY = torch.empty(z["dY"], dtype=torch.bfloat16)
+    dW = torch.empty(z["W"], dtype=torch.float32)
+    ws = torch.empty(16, dtype=torch.uint8)
+    # A float32 X against a bf16 descriptor (the kernels would read twice its bytes).
+    with pytest.raises(ValueError, match="dtype"):
+        fqt.fqt_layer_backward(d, c, X.float(), W, dY, X, dW, ws)
+    with pytest.raises(ValueError, match="elements"):
+        fqt.fqt_layer_backward(d, c, X, W, dY[:-1], X, dW, ws)
+    with pytest.raises(ValueError, match="contiguous"):
+        fqt.fqt_pack_input_signs(d, X.view(2, -1).t(), torch.empty(z["xsign"], dtype=torch.int64))
+    with pytest.raises(ValueError, match="elements"):
+        fqt.fqt_pack_weight_signs(d, W, torch.empty(z["wsign"] - 1, dtype=torch.int8),
+                                  torch.empty(z["K"], dtype=torch.int32))
+    # Everything the descriptor asks for, but host memory: still refused, nothing launched.
+    with pytest.raises(ValueError, match="device tensor"):
+        fqt.fqt_layer_backward(d, c, X, W, dY, X, dW, ws)
