@@ -7,9 +7,10 @@
 // chain gives I = sum_j q_j s_j exactly in int32.  For b = 8 the codes do not fit a
 // signed byte: the MFMA takes q - 128 and 128 * (sum of the signs it saw) is added back.
 //   dX: the weight signs arrive expanded to +-1 bytes (fqt_pack_weight_signs), so the
-//       inner loop is two 16-byte buffer loads and one MFMA.  The zero-point term
-//       c = sum over the valid taps of the per-(channel, tap) sign sums is a float32
-//       MFMA over the taps (exact: integers below 2^24).
+//       inner loop is 16-byte buffer loads and MFMAs.  The zero-point term c = sum over
+//       the valid taps of the per-(channel, tap) sign sums is summed per output in the
+//       split form and, in the register-tile form, is one float16 (D <= 2048) or a few
+//       float32 MFMAs of the sign sums against the 0/1 reach flags (exact either way).
 //   dW: the X signs stay packed; each 16-bit piece is expanded in registers to +-1
 //       bytes once and feeds up to four MFMAs (128 kept channels).  c = 2 popcount - len.
 // The rescale S * I + Z' * c is one float32 step per output without contraction.
@@ -17,7 +18,9 @@
 // MFMA layouts (32 x 32 outputs, 16 accumulators per lane): lane l feeds row (src0) and
 // column (src1) l % 32; in the i8 form its 16 bytes are contraction positions
 // 16 (l / 32) .. 16 (l / 32) + 15, in the f32 32x32x2 form its one value is position
-// l / 32.  Lane l then holds column l % 32 at rows 8 (v / 4) + 4 (l / 32) + (v % 4).
+// l / 32, in the f16 32x32x16 form its 8 values are 8 of the 16 positions (the same
+// ones in both operands).  Lane l then holds column l % 32 at rows
+// 8 (v / 4) + 4 (l / 32) + (v % 4).
 //
 // Operands are read through buffer resources: a lane whose row does not exist (padding
 // tap, pruned slot, channel past the end) gets the offset BUF_NONE, past every buffer,
@@ -36,6 +39,7 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // The wave index as a scalar, so that per-wave loop bounds and strides stay in SGPRs.
 __device__ __forceinline__ uint32_t wave_id() {
@@ -67,6 +71,22 @@ __device__ __forceinline__ v16i mfma_i8(v4i a, v4i b, v16i c) {
 
 __device__ __forceinline__ float rescale(float S, int I, float Zp, float c) {
   return __fadd_rn(__fmul_rn(S, float(I)), __fmul_rn(Zp, c));
+}
+
+// The dispatcher hands the workgroups of a launch to the eight XCDs in turn (block b to
+// XCD b % 8), and each XCD has its own L2.  xcd_tile maps the s-th block of a segment of n
+// blocks to a tile index so that every XCD walks runs of RUN consecutive tiles: its k-th
+// run (in dispatch order) is tiles [RUN (8 k + x), RUN (8 k + x + 1)) for x = s % 8, and
+// neighbouring tiles, which read the same operand rows, share one L2.  A bijection of
+// [0, n): blocks past the last whole round of 8 runs keep their own index.  (Any other
+// dispatch order changes only which L2 a tile's operands go through.)
+constexpr uint32_t XCDS = 8;
+template <uint32_t RUN>
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t s, uint32_t n) {
+  constexpr uint32_t ROUND = XCDS * RUN;
+  if (s >= n / ROUND * ROUND) return s;
+  const uint32_t x = s % XCDS, i = s / XCDS;
+  return ((i / RUN) * XCDS + x) * RUN + i % RUN;
 }
 
 // Output row (0..31) of accumulator v of a lane in half-wave g.
@@ -699,16 +719,21 @@ struct DxArgs {
   uint32_t N, C, H, W, HW, Ho, Wo, P, R, Dp, ctiles, CHW, taps, nch;   // nch = Dp / 32
   uint32_t codes_bytes, wsb_bytes;
   int kh, kw, sh, sw, ph, pw;
-  FastDiv divHW, divW, divKw, divNch, divCt;
+  FastDiv divHW, divW, divKw, divNch, divCt, divSh, divSw;
   uint32_t nblocks;              // blocks of the dX grid (compute tiles + zero pool)
   uint32_t zpieces;              // pieces of DX_ZCHUNK elements per pruned sample
-  uint32_t wide;                 // 1: four pixel tiles per block, one per wave
+  uint32_t wide;                 // 0: split form; CT >= 1: register tiles, CT channel tiles
+  uint32_t cblocks;              // register-tile form: channel blocks of 32 CT channels
+  FastDiv divCb;
 };
 
 constexpr int DX_MAX_TAPS = 64;
 constexpr uint32_t DX_ZCHUNK = 65536;    // elements of a pruned sample one block zeroes
 constexpr int DX_WAVES = 4;
 constexpr int DX_THREADS = DX_WAVES * 64;
+// Tiles (channel tiles fastest, then pixel tiles) of one XCD run: 16 split-form tiles of
+// 32 x 32, 32 register-form tiles of 256 pixels x 32 CT channels.
+constexpr uint32_t DX_XCD_RUN = 16, DXW_XCD_RUN = 32;
 
 // NB: contraction steps (tap, 32 bytes of D) a wave loads at once, sized on the host so
 // that the common shapes take one batch: the loads of a wave then cost one memory latency.
@@ -749,8 +774,49 @@ __device__ __forceinline__ void dx_zero_pool(const DxArgs &a, uint32_t zb, uint3
   }
 }
 
+// The code-row offsets of a block's BP pixel rows m0 .. m0 + BP - 1 over the taps:
+// rowoff[tap][p] = 32 * (code row of the output pixel that pixel m0 + p meets through the
+// tap), BUF_NONE where the tap falls between strides or outside dY, or past the live rows.
+// Thread t decodes pixel p = t % BP once and walks the taps t / BP, t / BP + NT / BP, ...
+// (a pixel's taps differ only in the tap's (i, j)).
+template <uint32_t BP, int NT>
+__device__ __forceinline__ void dx_row_table(const DxArgs &a, uint32_t m0, uint32_t live_rows,
+                                             uint32_t (*rowoff)[BP]) {
+  static_assert(NT % BP == 0, "whole pixel sets per pass");
+  constexpr uint32_t STEP = NT / BP;
+  const uint32_t p = uint32_t(threadIdx.x) % BP;
+  const uint32_t m = m0 + p;
+  const bool live = m < live_rows;
+  uint32_t slot = 0, h = 0, w = 0;
+  if (live) {
+    slot = fdiv(m, a.divHW);
+    const uint32_t pix = m - slot * a.HW;
+    h = fdiv(pix, a.divW);
+    w = pix - h * a.W;
+  }
+  uint32_t tap = uint32_t(threadIdx.x) / BP;
+  uint32_t ti = fdiv(tap, a.divKw), tj = tap - ti * uint32_t(a.kw);
+  for (; tap < a.taps; tap += STEP) {
+    uint32_t off = BUF_NONE;
+    const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
+    if (live && th >= 0 && tw >= 0) {
+      const uint32_t ho = fdiv(uint32_t(th), a.divSh), wo = fdiv(uint32_t(tw), a.divSw);
+      if (ho * uint32_t(a.sh) == uint32_t(th) && wo * uint32_t(a.sw) == uint32_t(tw) &&
+          ho < a.Ho && wo < a.Wo)
+        off = (slot * a.P + ho * a.Wo + wo) * 32;
+    }
+    rowoff[tap][p] = off;
+    tj += STEP;
+    while (tj >= uint32_t(a.kw)) {
+      tj -= uint32_t(a.kw);
+      ++ti;
+    }
+  }
+}
+
 template <bool B8, int NB>
 __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm) {
+  bid = xcd_tile<DX_XCD_RUN>(bid, a.nblocks);
   const int t = threadIdx.x, lane = t & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
@@ -799,23 +865,7 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
     const int e = t + k * DX_THREADS;
     if (e < 32 * taps) sm.wl[e >> 5][e & 31] = wlv[k];
   }
-  for (int e = t; e < 32 * taps; e += DX_THREADS) {
-    const int p = e & 31, tap = e >> 5;
-    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
-    const uint32_t m = m0 + p;
-    uint32_t off = BUF_NONE;
-    if (m < live_rows) {
-      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
-      const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
-      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
-      if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
-        const int ho = th / a.sh, wo = tw / a.sw;
-        if (ho < int(a.Ho) && wo < int(a.Wo))
-          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
-      }
-    }
-    sm.rowoff[tap][p] = off;
-  }
+  dx_row_table<32, DX_THREADS>(a, m0, live_rows, sm.rowoff);
   __syncthreads();
 
   // This lane: A row = channel c0 + i, B column = pixel m0 + i.
@@ -877,56 +927,60 @@ __device__ __forceinline__ void dx_body(const DxArgs &a, uint32_t bid, DxLds &sm
   }
 }
 
-// Large layers (many row tiles, at most DXW_MAX_TAPS taps): a block holds four pixel
-// tiles of 32 rows and one channel tile; wave w runs the whole contraction of tile w (no
-// split over the waves, no reduction), the four waves sharing the sign operand through
-// the L1 cache.  The per-(tap, pixel) code row offsets of the block's 128 pixels and the
-// channel sign sums are tabulated in LDS as in the split form.
-constexpr int DXW_TILES = DX_WAVES;
+// Large layers (many row tiles, at most DXW_MAX_TAPS taps): register tiles.  A block
+// holds 4 * DXT_RT pixel tiles of 32 rows and CT channel tiles; wave w runs the whole
+// contraction of pixel tiles DXT_RT w .. DXT_RT (w + 1) - 1 against all CT channel tiles
+// (no split over the waves, no reduction), so each loaded sign fragment feeds DXT_RT
+// MFMAs and each code fragment CT of them: (DXT_RT + CT) 1 KB loads per DXT_RT * CT
+// products instead of two per product.  The per-(tap, pixel) code row
+// offsets of the block's pixels and the channel sign sums are tabulated in LDS as in the
+// split form.  CT = 2 unless the layer has a single channel tile.
 constexpr int DXW_MAX_TAPS = 16;
-struct alignas(16) DxWideLds {
-  uint32_t rowoff[DXW_MAX_TAPS][DXW_TILES * 32];
-  int32_t wl[DXW_MAX_TAPS][32];
-  int32_t pix_out[DXW_TILES * 32];
-  float pix_s[DXW_TILES * 32], pix_z[DXW_TILES * 32];
+constexpr int DXT_RT = 2;                            // pixel tiles per wave
+constexpr int DXT_NB = 4;                            // contraction steps per load batch
+constexpr uint32_t DXT_BP = DX_WAVES * DXT_RT * 32;  // pixel rows per block
+template <int CT>
+struct alignas(16) DxTileLds {
+  uint32_t rowoff[DXW_MAX_TAPS][DXT_BP];
+  int32_t wl[DXW_MAX_TAPS][CT * 32];
+  int32_t pix_out[DXT_BP];
+  float pix_s[DXT_BP], pix_z[DXT_BP];
 };
 
-template <bool B8, int NB>
-__device__ __forceinline__ void dx_body_wide(const DxArgs &a, uint32_t bid, DxWideLds &sm) {
-  constexpr uint32_t BP = DXW_TILES * 32;        // pixel rows per block
+template <bool B8, int CT>
+__device__ __forceinline__ void dx_body_tiles(const DxArgs &a, uint32_t bid, DxTileLds<CT> &sm) {
+  static_assert(DXT_BP == DX_THREADS, "one pixel row per thread");
+  bid = xcd_tile<DXW_XCD_RUN>(bid, a.nblocks);
+  constexpr uint32_t BP = DXT_BP;
+  constexpr int CW = CT * 32;                    // channels per block
   const int t = threadIdx.x, lane = t & 63;
   const uint32_t wave = wave_id();
   const int i = lane & 31, g = lane >> 5;
   const int count = *a.count;
-  const uint32_t mt = fdiv(bid, a.divCt);
-  const uint32_t m0 = mt * BP, c0 = (bid - mt * a.ctiles) * 32;
+  const uint32_t mt = fdiv(bid, a.divCb);
+  const uint32_t m0 = mt * BP, c0 = (bid - mt * a.cblocks) * CW;
   const int taps = int(a.taps);
   // Loads that do not depend on the count issue with it (clamped indices).
-  int kn = 0;
-  float2 sz = make_float2(0.0f, 0.0f);
-  uint32_t ppix = 0;
-  if (t < int(BP)) {
-    const uint32_t m = min(m0 + uint32_t(t), a.N * a.HW - 1);
-    const uint32_t pslot = fdiv(m, a.divHW);
-    ppix = m - pslot * a.HW;
-    kn = a.kept[pslot];
-    if (a.slot_sz) sz = a.slot_sz[pslot];
-  }
-  constexpr int WLT = DXW_MAX_TAPS * 32 / DX_THREADS;
+  const uint32_t m = min(m0 + uint32_t(t), a.N * a.HW - 1);
+  const uint32_t pslot = fdiv(m, a.divHW);
+  const uint32_t ppix = m - pslot * a.HW;
+  const int kn = a.kept[pslot];
+  float2 sz = a.slot_sz ? a.slot_sz[pslot] : make_float2(0.0f, 0.0f);
+  constexpr int WLT = DXW_MAX_TAPS * CW / DX_THREADS;
   int wlv[WLT];
 #pragma unroll
   for (int k = 0; k < WLT; ++k) {
-    const int e = t + k * DX_THREADS, p = e & 31, tap = e >> 5;
+    const int e = t + k * DX_THREADS, p = e % CW, tap = e / CW;
     const uint32_t ch = c0 + uint32_t(p);
-    wlv[k] = (e < 32 * taps && ch < a.C) ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
+    wlv[k] = (tap < taps && ch < a.C) ? a.wlsum[ch * a.taps + uint32_t(tap)] : 0;
   }
   const uint32_t live_rows = uint32_t(count) * a.HW;
-  const uint32_t live_blocks = ((live_rows + BP - 1) / BP) * a.ctiles;
+  const uint32_t live_blocks = ((live_rows + BP - 1) / BP) * a.cblocks;
   if (bid >= live_blocks) {
     dx_zero_pool(a, bid - live_blocks, a.nblocks - live_blocks, count);
     return;
   }
-  if (t < int(BP)) {
+  {
     const bool live = m0 + uint32_t(t) < live_rows;
     if (!a.slot_sz && live) sz = make_float2(a.scale[kn], a.offset[kn]);
     sm.pix_out[t] = live ? int(uint32_t(kn) * a.CHW + ppix) : -1;
@@ -936,90 +990,116 @@ __device__ __forceinline__ void dx_body_wide(const DxArgs &a, uint32_t bid, DxWi
 #pragma unroll
   for (int k = 0; k < WLT; ++k) {
     const int e = t + k * DX_THREADS;
-    if (e < 32 * taps) sm.wl[e >> 5][e & 31] = wlv[k];
+    if (e / CW < taps) sm.wl[e / CW][e % CW] = wlv[k];
   }
-  for (int e = t; e < int(BP) * taps; e += DX_THREADS) {
-    const int p = e % int(BP), tap = e / int(BP);
-    const uint32_t ti = fdiv(uint32_t(tap), a.divKw), tj = uint32_t(tap) - ti * a.kw;
-    const uint32_t m = m0 + uint32_t(p);
-    uint32_t off = BUF_NONE;
-    if (m < live_rows) {
-      const uint32_t slot = fdiv(m, a.divHW), pix = m - slot * a.HW;
-      const uint32_t h = fdiv(pix, a.divW), w = pix - h * a.W;
-      const int th = int(h) + a.ph - int(ti), tw = int(w) + a.pw - int(tj);
-      if (th >= 0 && tw >= 0 && th % a.sh == 0 && tw % a.sw == 0) {
-        const int ho = th / a.sh, wo = tw / a.sw;
-        if (ho < int(a.Ho) && wo < int(a.Wo))
-          off = (slot * a.P + uint32_t(ho) * a.Wo + uint32_t(wo)) * 32;
-      }
-    }
-    sm.rowoff[tap][p] = off;
-  }
+  dx_row_table<BP, DX_THREADS>(a, m0, live_rows, sm.rowoff);
   __syncthreads();
 
-  // This lane: A row = channel c0 + i, B column = pixel m0 + 32 wave + i.
-  const uint32_t px = wave * 32 + uint32_t(i);
-  const uint32_t ch = c0 + i;
-  const uint32_t abase = ch < a.C ? ch * 32 + 16 * g : BUF_NONE;
+  // This lane: A rows = channels c0 + 32 ct + i, B columns = pixels 32 (DXT_RT wave + rt) + i.
+  uint32_t px[DXT_RT], abase[CT];
+#pragma unroll
+  for (int rt = 0; rt < DXT_RT; ++rt) px[rt] = (wave * DXT_RT + uint32_t(rt)) * 32 + uint32_t(i);
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    const uint32_t ch = c0 + uint32_t(32 * ct + i);
+    abase[ct] = ch < a.C ? ch * 32 + 16 * g : BUF_NONE;
+  }
   const __amdgpu_buffer_rsrc_t ars = buffer_of(a.wsb, a.wsb_bytes);
   const __amdgpu_buffer_rsrc_t brs = buffer_of(a.codes, a.codes_bytes);
   const uint32_t steps = a.taps * a.nch;
-  v16i acc = {0};
-  for (uint32_t s0 = 0; s0 < steps; s0 += NB) {
-    v4i A[NB], B[NB];
+  v16i acc[DXT_RT][CT];
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
+  for (int rt = 0; rt < DXT_RT; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = v16i{0};
+  for (uint32_t s0 = 0; s0 < steps; s0 += DXT_NB) {
+    // A batch's loads all issue before its first product; a step past the end reads zeros
+    // through its A operands and adds nothing.
+    v4i A[DXT_NB][CT], B[DXT_NB][DXT_RT];
+#pragma unroll
+    for (int u = 0; u < DXT_NB; ++u) {
       const uint32_t st0 = s0 + u;
       const bool live = st0 < steps;
       const uint32_t st = live ? st0 : 0;
       const uint32_t tap = fdiv(st, a.divNch);
       const uint32_t kc = st - tap * a.nch;
-      A[u] = load16(ars, live ? abase : BUF_NONE, (kc * a.taps + tap) * a.C * 32);
-      B[u] = load16(brs, sm.rowoff[tap][px] + 16 * g, kc * a.R * 32);
+      const uint32_t aoff = (kc * a.taps + tap) * a.C * 32;
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) A[u][ct] = load16(ars, live ? abase[ct] : BUF_NONE, aoff);
+#pragma unroll
+      for (int rt = 0; rt < DXT_RT; ++rt)
+        B[u][rt] = load16(brs, sm.rowoff[tap][px[rt]] + 16 * g, kc * a.R * 32);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int u = 0; u < NB; ++u) acc = mfma_i8(A[u], B8 ? bias128(B[u]) : B[u], acc);
+    for (int u = 0; u < DXT_NB; ++u)
+#pragma unroll
+      for (int rt = 0; rt < DXT_RT; ++rt) {
+        const v4i b = B8 ? bias128(B[u][rt]) : B[u][rt];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = mfma_i8(A[u][ct], b, acc[rt][ct]);
+      }
   }
 
-  const int off = sm.pix_out[px];
-  if (off < 0) return;                    // rows past the count belong to the zero blocks
-  const float S = sm.pix_s[px], Z = sm.pix_z[px];
-  int c[16], lt[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) { c[v] = 0; lt[v] = 0; }
-  for (int tap = 0; tap < taps; ++tap) {
-    const bool reach = sm.rowoff[tap][px] != BUF_NONE;
+  for (int rt = 0; rt < DXT_RT; ++rt) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {          // rows 8 q + 4 g .. + 3 = acc_row(4 q .. 4 q + 3, g)
-      const int4 w4 = *reinterpret_cast<const int4 *>(&sm.wl[tap][8 * q + 4 * g]);
-      c[4 * q + 0] += reach ? w4.x : 0; c[4 * q + 1] += reach ? w4.y : 0;
-      c[4 * q + 2] += reach ? w4.z : 0; c[4 * q + 3] += reach ? w4.w : 0;
-      if (B8) {
-        lt[4 * q + 0] += w4.x; lt[4 * q + 1] += w4.y; lt[4 * q + 2] += w4.z; lt[4 * q + 3] += w4.w;
+    for (int ct = 0; ct < CT; ++ct) {
+      // Zero-point term of each output, c = sum over the taps that reach the pixel of the
+      // channel's line sign sum: the 32 x 32 product [channel][tap] x [tap][pixel] of the
+      // sign sums and the 0/1 reach flags in the accumulator layout of the tile.  Exact:
+      // with D <= 2048 every sign sum is a float16 integer and all taps go into one f16
+      // MFMA (lane half g holds taps 8 g .. 8 g + 7); else two taps per float32 MFMA.
+      v16f cz = v16f{0};
+      if (a.Dp <= 2048) {
+        f16x8 wa, rb;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int tap = 8 * g + k;
+          const bool in = tap < taps;
+          wa[k] = in ? _Float16(sm.wl[tap][32 * ct + i]) : _Float16(0.0f);
+          rb[k] = in && sm.rowoff[tap][px[rt]] != BUF_NONE ? _Float16(1.0f) : _Float16(0.0f);
+        }
+        cz = __builtin_amdgcn_mfma_f32_32x32x16_f16(wa, rb, cz, 0, 0, 0);
+      } else {
+        for (int j = 0; 2 * j < taps; ++j) {
+          const int tap = 2 * j + g;
+          const bool in = tap < taps;
+          const float wv = in ? float(sm.wl[tap][32 * ct + i]) : 0.0f;
+          const float rv = in && sm.rowoff[tap][px[rt]] != BUF_NONE ? 1.0f : 0.0f;
+          cz = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, rv, cz, 0, 0, 0);
+        }
+      }
+      const int off = sm.pix_out[px[rt]];
+      if (off < 0) continue;               // rows past the count belong to the zero blocks
+      const float S = sm.pix_s[px[rt]], Z = sm.pix_z[px[rt]];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = 32 * ct + acc_row(v, g);
+        const uint32_t cc = c0 + uint32_t(row);
+        if (cc >= a.C) continue;
+        int lt = 0;
+        if (B8)
+          for (int tap = 0; tap < taps; ++tap) lt += sm.wl[tap][row];
+        const int Iv = acc[rt][ct][v] + (B8 ? 128 * lt : 0);
+        const float out = rescale(S, Iv, Z, cz[v]);
+        const size_t o = size_t(off) + size_t(cc) * a.HW;
+        if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
+        else static_cast<float *>(a.dX)[o] = out;
+        if (a.I_out) a.I_out[o] = Iv;
       }
     }
   }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const uint32_t cc = c0 + uint32_t(acc_row(v, g));
-    if (cc >= a.C) continue;
-    const int Iv = acc[v] + (B8 ? 128 * lt[v] : 0);
-    const float out = rescale(S, Iv, Z, float(c[v]));
-    const size_t o = size_t(off) + size_t(cc) * a.HW;
-    if (a.dx_t == FQT_BF16) static_cast<uint16_t *>(a.dX)[o] = f32_to_bf16(out);
-    else static_cast<float *>(a.dX)[o] = out;
-    if (a.I_out) a.I_out[o] = Iv;
-  }
 }
 
-template <bool WIDE>
-using DxLdsOf = std::conditional_t<WIDE, DxWideLds, DxLds>;
+// WT: 0 for the split form, CT (1 or 2 channel tiles per wave) for the register-tile form.
+template <int WT>
+using DxLdsOf = std::conditional_t<WT != 0, DxTileLds<WT == 0 ? 1 : WT>, DxLds>;
 
-template <bool B8, int NB, bool WIDE>
+template <bool B8, int NB, int WT>
 __global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
-  __shared__ DxLdsOf<WIDE> sm;
-  if constexpr (WIDE) dx_body_wide<B8, NB>(a, blockIdx.x, sm);
+  __shared__ DxLdsOf<WT> sm;
+  if constexpr (WT != 0) dx_body_tiles<B8, WT>(a, blockIdx.x, sm);
   else dx_body<B8, NB>(a, blockIdx.x, sm);
 }
 
@@ -1030,19 +1110,19 @@ enum DwForm { DWF_PARTS = 0, DWF_DIRECT = 1, DWF_KRED = 2 };
 
 // Both products in one launch (the layer backward): blocks [0, ndw) are dW blocks, the rest
 // dX blocks; the two share one LDS allocation.
-template <bool WIDE>
+template <int WT>
 union ProductsLds {
-  DxLdsOf<WIDE> dx;
+  DxLdsOf<WT> dx;
   DwRedLds dw;
 };
-template <bool B8, int NB, int DWF, bool WIDE>
+template <bool B8, int NB, int DWF, int WT>
 __global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
-  __shared__ ProductsLds<WIDE> sm;
+  __shared__ ProductsLds<WT> sm;
   if (blockIdx.x < ndw) {
     if constexpr (DWF == DWF_KRED) dw_kred_body<B8>(dwa, blockIdx.x, sm.dw);
     else dw_part_body<B8, DWF == DWF_DIRECT>(dwa, blockIdx.x);
   } else {
-    if constexpr (WIDE) dx_body_wide<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
+    if constexpr (WT != 0) dx_body_tiles<B8, WT>(dxa, blockIdx.x - ndw, sm.dx);
     else dx_body<B8, NB>(dxa, blockIdx.x - ndw, sm.dx);
   }
 }
@@ -1295,15 +1375,18 @@ DxArgs make_dx_args(const Layer &L, const fqt_qgrad &q, const int8_t *wsb,
   a.divHW = make_fastdiv(uint32_t(L.HW)); a.divW = make_fastdiv(uint32_t(L.W));
   a.divKw = make_fastdiv(uint32_t(L.kw)); a.divNch = make_fastdiv(a.nch);
   a.divCt = make_fastdiv(a.ctiles);
+  a.divSh = make_fastdiv(uint32_t(L.sh)); a.divSw = make_fastdiv(uint32_t(L.sw));
   // Capacity tiles plus a pool of blocks that only zero pruned samples, a piece of at most
   // DX_ZCHUNK elements each: whatever the device-side count, at least
   // min(2048, N * pieces) blocks are left for the zeroing.
   a.zpieces = uint32_t((int64_t(a.CHW) + DX_ZCHUNK - 1) / DX_ZCHUNK);
   // Four pixel tiles per block once the capacity has 16384 tiles (with few taps).
   const int64_t tiles = ((L.N * L.HW + 31) / 32) * a.ctiles;
-  a.wide = (a.taps <= uint32_t(DXW_MAX_TAPS) && tiles >= 16384) ? 1u : 0u;
-  const int64_t rows = a.wide ? DXW_TILES * 32 : 32;
-  a.nblocks = uint32_t(((L.N * L.HW + rows - 1) / rows) * a.ctiles +
+  a.wide = (a.taps <= uint32_t(DXW_MAX_TAPS) && tiles >= 16384) ? (a.ctiles > 1 ? 2u : 1u) : 0u;
+  a.cblocks = a.wide ? (a.ctiles + a.wide - 1) / a.wide : a.ctiles;
+  a.divCb = make_fastdiv(a.cblocks);
+  const int64_t rows = a.wide ? DXT_BP : 32;
+  a.nblocks = uint32_t(((L.N * L.HW + rows - 1) / rows) * a.cblocks +
                        std::min<int64_t>(2048, L.N * int64_t(a.zpieces)));
   return a;
 }
@@ -1386,18 +1469,20 @@ int launch_gemm_dx(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
   const DxArgs a = make_dx_args(L, q, wsb, wlsum, dX, I_out);
   const dim3 grid(a.nblocks);
   const int nb = dx_batch(a);
-  auto go = [&]<bool B8, bool WIDE>() {
-    if (nb == 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
-    else if (nb == 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
-    else hipLaunchKernelGGL((k_mfma_dx<B8, 10, WIDE>), grid, dim3(DX_THREADS), 0, s, a);
+  auto go = [&]<bool B8, int WT>() {
+    if constexpr (WT != 0)      // the register-tile form batches DXT_NB steps itself
+      hipLaunchKernelGGL((k_mfma_dx<B8, 4, WT>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (nb == 4) hipLaunchKernelGGL((k_mfma_dx<B8, 4, 0>), grid, dim3(DX_THREADS), 0, s, a);
+    else if (nb == 8) hipLaunchKernelGGL((k_mfma_dx<B8, 8, 0>), grid, dim3(DX_THREADS), 0, s, a);
+    else hipLaunchKernelGGL((k_mfma_dx<B8, 10, 0>), grid, dim3(DX_THREADS), 0, s, a);
   };
-  if (cfg.bits == 8) {
-    if (a.wide) go.template operator()<true, true>();
-    else go.template operator()<true, false>();
-  } else {
-    if (a.wide) go.template operator()<false, true>();
-    else go.template operator()<false, false>();
-  }
+  auto go2 = [&]<bool B8>() {
+    if (a.wide == 2) go.template operator()<B8, 2>();
+    else if (a.wide == 1) go.template operator()<B8, 1>();
+    else go.template operator()<B8, 0>();
+  };
+  if (cfg.bits == 8) go2.template operator()<true>();
+  else go2.template operator()<false>();
   return last_launch_status();
 }
 
@@ -1427,21 +1512,25 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
                       : kred ? dw_kred_blocks(L, dwa) : dw_part_blocks(L, dwa);
   const dim3 grid(ndw + dxa.nblocks);
   const int nb = dx_batch(dxa);
-  auto go = [&]<bool B8, int DWF, bool WIDE>() {
-    if (nb == 4)
-      hipLaunchKernelGGL((k_products<B8, 4, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
-                         dwa, ndw);
+  auto go = [&]<bool B8, int DWF, int WT>() {
+    if constexpr (WT != 0)
+      hipLaunchKernelGGL((k_products<B8, 4, DWF, WT>), grid, dim3(DX_THREADS), 0, s, dxa, dwa,
+                         ndw);
+    else if (nb == 4)
+      hipLaunchKernelGGL((k_products<B8, 4, DWF, 0>), grid, dim3(DX_THREADS), 0, s, dxa, dwa,
+                         ndw);
     else if (nb == 8)
-      hipLaunchKernelGGL((k_products<B8, 8, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
-                         dwa, ndw);
+      hipLaunchKernelGGL((k_products<B8, 8, DWF, 0>), grid, dim3(DX_THREADS), 0, s, dxa, dwa,
+                         ndw);
     else
-      hipLaunchKernelGGL((k_products<B8, 10, DWF, WIDE>), grid, dim3(DX_THREADS), 0, s, dxa,
-                         dwa, ndw);
+      hipLaunchKernelGGL((k_products<B8, 10, DWF, 0>), grid, dim3(DX_THREADS), 0, s, dxa, dwa,
+                         ndw);
     if (DWF == DWF_PARTS) launch_dw_finish<B8>(L, dwa, s);
   };
   auto go2 = [&]<bool B8, int DWF>() {
-    if (dxa.wide) go.template operator()<B8, DWF, true>();
-    else go.template operator()<B8, DWF, false>();
+    if (dxa.wide == 2) go.template operator()<B8, DWF, 2>();
+    else if (dxa.wide == 1) go.template operator()<B8, DWF, 1>();
+    else go.template operator()<B8, DWF, 0>();
   };
   auto go3 = [&]<bool B8>() {
     // With the dW product in its own launch the products launch has no dW blocks: the big
