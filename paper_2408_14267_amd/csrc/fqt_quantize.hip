@@ -1124,21 +1124,23 @@ __device__ __forceinline__ float unit24(uint32_t u) {
 // b-bit stochastic rounding code of x (Section 3.2): v = clamp((x - Z) * inv, 0, B),
 // q = floor(v) + [u < v - floor(v)] for the uniform u = u24 * 2^-24 (the same test as
 // u24 < frac(v) * 2^24: both sides scale by a power of two).  inv = 0 (R = 0) gives q = 0.
+// For 0 <= v <= 255 the truncating conversion is floor(v) and v_fract_f32 gives
+// v - floor(v) exactly.
 __device__ __forceinline__ uint32_t sr_code(float x, float z, float inv, float Bf, float u) {
   float v = __fmul_rn(__fsub_rn(x, z), inv);
   v = fminf(fmaxf(v, 0.0f), Bf);
-  const float fl = floorf(v);
-  return static_cast<uint32_t>(fl) + (u < __fsub_rn(v, fl) ? 1u : 0u);
+  return static_cast<uint32_t>(v) + (u < __builtin_amdgcn_fractf(v) ? 1u : 0u);
 }
 // b = 1: v is clamped to [0, 1], so q = [u < v]; as u < 1, the test on the unclamped
 // product gives the same bit (true for v >= 1, false for v <= 0 and for NaN).
 __device__ __forceinline__ uint32_t sr_bit(float x, float z, float inv, float u) {
   return u < __fmul_rn(__fsub_rn(x, z), inv) ? 1u : 0u;
 }
+// The code of x in group p, whose parameters in LDS have inv = 0 when the group is pruned:
+// then v = (x - z) * 0 is 0 or NaN and both rounding forms give 0 (also for R = 0).
 template <bool ONE>
 __device__ __forceinline__ uint32_t sr_any(float x, const GroupParam &p, float Bf, float u) {
-  const uint32_t c = ONE ? sr_bit(x, p.z, p.inv, u) : sr_code(x, p.z, p.inv, Bf, u);
-  return p.rank >= 0 ? c : 0u;
+  return ONE ? sr_bit(x, p.z, p.inv, u) : sr_code(x, p.z, p.inv, Bf, u);
 }
 
 struct QPackArgs {
@@ -1236,6 +1238,7 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
       const uint32_t n = fdiv(r, g.divP);
       p = a.sp[n];
       if (p.rank >= 0) row = int32_t(uint32_t(p.rank) * g.P + (r - n * g.P));
+      else p.inv = 0.0f;                        // pruned: every code 0
     }
     spar[t] = p;
     prow[t] = row;
@@ -1244,6 +1247,7 @@ __global__ __launch_bounds__(THREADS) void k_qpack(QPackArgs a) {
     GroupParam p;
     p.z = 0.0f; p.inv = 0.0f; p.rank = -1; p.pad = 0;
     if (d < g.D) p = a.cp[d];
+    if (p.rank < 0) p.inv = 0.0f;               // pruned: every code 0
     cpar[t - TILE] = p;
   }
   __syncthreads();
