@@ -548,17 +548,21 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
     }
   }
 }
-// Blocks of the big form with CT column tiles per wave (two row tiles).
-uint32_t dw_big_blocks(uint32_t D, uint32_t K, int ct) {
-  return ((D + 63) / 64) * ((K + DW_WAVES * 32 * ct - 1) / (DW_WAVES * 32 * ct));
+// Blocks of the big form with RT row tiles and CT column tiles per wave.
+uint32_t dw_big_blocks(uint32_t D, uint32_t K, int rt, int ct) {
+  return ((D + 32 * rt - 1) / (32 * rt)) * ((K + DW_WAVES * 32 * ct - 1) / (DW_WAVES * 32 * ct));
 }
 
-// Split-R partials in the big form (long slices of the contraction, wide outputs).
-template <bool B8>
+// Split-R partials in the big form (long slices of the contraction, wide outputs): two row
+// tiles per wave, or one when the kept channels are expected to fit 32 rows (a second
+// row tile would multiply zeros).
+template <bool B8, int RT>
 __global__ __launch_bounds__(DW_THREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) void k_mfma_dw_split(DwArgs a) {
-  dw_big_body<B8, 2, 2, 2, true>(a, blockIdx.x);
+  dw_big_body<B8, RT, 2, 2, true>(a, blockIdx.x);
 }
-uint32_t dw_split_blocks(const DwArgs &a) { return a.S * dw_big_blocks(a.D, a.K, 2); }
+uint32_t dw_split_blocks(const DwArgs &a, int rt) {
+  return a.S * dw_big_blocks(a.D, a.K, rt, 2);
+}
 
 // Long contractions: two waves per SIMD (the accumulators and the word ring fit 256
 // registers).
@@ -1409,18 +1413,30 @@ bool dw_big(const Layer &L, const DwArgs &a) {
 bool dw_split_big(const Layer &L, const DwArgs &a) {
   return a.S > 1 && L.Wr >= 8192 && a.wps >= 16;
 }
+// Row tiles of the split form: one when the expected kept channels (D, or D / b with AGP)
+// fit 32 rows.
+int dw_split_rt(const Layer &L, const fqt_quant_cfg &cfg) {
+  const int64_t dkeep =
+      cfg.agp_mode == FQT_AGP_OFF ? L.D : (L.D + cfg.bits - 1) / std::max(cfg.bits, 1);
+  return dkeep <= 32 ? 1 : 2;
+}
 template <bool B8>
-void launch_dw_split(const DwArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(k_mfma_dw_split<B8>, dim3(dw_split_blocks(a)), dim3(DW_THREADS), 0, s, a);
+void launch_dw_split(const DwArgs &a, int rt, hipStream_t s) {
+  if (rt == 1)
+    hipLaunchKernelGGL((k_mfma_dw_split<B8, 1>), dim3(dw_split_blocks(a, 1)), dim3(DW_THREADS), 0,
+                       s, a);
+  else
+    hipLaunchKernelGGL((k_mfma_dw_split<B8, 2>), dim3(dw_split_blocks(a, 2)), dim3(DW_THREADS), 0,
+                       s, a);
 }
 
 template <bool B8>
 void launch_dw_big(const DwArgs &a, hipStream_t s) {
   if (a.Wr >= uint32_t(DWB_LONG_WORDS))
-    hipLaunchKernelGGL(k_mfma_dw_big<B8>, dim3(dw_big_blocks(a.D, a.K, 4)), dim3(DW_THREADS), 0,
-                       s, a);
+    hipLaunchKernelGGL(k_mfma_dw_big<B8>, dim3(dw_big_blocks(a.D, a.K, 2, 4)), dim3(DW_THREADS),
+                       0, s, a);
   else
-    hipLaunchKernelGGL(k_mfma_dw_short<B8>, dim3(dw_big_blocks(a.D, a.K, 2)), dim3(DW_THREADS),
+    hipLaunchKernelGGL(k_mfma_dw_short<B8>, dim3(dw_big_blocks(a.D, a.K, 2, 2)), dim3(DW_THREADS),
                        0, s, a);
 }
 
@@ -1448,7 +1464,7 @@ int launch_gemm_dw(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q,
       hipLaunchKernelGGL(k_mfma_dw_kred<B8>, dim3(dw_kred_blocks(L, a)), dim3(DW_THREADS), 0, s,
                          a);
     } else if (dw_split_big(L, a)) {
-      launch_dw_split<B8>(a, s);
+      launch_dw_split<B8>(a, dw_split_rt(L, cfg), s);
       launch_dw_finish<B8>(L, a, s);
     } else if (a.S == 1) {
       hipLaunchKernelGGL((k_mfma_dw_part<B8, true>), grid, dim3(DW_THREADS), 0, s, a);
@@ -1505,8 +1521,8 @@ int launch_products(const Layer &L, const fqt_quant_cfg &cfg, const fqt_qgrad &q
     if (cfg.bits == 8) launch_dw_big<true>(dwa, s);
     else launch_dw_big<false>(dwa, s);
   } else if (split_big) {
-    if (cfg.bits == 8) launch_dw_split<true>(dwa, s);
-    else launch_dw_split<false>(dwa, s);
+    if (cfg.bits == 8) launch_dw_split<true>(dwa, dw_split_rt(L, cfg), s);
+    else launch_dw_split<false>(dwa, dw_split_rt(L, cfg), s);
   }
   const uint32_t ndw = (big || split_big) ? 0u
                       : kred ? dw_kred_blocks(L, dwa) : dw_part_blocks(L, dwa);

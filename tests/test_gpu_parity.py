@@ -82,9 +82,13 @@ CASES = [
      Recipe("sample_lognormal", sigma=1.0), "f32"),
     ("conv_bigmap_8_samples_b2", LayerShape("c", "conv2d", 8, 4, 70, 256, 256, 3, 3, 1, 1, 1, 1),
      2, 0, Recipe("sample_lognormal", sigma=1.0), "f32"),
-    # 524288 rows, b = 8: the long split-R dW partials in 64 x 64 wave tiles, biased codes.
+    # 524288 rows, b = 8: the long split-R dW partials, biased codes; about 5 kept channels
+    # expected, so one row tile per wave.
     ("conv_bigmap_b8", LayerShape("c", "conv2d", 8, 4, 40, 256, 256, 3, 3, 1, 1, 1, 1), 8, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # The same long split-R partials with about 40 kept channels: two row tiles per wave.
+    ("conv_bigmap_rt2_b2", LayerShape("c", "conv2d", 8, 4, 80, 256, 256, 3, 3, 1, 1, 1, 1), 2,
+     0, Recipe("channel_lognormal", sigma=1.0), "f32"),
     # 16384 dX tiles of 32 x 32: the dX product in its four-tiles-per-block form.
     ("conv_wide_dx_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
