@@ -1290,13 +1290,14 @@ __global__ __launch_bounds__(FWD_THREADS) void k_mfma_fwd(FwdArgs a) {
 // Splits of the dW contraction over N*Ho*Wo: enough 32x32 wave tiles of the expected
 // kept channels (all of them without AGP, about D / b with it) to give about 1024 waves
 // while every split keeps at least 16 words (1024 positions), and at most 256 words per
-// split, within at most DW_MAX_SPLITS splits, 128 MB of partials and one batch of words
-// per split.
+// split (about 64 in the long split form, below), within at most DW_MAX_SPLITS splits,
+// 128 MB of partials and one batch of words per split.
 constexpr int64_t DW_TARGET_WAVES = 1024;
 constexpr int64_t DW_MIN_WORDS = 16;
 constexpr int64_t DW_MAX_WORDS = 256;
 constexpr int64_t DW_MAX_SPLITS = 4096;
 constexpr int64_t DW_MAX_PART_BYTES = int64_t(128) << 20;
+constexpr int64_t DW_SPLIT_WORDS = 64;
 int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   const int64_t dkeep =
       cfg.agp_mode == FQT_AGP_OFF ? L.D : std::max<int64_t>(1, (L.D + cfg.bits - 1) / cfg.bits);
@@ -1305,9 +1306,20 @@ int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
                                 (L.Wr + DW_MIN_WORDS - 1) / DW_MIN_WORDS),
                        (L.Wr + DW_MAX_WORDS - 1) / DW_MAX_WORDS);
   const int64_t kp = ((L.K + 31) / 32) * 32;
-  S = std::min(S, std::max<int64_t>(1, DW_MAX_PART_BYTES / (L.D * kp * 4)));
+  const int64_t part_cap = std::max<int64_t>(1, DW_MAX_PART_BYTES / (L.D * kp * 4));
+  S = std::min(S, part_cap);
   S = std::min(S, DW_MAX_SPLITS);
   S = std::min(S, (L.Wr + DW_PREF - 1) / DW_PREF);
+  // Long contractions in the split form (their own launch: at least 8192 words, slices of
+  // at least 16): slices of about DW_SPLIT_WORDS words, so that each wave's chain of loads
+  // is short, while the many-split finish keeps at most 4 splits per block of its
+  // D x ceil(Kp / 64) blocks (its reduction over the splits is serial per thread).
+  if (S > 1 && L.Wr >= 8192 && (L.Wr + S - 1) / S >= 16) {
+    int64_t Sb = std::min((L.Wr + DW_SPLIT_WORDS - 1) / DW_SPLIT_WORDS,
+                          4 * L.D * ((kp + 63) / 64));
+    Sb = std::min(std::min(Sb, part_cap), DW_MAX_SPLITS);
+    S = std::max(S, Sb);
+  }
   return int(std::max<int64_t>(S, 1));
 }
 
