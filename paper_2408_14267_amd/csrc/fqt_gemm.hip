@@ -1298,6 +1298,7 @@ constexpr int64_t DW_MAX_WORDS = 256;
 constexpr int64_t DW_MAX_SPLITS = 4096;
 constexpr int64_t DW_MAX_PART_BYTES = int64_t(128) << 20;
 constexpr int64_t DW_SPLIT_WORDS = 64;
+constexpr int64_t DW_SPLIT_MIN = 512;         // contraction words of the split form, at least
 int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   const int64_t dkeep =
       cfg.agp_mode == FQT_AGP_OFF ? L.D : std::max<int64_t>(1, (L.D + cfg.bits - 1) / cfg.bits);
@@ -1310,11 +1311,11 @@ int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   S = std::min(S, part_cap);
   S = std::min(S, DW_MAX_SPLITS);
   S = std::min(S, (L.Wr + DW_PREF - 1) / DW_PREF);
-  // Long contractions in the split form (their own launch: at least 8192 words, slices of
-  // at least 16): slices of about DW_SPLIT_WORDS words, so that each wave's chain of loads
-  // is short, while the many-split finish keeps at most 4 splits per block of its
+  // Long contractions in the split form (their own launch: at least DW_SPLIT_MIN words,
+  // slices of at least 16): slices of about DW_SPLIT_WORDS words, so that each wave's chain
+  // of loads is short, while the many-split finish keeps at most 4 splits per block of its
   // D x ceil(Kp / 64) blocks (its reduction over the splits is serial per thread).
-  if (S > 1 && L.Wr >= 8192 && (L.Wr + S - 1) / S >= 16) {
+  if (S > 1 && L.Wr >= DW_SPLIT_MIN && (L.Wr + S - 1) / S >= 16) {
     int64_t Sb = std::min((L.Wr + DW_SPLIT_WORDS - 1) / DW_SPLIT_WORDS,
                           4 * L.D * ((kp + 63) / 64));
     Sb = std::min(std::min(Sb, part_cap), DW_MAX_SPLITS);
@@ -1419,11 +1420,12 @@ bool dw_big(const Layer &L, const DwArgs &a) {
   return a.S == 1 && ((L.D + 63) / 64) * ((L.K + 63) / 64) >= 1024;
 }
 
-// Split-R products over very long contractions (N*Ho*Wo of 2^19 rows and more, slices of
-// 16 words and more): the partials in the big form's 64 x 64 wave tiles.  Shorter ones stay
-// in the products launch, where their partial blocks overlap the dX blocks.
+// Split-R products over long contractions (N*Ho*Wo of DW_SPLIT_MIN words and more, slices
+// of 16 words and more): the partials in the big form's wave tiles, in a launch of their
+// own.  Shorter ones stay in the products launch, where their partial blocks overlap the dX
+// blocks.
 bool dw_split_big(const Layer &L, const DwArgs &a) {
-  return a.S > 1 && L.Wr >= 8192 && a.wps >= 16;
+  return a.S > 1 && L.Wr >= DW_SPLIT_MIN && a.wps >= 16;
 }
 // Row tiles of the split form: one when the expected kept channels (D, or D / b with AGP)
 // fit 32 rows.
