@@ -1298,7 +1298,7 @@ constexpr int64_t DW_MAX_WORDS = 256;
 constexpr int64_t DW_MAX_SPLITS = 4096;
 constexpr int64_t DW_MAX_PART_BYTES = int64_t(128) << 20;
 constexpr int64_t DW_SPLIT_WORDS = 64;
-constexpr int64_t DW_SPLIT_MIN = 512;         // contraction words of the split form, at least
+constexpr int64_t DW_SPLIT_MIN = 768;         // contraction words of the split form, at least
 int gemm_dw_splits(const Layer &L, const fqt_quant_cfg &cfg) {
   const int64_t dkeep =
       cfg.agp_mode == FQT_AGP_OFF ? L.D : std::max<int64_t>(1, (L.D + cfg.bits - 1) / cfg.bits);
