@@ -177,9 +177,17 @@ __device__ __forceinline__ Ctr4 philox4x32_10(Ctr4 c, uint32_t k0, uint32_t k1) 
     const uint64_t p0 = uint64_t(0xD2511F53u) * c.v[0];
     const uint64_t p1 = uint64_t(0xCD9E8D57u) * c.v[2];
     Ctr4 n;
-    n.v[0] = uint32_t(p1 >> 32) ^ c.v[1] ^ k0;
+    if (r < 2) {
+      // Counter words that are the same across a wave (stream, layer, step) keep the
+      // first rounds partly on the scalar unit; plain XORs leave the compiler that choice.
+      n.v[0] = uint32_t(p1 >> 32) ^ c.v[1] ^ k0;
+      n.v[2] = uint32_t(p0 >> 32) ^ c.v[3] ^ k1;
+    } else {
+      // Both XORs in one instruction (bitop3 with truth table 0x96 = a ^ b ^ c).
+      n.v[0] = __builtin_amdgcn_bitop3_b32(uint32_t(p1 >> 32), c.v[1], k0, 0x96);
+      n.v[2] = __builtin_amdgcn_bitop3_b32(uint32_t(p0 >> 32), c.v[3], k1, 0x96);
+    }
     n.v[1] = uint32_t(p1);
-    n.v[2] = uint32_t(p0 >> 32) ^ c.v[3] ^ k1;
     n.v[3] = uint32_t(p0);
     c = n;
   }

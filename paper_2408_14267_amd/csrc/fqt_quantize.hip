@@ -1125,10 +1125,11 @@ __device__ __forceinline__ float unit24(uint32_t u) {
 // q = floor(v) + [u < v - floor(v)] for the uniform u = u24 * 2^-24 (the same test as
 // u24 < frac(v) * 2^24: both sides scale by a power of two).  inv = 0 (R = 0) gives q = 0.
 // For 0 <= v <= 255 the truncating conversion is floor(v) and v_fract_f32 gives
-// v - floor(v) exactly.
+// v - floor(v) exactly.  The clamp is one v_med3_f32; a NaN product (inf * 0) makes it
+// return the minimum of its three inputs, 0, as max-then-min would.
 __device__ __forceinline__ uint32_t sr_code(float x, float z, float inv, float Bf, float u) {
   float v = __fmul_rn(__fsub_rn(x, z), inv);
-  v = fminf(fmaxf(v, 0.0f), Bf);
+  v = __builtin_amdgcn_fmed3f(v, 0.0f, Bf);
   return static_cast<uint32_t>(v) + (u < __builtin_amdgcn_fractf(v) ? 1u : 0u);
 }
 // b = 1: v is clamped to [0, 1], so q = [u < v]; as u < 1, the test on the unclamped
