@@ -390,5 +390,12 @@ __device__ __forceinline__ uint64_t wave_scan_add_u64(uint64_t v) {
 #undef FQT_DPP_ADD64
   return v;
 }
+// Sum of v over the wave, in every lane (the scan's last lane, read as two scalars).
+__device__ __forceinline__ uint64_t wave_total_u64(uint64_t v) {
+  const uint64_t s = wave_scan_add_u64(v);
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(s)), 63));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(s >> 32)), 63));
+  return (uint64_t(hi) << 32) | lo;
+}
 
 }  // namespace fqt

@@ -902,51 +902,114 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
     // usually take a few rounds (ranges that decay geometrically over the groups take the
     // most); past SAT_ROUNDS the sort below decides instead.
     constexpr int SAT_ROUNDS = 8;
-    __shared__ uint64_t rsum[2][SEL_NW];
-    __shared__ int32_t rcnt[2][SEL_NW];
-    uint64_t W = 0;
-    {
-      const uint64_t ws = wave_scan_add_u64(own_w);
-      if (lane == 63) rsum[1][wave] = ws;
+    if constexpr (GP <= 256) {
+      // Each wave that holds groups runs the rounds itself over all G weights (lane l holds
+      // groups l + 64 m): wave scans and ballots, no barrier per round; all of them reach the
+      // same result, and one barrier hands the outcome to the other waves.  The weights
+      // pass through sbuf[0], which the sort below reuses only after that barrier.
+      constexpr int M = GP / 64;
+      const int nw = (G + 63) / 64;
+      __shared__ uint64_t sat_out[2];        // s_sat (or ~0 when the rounds did not settle), W
+      if (t < GP) sbuf[0][t] = t < G ? own_w : 0ull;
       __syncthreads();
+      if (wave < nw) {
+        uint64_t wl[M];
+        uint64_t tot = 0;
 #pragma unroll
-      for (int w = 0; w < GP / 64; ++w) W += rsum[1][w];
-    }
-    int64_t s = 0;
-    bool done = false;
-    for (int round = 0; round < SAT_ROUNDS; ++round) {
-      const int64_t A = int64_t(G) - int64_t(b) * s;
-      const bool pass = t < G && !own_sat && own_w > 0 &&
-                        A * int64_t(own_w) >= int64_t(b) * int64_t(W);
-      const uint64_t ws = wave_scan_add_u64(pass ? own_w : 0ull);
-      const int32_t wc = __builtin_popcountll(__ballot(pass));
-      const int buf = round & 1;
-      if (lane == 63) {
-        rsum[buf][wave] = ws;
-        rcnt[buf][wave] = wc;
+        for (int m = 0; m < M; ++m) {
+          wl[m] = m < nw ? sbuf[0][lane + 64 * m] : 0ull;
+          tot += wl[m];
+        }
+        uint64_t W = wave_total_u64(tot);
+        int64_t s = 0;
+        bool done = false;
+        uint32_t satm = 0;                   // bit m: group lane + 64 m saturated
+        for (int round = 0; round < SAT_ROUNDS; ++round) {
+          const int64_t A = int64_t(G) - int64_t(b) * s;
+          uint64_t ps = 0;
+          uint32_t pm = 0;
+          int32_t cnt = 0;
+#pragma unroll
+          for (int m = 0; m < M; ++m) {
+            if (m >= nw) break;
+            // Groups past G hold weight 0 and never pass.
+            const bool pass = !((satm >> m) & 1u) && wl[m] > 0 &&
+                              A * int64_t(wl[m]) >= int64_t(b) * int64_t(W);
+            ps += pass ? wl[m] : 0ull;
+            pm |= pass ? (1u << m) : 0u;
+            cnt += __builtin_popcountll(__ballot(pass));
+          }
+          if (cnt == 0) {
+            done = true;
+            break;
+          }
+          const uint64_t sum = wave_total_u64(ps);
+          satm |= pm;
+          s += cnt;
+          W -= sum;
+        }
+        own_sat = t < G && ((satm >> wave) & 1u);
+        if (t == 0) {
+          sat_out[0] = done ? uint64_t(s) : ~0ull;
+          sat_out[1] = W;
+        }
       }
       __syncthreads();
-      uint64_t sum = 0;
-      int32_t cnt = 0;
-#pragma unroll
-      for (int w = 0; w < GP / 64; ++w) {
-        sum += rsum[buf][w];
-        cnt += rcnt[buf][w];
+      if (sat_out[0] != ~0ull) {
+        s_sat = int64_t(sat_out[0]);
+        w_rem = s_sat < G ? sat_out[1] : 0;
+      } else {
+        own_sat = false;
+        need_sort = true;
       }
-      if (cnt == 0) {
-        done = true;
-        break;
-      }
-      own_sat = own_sat || pass;
-      s += cnt;
-      W -= sum;
-    }
-    if (done) {
-      s_sat = s;
-      w_rem = s < G ? W : 0;
     } else {
-      own_sat = false;
-      need_sort = true;
+      // Up to 1024 groups: one group per thread, the round sums combined through LDS.
+      __shared__ uint64_t rsum[2][SEL_NW];
+      __shared__ int32_t rcnt[2][SEL_NW];
+      uint64_t W = 0;
+      {
+        const uint64_t ws = wave_scan_add_u64(own_w);
+        if (lane == 63) rsum[1][wave] = ws;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < GP / 64; ++w) W += rsum[1][w];
+      }
+      int64_t s = 0;
+      bool done = false;
+      for (int round = 0; round < SAT_ROUNDS; ++round) {
+        const int64_t A = int64_t(G) - int64_t(b) * s;
+        const bool pass = t < G && !own_sat && own_w > 0 &&
+                          A * int64_t(own_w) >= int64_t(b) * int64_t(W);
+        const uint64_t ws = wave_scan_add_u64(pass ? own_w : 0ull);
+        const int32_t wc = __builtin_popcountll(__ballot(pass));
+        const int buf = round & 1;
+        if (lane == 63) {
+          rsum[buf][wave] = ws;
+          rcnt[buf][wave] = wc;
+        }
+        __syncthreads();
+        uint64_t sum = 0;
+        int32_t cnt = 0;
+#pragma unroll
+        for (int w = 0; w < GP / 64; ++w) {
+          sum += rsum[buf][w];
+          cnt += rcnt[buf][w];
+        }
+        if (cnt == 0) {
+          done = true;
+          break;
+        }
+        own_sat = own_sat || pass;
+        s += cnt;
+        W -= sum;
+      }
+      if (done) {
+        s_sat = s;
+        w_rem = s < G ? W : 0;
+      } else {
+        own_sat = false;
+        need_sort = true;
+      }
     }
   }
   if (need_sort) {
