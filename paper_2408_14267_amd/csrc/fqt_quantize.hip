@@ -1086,9 +1086,20 @@ __device__ __forceinline__ void select_fused_body(const SelectArgs &a, int set) 
       keep = lh < rh || (lh == rh && ll < rl);
     }
   }
-  int32_t count;
-  const int32_t rank = block_incl_scan<GP / 64, int32_t>(keep ? 1 : 0, scr_i, count, lane, wave) -
-                       (keep ? 1 : 0);
+  // Rank among the kept groups: kept lanes below this one in the wave (mbcnt of the
+  // ballot) plus the kept counts of the waves before it.
+  const uint64_t kb = __ballot(keep);
+  const int32_t below = int32_t(__builtin_amdgcn_mbcnt_hi(
+      uint32_t(kb >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(kb), 0u)));
+  if (lane == 0) scr_i[wave] = int32_t(__builtin_popcountll(kb));
+  __syncthreads();
+  int32_t count = 0, rank = below;
+#pragma unroll
+  for (int w = 0; w < GP / 64; ++w) {
+    const int32_t c = scr_i[w];
+    rank += w < wave ? c : 0;
+    count += c;
+  }
   if (t == 0) *S.count = count;
   if (t >= G) return;
   const float R = own_R;
