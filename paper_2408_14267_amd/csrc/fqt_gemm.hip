@@ -949,7 +949,43 @@ struct alignas(16) DxTileLds {
   int32_t wl[DXW_MAX_TAPS][CT * 32];
   int32_t pix_out[DXT_BP];
   float pix_s[DXT_BP], pix_z[DXT_BP];
+  // A wave's output tile, [channel row][pixel] (two channel tiles: full 32-channel tiles;
+  // one channel tile has C <= 32 and stores element by element).
+  uint32_t stage[CT == 2 ? DX_WAVES : 1][CT == 2 ? 32 * 32 : 1];
 };
+
+// Stores of one wave's 32 x 32 output tile (channels c0t .. c0t + 31 x the 32 pixels from
+// block pixel p0) from its row-major copy in LDS: lane L writes half h = L % 2 (16
+// pixels) of channel row L / 2, as 16-byte stores when those 16 pixels are live, in one
+// sample (consecutive offsets) and 16-byte aligned in dX; else element by element.
+template <typename T>
+__device__ __forceinline__ void dx_store_tile(const DxArgs &a, const int32_t *pix_out,
+                                              const T *stage, uint32_t c0t, uint32_t p0,
+                                              int lane) {
+  constexpr int PER16 = 16 / sizeof(T);            // elements per 16-byte store
+  static_assert(16 % PER16 == 0, "whole 16-byte pieces");
+  const int rr = lane >> 1, h = lane & 1;
+  const uint32_t cc = c0t + uint32_t(rr);
+  if (cc >= a.C) return;
+  const uint32_t pb = p0 + 16 * h;
+  const int o0 = pix_out[pb], o15 = pix_out[pb + 15];
+  const T *src = stage + rr * 32 + 16 * h;
+  T *dst = static_cast<T *>(a.dX);
+  const size_t base = size_t(o0) + size_t(cc) * a.HW;
+  // (o15 = o0 + 15 with both live: the 16 offsets are consecutive, also where a sample
+  // boundary falls inside, which only C = 1 allows.)
+  if (o0 >= 0 && o15 == o0 + 15 && (reinterpret_cast<uintptr_t>(dst + base) & 15) == 0) {
+    const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
+    uint4 *d4 = reinterpret_cast<uint4 *>(dst + base);
+#pragma unroll
+    for (int k = 0; k < 16 / PER16; ++k) d4[k] = s4[k];
+  } else {
+    for (int j = 0; j < 16; ++j) {
+      const int o = pix_out[pb + j];
+      if (o >= 0) dst[size_t(o) + size_t(cc) * a.HW] = src[j];
+    }
+  }
+}
 
 template <bool B8, int CT>
 __device__ __forceinline__ void dx_body_tiles(const DxArgs &a, uint32_t bid, DxTileLds<CT> &sm) {
@@ -1075,8 +1111,38 @@ __device__ __forceinline__ void dx_body_tiles(const DxArgs &a, uint32_t bid, DxT
         }
       }
       const int off = sm.pix_out[px[rt]];
-      if (off < 0) continue;               // rows past the count belong to the zero blocks
       const float S = sm.pix_s[px[rt]], Z = sm.pix_z[px[rt]];
+      if constexpr (CT == 2) {
+        if (!a.I_out && c0 + uint32_t(32 * ct + 32) <= a.C) {
+          // A whole tile of 32 channels goes through the wave's LDS copy (row-major), then
+          // out in 16-byte pieces along the pixels: 2-byte stores scattered over 32 channel
+          // rows were the slowest part of the kernel.
+          uint32_t *st = sm.stage[wave];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int row = acc_row(v, g);
+            int lt = 0;
+            if (B8)
+              for (int tap = 0; tap < taps; ++tap) lt += sm.wl[tap][32 * ct + row];
+            const float out = rescale(S, acc[rt][ct][v] + (B8 ? 128 * lt : 0), Z, cz[v]);
+            if (a.dx_t == FQT_BF16)
+              reinterpret_cast<uint16_t *>(st)[row * 32 + i] = f32_to_bf16(out);
+            else
+              reinterpret_cast<float *>(st)[row * 32 + i] = out;
+          }
+          __builtin_amdgcn_wave_barrier();    // LDS operations of a wave run in order
+          const uint32_t p0 = (wave * DXT_RT + uint32_t(rt)) * 32;
+          if (a.dx_t == FQT_BF16)
+            dx_store_tile<uint16_t>(a, sm.pix_out, reinterpret_cast<const uint16_t *>(st),
+                                    c0 + uint32_t(32 * ct), p0, lane);
+          else
+            dx_store_tile<float>(a, sm.pix_out, reinterpret_cast<const float *>(st),
+                                 c0 + uint32_t(32 * ct), p0, lane);
+          __builtin_amdgcn_wave_barrier();    // the next tile's copy waits for these reads
+          continue;
+        }
+      }
+      if (off < 0) continue;               // rows past the count belong to the zero blocks
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = 32 * ct + acc_row(v, g);

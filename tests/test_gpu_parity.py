@@ -92,6 +92,11 @@ CASES = [
     # 16384 dX tiles of 32 x 32: the dX product in its four-tiles-per-block form.
     ("conv_wide_dx_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2, 0,
      Recipe("channel_lognormal", sigma=1.0), "f32"),
+    # The same form on odd 297 x 297 maps with 40 channels: pixel tiles that straddle two
+    # samples, rows that are not 16-byte aligned and the partial second channel tile take
+    # the element-by-element stores, the rest the 16-byte ones.
+    ("conv_wide_dx_oddmap_b2", LayerShape("c", "conv2d", 3, 40, 8, 297, 297, 3, 3, 1, 1, 1, 1),
+     2, 0, Recipe("channel_lognormal", sigma=1.0), "f32"),
     # Large one-split dW outputs: the 2 x 2-tile dW form (ragged sizes, b = 8 bias).
     ("linear_bigdw_b2", LayerShape("fc", "linear", 64, 2048, 2048), 2, 0,
      Recipe("channel_lognormal", sigma=1.5), "f32"),
@@ -133,6 +138,8 @@ WORKLOAD_CASES = [
     # 16384 dX tiles with bf16 output: the dX product's four-tiles-per-block form in bf16.
     ("conv_wide_dx_bf16_b2", LayerShape("c", "conv2d", 4, 64, 8, 256, 256, 3, 3, 1, 1, 1, 1), 2,
      0, _CH15, "bf16"),
+    ("conv_wide_dx_oddmap_bf16_b4", LayerShape("c", "conv2d", 3, 64, 8, 297, 297, 3, 3, 1, 1, 1,
+                                                1), 4, 0, _CH15, "bf16"),
     # A point of the binary GEMM sweep as a layer (M = N = 1024, K = 2304 rows) at b = 4 with
     # Bernoulli AGP.
     ("gemm_sweep_1024x1024x2304_b4", LayerShape("g", "linear", 2304, 1024, 1024), 4, 0,
