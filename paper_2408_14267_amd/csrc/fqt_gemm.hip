@@ -1166,8 +1166,11 @@ __device__ __forceinline__ void dx_body_tiles(const DxArgs &a, uint32_t bid, DxT
 template <int WT>
 using DxLdsOf = std::conditional_t<WT != 0, DxTileLds<WT == 0 ? 1 : WT>, DxLds>;
 
+// The register-tile forms (WT != 0) are held to three waves per SIMD (at most 170
+// registers; the compiler's own choice, 182, leaves two).
 template <bool B8, int NB, int WT>
-__global__ __launch_bounds__(DX_THREADS) void k_mfma_dx(DxArgs a) {
+__global__ __launch_bounds__(DX_THREADS) __attribute__((amdgpu_waves_per_eu(WT != 0 ? 3 : 1)))
+void k_mfma_dx(DxArgs a) {
   __shared__ DxLdsOf<WT> sm;
   if constexpr (WT != 0) dx_body_tiles<B8, WT>(a, blockIdx.x, sm);
   else dx_body<B8, NB>(a, blockIdx.x, sm);
@@ -1186,7 +1189,8 @@ union ProductsLds {
   DwRedLds dw;
 };
 template <bool B8, int NB, int DWF, int WT>
-__global__ __launch_bounds__(DX_THREADS) void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
+__global__ __launch_bounds__(DX_THREADS) __attribute__((amdgpu_waves_per_eu(WT != 0 ? 3 : 1)))
+void k_products(DxArgs dxa, DwArgs dwa, uint32_t ndw) {
   __shared__ ProductsLds<WT> sm;
   if (blockIdx.x < ndw) {
     if constexpr (DWF == DWF_KRED) dw_kred_body<B8>(dwa, blockIdx.x, sm.dw);
