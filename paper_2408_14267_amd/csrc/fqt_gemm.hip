@@ -517,6 +517,56 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
     }
     return;
   }
+  // The 32 x 32 tiles go out through a row-major LDS copy per wave, each lane storing 16
+  // consecutive columns of one kept row in 16-byte pieces (the integer debug output takes
+  // the element stores below).
+  if constexpr (!SPLIT) {
+    if (!a.I_out) {
+      __shared__ float stage[DW_WAVES][32 * 32];
+      float *st = stage[wave];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int qrow = int(qsum[rt] + lane_xor<32>(qsum[rt])) + (B8 ? 128 * int(a.Rp) : 0);
+        int qv[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) qv[v] = __shfl(qrow, acc_row(v, g));
+        const uint32_t jt = j0 + 32 * rt;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          const int T = int(tcnt[ct]);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const uint32_t j = jt + uint32_t(acc_row(v, g));
+            float out = 0.0f;
+            if (int(j) < count) {
+              const float2 sz = a.slot_sz ? a.slot_sz[j]
+                                          : make_float2(a.scale[a.kept[j]], a.offset[a.kept[j]]);
+              const int I = 2 * (acc[rt][ct][v] + (B8 ? 128 * T : 0)) - qv[v];
+              out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
+            }
+            st[acc_row(v, g) * 32 + i] = out;
+          }
+          __builtin_amdgcn_wave_barrier();    // LDS operations of a wave run in order
+          const uint32_t j = jt + uint32_t(lane >> 1);
+          const uint32_t c0 = k0 + 32 * ct + 16 * uint32_t(lane & 1);
+          if (j < a.D && c0 < a.K) {
+            const float *src = st + (lane >> 1) * 32 + 16 * (lane & 1);
+            float *dst = a.dW + size_t(a.kept[j]) * a.K + c0;
+            if (c0 + 16 <= a.K && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+              const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
+              uint4 *d4 = reinterpret_cast<uint4 *>(dst);
+#pragma unroll
+              for (int k = 0; k < 4; ++k) d4[k] = s4[k];
+            } else {
+              for (uint32_t e = 0; e < 16 && c0 + e < a.K; ++e) dst[e] = src[e];
+            }
+          }
+          __builtin_amdgcn_wave_barrier();    // the next tile's copy waits for these reads
+        }
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     // Sum of the codes of row i of the tile (b = 8: of q - 128 over all Rp positions).
