@@ -60,91 +60,12 @@ __global__ __launch_bounds__(THREADS) void k_pack_along_rows(const void *__restr
   }
 }
 
-struct Im2colGeom {
-  uint32_t C, H, W, Wo, P, R, nw, cgroups;
-  int kh, kw, sh, sw, ph, pw;
-  FastDiv divP, divWo, divNw;
-};
-
-constexpr int IM2COL_CPW = 4;   // channels per wave sharing one index decomposition
-
-// Bit-im2col: line (c, i, j), bit (n, ho, wo) = X[n][c][ho*sh - ph + i][wo*sw - pw + j] > 0;
-// positions in the zero padding give bit 0 (sign -1).  One wave owns 64 consecutive
-// (n, ho, wo) of IM2COL_CPW channels: one index decomposition per lane serves every
-// channel and kernel tap.  The words of a channel's taps are gathered into lanes
-// 0..taps-1 and stored by one instruction.  KH, KW > 0 fix the kernel size at compile
-// time (fully unrolled); 0 reads it from the geometry.  WM: word-major output, word w of
-// line l at w * C*kh*kw + l (the layout the dW product reads).
+// Bit-im2col, one wave per 64 positions of IM2COL_CPW channels (the body is shared with the
+// layer backward's selection launch).
 template <int DT, int KH, int KW, bool WM>
 __global__ __launch_bounds__(THREADS) void k_pack_im2col(const void *__restrict__ x, Im2colGeom g,
                                                          uint64_t *__restrict__ dst) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t item = blockIdx.x * WAVES + (threadIdx.x >> 6);
-  if (item >= g.cgroups * g.nw) return;
-  const uint32_t cg = fdiv(item, g.divNw), w = item - cg * g.nw;
-  const uint32_t r0 = (w << 6) + lane;
-  const bool valid = r0 < g.R;
-  const uint32_t r = valid ? r0 : 0;
-  const uint32_t n = fdiv(r, g.divP), pix = r - n * g.P;
-  const uint32_t ho = fdiv(pix, g.divWo), wo = pix - ho * g.Wo;
-  const int h0 = int(ho) * g.sh - g.ph, w0 = int(wo) * g.sw - g.pw;
-  const int kh = KH > 0 ? KH : g.kh, kw = KW > 0 ? KW : g.kw;
-  const int taps = kh * kw;
-  uint32_t hok = 0, wok = 0;
-  for (int i = 0; i < kh; ++i) hok |= uint32_t(valid && h0 + i >= 0 && h0 + i < int(g.H)) << i;
-  for (int j = 0; j < kw; ++j) wok |= uint32_t(w0 + j >= 0 && w0 + j < int(g.W)) << j;
-  const int plane = int(g.H * g.W);
-  int base = (int(n * g.C + cg * IM2COL_CPW) * int(g.H) + h0) * int(g.W) + w0;
-  for (int cc = 0; cc < IM2COL_CPW; ++cc, base += plane) {
-    const uint32_t c = cg * IM2COL_CPW + cc;
-    if (c >= g.C) break;
-    uint64_t mine = 0;
-    if constexpr (KH > 0) {
-      float v[KH * KW];
-#pragma unroll
-      for (int i = 0; i < KH; ++i)
-#pragma unroll
-        for (int j = 0; j < KW; ++j) {
-          const bool ok = (hok >> i) & (wok >> j) & 1u;
-          v[i * KW + j] = load_elem<DT>(x, ok ? base + i * int(g.W) + j : 0);
-        }
-#pragma unroll
-      for (int i = 0; i < KH; ++i)
-#pragma unroll
-        for (int j = 0; j < KW; ++j) {
-          const bool ok = (hok >> i) & (wok >> j) & 1u;
-          const uint64_t m = __ballot(ok && v[i * KW + j] > 0.0f);
-          if (lane == i * KW + j) mine = m;
-        }
-      if (lane < KH * KW)
-        dst[WM ? size_t(w) * g.C * (KH * KW) + size_t(c) * (KH * KW) + lane
-               : (size_t(c) * (KH * KW) + lane) * g.nw + w] = mine;
-    } else {
-      for (int t0 = 0; t0 < taps; t0 += 16) {
-        int ti = t0 / kw, tj = t0 - ti * kw;
-        float v[16];
-        uint32_t okm = 0;
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const bool ok = t0 + u < taps && ((hok >> ti) & (wok >> tj) & 1u);
-          okm |= uint32_t(ok) << u;
-          v[u] = load_elem<DT>(x, ok ? base + ti * int(g.W) + tj : 0);
-          if (++tj == kw) {
-            tj = 0;
-            ++ti;
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const uint64_t m = __ballot(((okm >> u) & 1u) && v[u] > 0.0f);
-          if (lane == u) mine = m;
-        }
-        if (lane < 16 && t0 + lane < taps)
-          dst[WM ? size_t(w) * g.C * taps + size_t(c) * taps + t0 + lane
-                 : (size_t(c) * taps + t0 + lane) * g.nw + w] = mine;
-      }
-    }
-  }
+  wave_im2col_body<DT, KH, KW, WM>(x, g, dst, blockIdx.x * WAVES + (threadIdx.x >> 6));
 }
 
 // Bit-im2col through an LDS band of sign bytes (the body is shared with the layer
@@ -306,11 +227,8 @@ int launch_pack_bits(const void *src, int dtype, int64_t rows, int64_t cols, int
     });
   } else {
     const Layer &L = *conv;
-    const uint32_t cgroups = uint32_t((L.C + IM2COL_CPW - 1) / IM2COL_CPW);
-    Im2colGeom g{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
-                 uint32_t(L.R), uint32_t(L.Wr), cgroups, L.kh, L.kw, L.sh, L.sw, L.ph, L.pw,
-                 make_fastdiv(uint32_t(L.P)), make_fastdiv(uint32_t(L.Wo)),
-                 make_fastdiv(uint32_t(L.Wr))};
+    const Im2colGeom g = im2col_geom(L);
+    const uint32_t cgroups = g.cgroups;
     nw = L.Wr;
     lines = L.K;
     len = L.R;

@@ -1148,12 +1148,15 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
 
 // The same two selection workgroups, then spare workgroups that pack the products' sign
 // operands (they do not depend on dY): blocks [2, 2 + npw) the weight bytes, the rest the
-// im2col of X: bit-level (KH < 0; block order of bit_im2col_body) or through the band
-// (word group fastest, then 64-channel groups).
+// im2col of X, in one of three forms: bit-level (block order of bit_im2col_body), through
+// the band (word group fastest, then 64-channel groups), or a wave per 64 positions of
+// IM2COL_CPW channels (any convolution; work items in wave order).
+enum SignForm { SIGN_BITS = 0, SIGN_BAND = 1, SIGN_WAVE = 2 };
 struct SignArgs {
   const void *x;
   BandGeom bg;
   BitGeom bt;
+  Im2colGeom ig;
   uint64_t *xsign;
   uint32_t nwb;          // word-group blocks of the band (samples x word groups)
   FastDiv divNwb;
@@ -1163,8 +1166,9 @@ struct SignArgs {
   int32_t *wlsum;
   uint32_t npw;
 };
-// DT: dtype of X; WDT: dtype of W.
-template <int GP, int DT, int KH, int KW, int WDT = DT>
+// DT: dtype of X; WDT: dtype of W; KH, KW: the kernel size of the band and wave forms
+// (0: read from the geometry).
+template <int GP, int DT, int FORM, int KH, int KW, int WDT = DT>
 __global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) void k_select_signs(
     SelectArgs a, SignArgs sg) {
   extern __shared__ uint32_t band[];
@@ -1174,13 +1178,16 @@ __global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) voi
     select_fused_body<GP>(a, int(b));
   } else if (b - 2 < sg.npw) {
     pack_w_body<WDT>(sg.w, sg.pg, sg.wsb, sg.wlsum, b - 2, pws);
-  } else if constexpr (KH < 0) {
+  } else if constexpr (FORM == SIGN_BITS) {
     bit_im2col_body<DT, SEL_NT>(sg.x, sg.bt, sg.xsign, b - 2 - sg.npw,
                                 reinterpret_cast<uint64_t *>(band));
-  } else {
+  } else if constexpr (FORM == SIGN_BAND) {
     const uint32_t f = b - 2 - sg.npw;
     const uint32_t cb = fdiv(f, sg.divNwb);
     band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.nwb, cb, band);
+  } else {
+    wave_im2col_body<DT, KH, KW, true>(sg.x, sg.ig, sg.xsign,
+                                       (b - 2 - sg.npw) * SEL_NW + (threadIdx.x >> 6));
   }
 }
 // Static LDS of k_select_signs<GP>: the selection's arrays and the weight-byte tile.
@@ -1534,11 +1541,11 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     sa.set[0].slots = 2;          // the selection reads the reduced keys
     sa.set[1].slots = 2;
   }
-  // Sign operands in the selection launch: a convolution whose X and W share a dtype and
-  // whose im2col staging fits the LDS left beside the selection (64 KB per workgroup in
-  // all): bit-level for stride-1 same-padded convolutions (at most about 448 im2col
-  // workgroups: with two 1024-thread workgroups per CU the launch fits the chip in one
-  // round), else through the band.
+  // Sign operands in the selection launch, for convolutions: bit-level for stride-1
+  // same-padded convolutions whose staging fits the LDS left beside the selection (64 KB per
+  // workgroup in all; at most about 448 im2col workgroups: with two 1024-thread workgroups
+  // per CU the launch fits the chip in one round), else through the band where X and W share
+  // a dtype and its staging fits, else a wave per 64 positions.
   BitGeom bt;
   BandGeom bg;
   size_t sign_lds = 0;
@@ -1548,7 +1555,8 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   const bool with_bits = sign_ok && bit_geom(L, SEL_NT, 448, lds_left, &bt, &sign_lds);
   const bool with_band = sign_ok && !with_bits && L.x_t == L.w_t &&
                          band_geom(L, signs->X, L.x_t, SEL_NT, lds_left, &bg, &sign_lds);
-  if (with_bits || with_band) {
+  const bool with_wave = sign_ok && !with_bits && !with_band && L.kind == FQT_CONV2D;
+  if (with_bits || with_band || with_wave) {
     SignArgs sg;
     sg.x = signs->X; sg.xsign = signs->xsign;
     sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
@@ -1558,6 +1566,9 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
       bit_geom_vec(&bt, signs->X);
       sg.bt = bt;
       xblocks = bit_blocks(bt);
+    } else if (with_wave) {
+      sg.ig = im2col_geom(L);
+      xblocks = uint32_t((int64_t(sg.ig.cgroups) * sg.ig.nw + SEL_NW - 1) / SEL_NW);
     } else {
       sg.bg = bg;
       sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);
@@ -1566,23 +1577,27 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     const dim3 grid(2 + sg.npw + xblocks);
     dispatch_dtype(L.x_t, [&]<int DT>() {
       auto go = [&]<int GPT>() {
-        if (with_bits && L.w_t != DT)
-          dispatch_dtype(L.w_t, [&]<int WDT>() {
-            hipLaunchKernelGGL((k_select_signs<GPT, DT, -1, -1, WDT>), grid, dim3(SEL_NT),
-                               sign_lds, s, sa, sg);
-          });
-        else if (with_bits)
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, -1, -1>), grid, dim3(SEL_NT), sign_lds, s,
-                             sa, sg);
-        else if (L.kh == 3 && L.kw == 3)
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 3, 3>), grid, dim3(SEL_NT), sign_lds, s,
-                             sa, sg);
-        else if (L.kh == 1 && L.kw == 1)
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 1, 1>), grid, dim3(SEL_NT), sign_lds, s,
-                             sa, sg);
-        else
-          hipLaunchKernelGGL((k_select_signs<GPT, DT, 0, 0>), grid, dim3(SEL_NT), sign_lds, s,
-                             sa, sg);
+        // The band form needs X and W of one dtype; the others take W's dtype apart.
+        auto launch = [&]<int FORM, int KH, int KW>() {
+          if constexpr (FORM != SIGN_BAND) {
+            if (L.w_t != DT) {
+              dispatch_dtype(L.w_t, [&]<int WDT>() {
+                hipLaunchKernelGGL((k_select_signs<GPT, DT, FORM, KH, KW, WDT>), grid,
+                                   dim3(SEL_NT), sign_lds, s, sa, sg);
+              });
+              return;
+            }
+          }
+          hipLaunchKernelGGL((k_select_signs<GPT, DT, FORM, KH, KW>), grid, dim3(SEL_NT),
+                             sign_lds, s, sa, sg);
+        };
+        if (with_bits) launch.template operator()<SIGN_BITS, 0, 0>();
+        else if (with_band && L.kh == 3 && L.kw == 3) launch.template operator()<SIGN_BAND, 3, 3>();
+        else if (with_band && L.kh == 1 && L.kw == 1) launch.template operator()<SIGN_BAND, 1, 1>();
+        else if (with_band) launch.template operator()<SIGN_BAND, 0, 0>();
+        else if (L.kh == 3 && L.kw == 3) launch.template operator()<SIGN_WAVE, 3, 3>();
+        else if (L.kh == 1 && L.kw == 1) launch.template operator()<SIGN_WAVE, 1, 1>();
+        else launch.template operator()<SIGN_WAVE, 0, 0>();
       };
       if (gp == 256) go.template operator()<256>();
       else go.template operator()<1024>();

@@ -1,7 +1,6 @@
-// Device bodies of the two sign packers that feed the MFMA products (Section 5.1
-// binarizer; Appendix C, Alg. 2 encoders, the Unfolder and the {0,1} <-> {+-1}
-// conversion):
-//   band im2col   sign(unfold(X)) as word-major bits, the dW operand;
+// Device bodies of the sign packers that feed the MFMA products (Section 5.1 binarizer;
+// Appendix C, Alg. 2 encoders, the Unfolder and the {0,1} <-> {+-1} conversion):
+//   band, bit-level and wave im2col   sign(unfold(X)) as word-major bits, the dW operand;
 //   weight bytes  sign(W) as +-1 bytes with per-line sums, the dX operand.
 // fqt_pack.hip launches them on their own; the layer backward runs them in spare blocks
 // of the AGP selection launch, whose two selection workgroups leave the chip idle.
@@ -55,7 +54,7 @@ inline bool band_geom(const Layer &L, const void *x, int dtype, int nt, size_t l
     const int64_t orows = (64 * wpb - 1 + L.Wo - 1) / L.Wo + 1;
     const int64_t BR = (orows - 1) * L.sh + L.kh;
     const int64_t plane = BR * WL;
-    const size_t bytes = size_t(plane * chans);
+    const size_t bytes = size_t(plane * std::min<int64_t>(chans, L.C));   // channels staged
     if (bytes > lds_max) continue;
     const int64_t wgroups = (wps + wpb - 1) / wpb;
     *bg = BandGeom{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
@@ -396,6 +395,101 @@ __device__ __forceinline__ void bit_im2col_body(const void *__restrict__ x, cons
     uint64_t v = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
     v &= rowm[j * g.kh + i] & colm[j * g.kw + jj];
     dst[size_t(w0 + j) * g.K + size_t(c0) * g.taps + ll] = v;
+  }
+}
+
+// ----------------------------------------------------------------------------- wave im2col
+struct Im2colGeom {
+  uint32_t C, H, W, Wo, P, R, nw, cgroups;
+  int kh, kw, sh, sw, ph, pw;
+  FastDiv divP, divWo, divNw;
+};
+
+constexpr int IM2COL_CPW = 4;   // channels per wave sharing one index decomposition
+inline Im2colGeom im2col_geom(const Layer &L) {
+  return Im2colGeom{uint32_t(L.C), uint32_t(L.H), uint32_t(L.W), uint32_t(L.Wo), uint32_t(L.P),
+                    uint32_t(L.R), uint32_t(L.Wr), uint32_t((L.C + IM2COL_CPW - 1) / IM2COL_CPW),
+                    L.kh, L.kw, L.sh, L.sw, L.ph, L.pw, make_fastdiv(uint32_t(L.P)),
+                    make_fastdiv(uint32_t(L.Wo)), make_fastdiv(uint32_t(L.Wr))};
+}
+
+
+// Bit-im2col: line (c, i, j), bit (n, ho, wo) = X[n][c][ho*sh - ph + i][wo*sw - pw + j] > 0;
+// positions in the zero padding give bit 0 (sign -1).  One wave owns 64 consecutive
+// (n, ho, wo) of IM2COL_CPW channels (work item `item` = channel group * nw + word): one
+// index decomposition per lane serves every
+// channel and kernel tap.  The words of a channel's taps are gathered into lanes
+// 0..taps-1 and stored by one instruction.  KH, KW > 0 fix the kernel size at compile
+// time (fully unrolled); 0 reads it from the geometry.  WM: word-major output, word w of
+// line l at w * C*kh*kw + l (the layout the dW product reads).
+template <int DT, int KH, int KW, bool WM>
+__device__ __forceinline__ void wave_im2col_body(const void *__restrict__ x, const Im2colGeom &g,
+                                                 uint64_t *__restrict__ dst, uint32_t item) {
+  const int lane = threadIdx.x & 63;
+  if (item >= g.cgroups * g.nw) return;
+  const uint32_t cg = fdiv(item, g.divNw), w = item - cg * g.nw;
+  const uint32_t r0 = (w << 6) + lane;
+  const bool valid = r0 < g.R;
+  const uint32_t r = valid ? r0 : 0;
+  const uint32_t n = fdiv(r, g.divP), pix = r - n * g.P;
+  const uint32_t ho = fdiv(pix, g.divWo), wo = pix - ho * g.Wo;
+  const int h0 = int(ho) * g.sh - g.ph, w0 = int(wo) * g.sw - g.pw;
+  const int kh = KH > 0 ? KH : g.kh, kw = KW > 0 ? KW : g.kw;
+  const int taps = kh * kw;
+  uint32_t hok = 0, wok = 0;
+  for (int i = 0; i < kh; ++i) hok |= uint32_t(valid && h0 + i >= 0 && h0 + i < int(g.H)) << i;
+  for (int j = 0; j < kw; ++j) wok |= uint32_t(w0 + j >= 0 && w0 + j < int(g.W)) << j;
+  const int plane = int(g.H * g.W);
+  int base = (int(n * g.C + cg * IM2COL_CPW) * int(g.H) + h0) * int(g.W) + w0;
+  for (int cc = 0; cc < IM2COL_CPW; ++cc, base += plane) {
+    const uint32_t c = cg * IM2COL_CPW + cc;
+    if (c >= g.C) break;
+    uint64_t mine = 0;
+    if constexpr (KH > 0) {
+      float v[KH * KW];
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int j = 0; j < KW; ++j) {
+          const bool ok = (hok >> i) & (wok >> j) & 1u;
+          v[i * KW + j] = load_elem<DT>(x, ok ? base + i * int(g.W) + j : 0);
+        }
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int j = 0; j < KW; ++j) {
+          const bool ok = (hok >> i) & (wok >> j) & 1u;
+          const uint64_t m = __ballot(ok && v[i * KW + j] > 0.0f);
+          if (lane == i * KW + j) mine = m;
+        }
+      if (lane < KH * KW)
+        dst[WM ? size_t(w) * g.C * (KH * KW) + size_t(c) * (KH * KW) + lane
+               : (size_t(c) * (KH * KW) + lane) * g.nw + w] = mine;
+    } else {
+      for (int t0 = 0; t0 < taps; t0 += 16) {
+        int ti = t0 / kw, tj = t0 - ti * kw;
+        float v[16];
+        uint32_t okm = 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const bool ok = t0 + u < taps && ((hok >> ti) & (wok >> tj) & 1u);
+          okm |= uint32_t(ok) << u;
+          v[u] = load_elem<DT>(x, ok ? base + ti * int(g.W) + tj : 0);
+          if (++tj == kw) {
+            tj = 0;
+            ++ti;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const uint64_t m = __ballot(((okm >> u) & 1u) && v[u] > 0.0f);
+          if (lane == u) mine = m;
+        }
+        if (lane < 16 && t0 + lane < taps)
+          dst[WM ? size_t(w) * g.C * taps + size_t(c) * taps + t0 + lane
+                 : (size_t(c) * taps + t0 + lane) * g.nw + w] = mine;
+      }
+    }
   }
 }
 
