@@ -1150,8 +1150,9 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
 // operands (they do not depend on dY): blocks [2, 2 + npw) the weight bytes, the rest the
 // im2col of X, in one of three forms: bit-level (block order of bit_im2col_body), through
 // the band (word group fastest, then 64-channel groups), or a wave per 64 positions of
-// IM2COL_CPW channels (any convolution; work items in wave order).
-enum SignForm { SIGN_BITS = 0, SIGN_BAND = 1, SIGN_WAVE = 2 };
+// IM2COL_CPW channels (any convolution; work items in wave order); for a linear layer the
+// sign words of X down its rows (a wave per work item of rows_wave_body).
+enum SignForm { SIGN_BITS = 0, SIGN_BAND = 1, SIGN_WAVE = 2, SIGN_ROWS = 3 };
 struct SignArgs {
   const void *x;
   BandGeom bg;
@@ -1185,9 +1186,12 @@ __global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) voi
     const uint32_t f = b - 2 - sg.npw;
     const uint32_t cb = fdiv(f, sg.divNwb);
     band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.nwb, cb, band);
-  } else {
+  } else if constexpr (FORM == SIGN_WAVE) {
     wave_im2col_body<DT, KH, KW, true>(sg.x, sg.ig, sg.xsign,
                                        (b - 2 - sg.npw) * SEL_NW + (threadIdx.x >> 6));
+  } else {
+    rows_wave_body<DT>(sg.x, sg.ig.R, sg.ig.C, sg.xsign,
+                       (b - 2 - sg.npw) * SEL_NW + (threadIdx.x >> 6));
   }
 }
 // Static LDS of k_select_signs<GP>: the selection's arrays and the weight-byte tile.
@@ -1541,11 +1545,12 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     sa.set[0].slots = 2;          // the selection reads the reduced keys
     sa.set[1].slots = 2;
   }
-  // Sign operands in the selection launch, for convolutions: bit-level for stride-1
+  // Sign operands in the selection launch.  Convolutions: bit-level for stride-1
   // same-padded convolutions whose staging fits the LDS left beside the selection (64 KB per
   // workgroup in all; at most about 448 im2col workgroups: with two 1024-thread workgroups
   // per CU the launch fits the chip in one round), else through the band where X and W share
-  // a dtype and its staging fits, else a wave per 64 positions.
+  // a dtype and its staging fits, else a wave per 64 positions.  Linear layers: the rows
+  // form.
   BitGeom bt;
   BandGeom bg;
   size_t sign_lds = 0;
@@ -1556,7 +1561,8 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   const bool with_band = sign_ok && !with_bits && L.x_t == L.w_t &&
                          band_geom(L, signs->X, L.x_t, SEL_NT, lds_left, &bg, &sign_lds);
   const bool with_wave = sign_ok && !with_bits && !with_band && L.kind == FQT_CONV2D;
-  if (with_bits || with_band || with_wave) {
+  const bool with_rows = sign_ok && L.kind == FQT_LINEAR;
+  if (with_bits || with_band || with_wave || with_rows) {
     SignArgs sg;
     sg.x = signs->X; sg.xsign = signs->xsign;
     sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
@@ -1569,6 +1575,12 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
     } else if (with_wave) {
       sg.ig = im2col_geom(L);
       xblocks = uint32_t((int64_t(sg.ig.cgroups) * sg.ig.nw + SEL_NW - 1) / SEL_NW);
+    } else if (with_rows) {
+      sg.ig = Im2colGeom{};
+      sg.ig.R = uint32_t(L.N);       // rows of X
+      sg.ig.C = uint32_t(L.C);       // columns of X
+      const int64_t items = ((L.N + 63) / 64) * ((L.C + 15) / 16);
+      xblocks = uint32_t((items + SEL_NW - 1) / SEL_NW);
     } else {
       sg.bg = bg;
       sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);
@@ -1591,7 +1603,8 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
           hipLaunchKernelGGL((k_select_signs<GPT, DT, FORM, KH, KW>), grid, dim3(SEL_NT),
                              sign_lds, s, sa, sg);
         };
-        if (with_bits) launch.template operator()<SIGN_BITS, 0, 0>();
+        if (with_rows) launch.template operator()<SIGN_ROWS, 0, 0>();
+        else if (with_bits) launch.template operator()<SIGN_BITS, 0, 0>();
         else if (with_band && L.kh == 3 && L.kw == 3) launch.template operator()<SIGN_BAND, 3, 3>();
         else if (with_band && L.kh == 1 && L.kw == 1) launch.template operator()<SIGN_BAND, 1, 1>();
         else if (with_band) launch.template operator()<SIGN_BAND, 0, 0>();

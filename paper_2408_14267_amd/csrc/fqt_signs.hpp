@@ -1,6 +1,7 @@
 // Device bodies of the sign packers that feed the MFMA products (Section 5.1 binarizer;
 // Appendix C, Alg. 2 encoders, the Unfolder and the {0,1} <-> {+-1} conversion):
-//   band, bit-level and wave im2col   sign(unfold(X)) as word-major bits, the dW operand;
+//   band, bit-level and wave im2col   sign(unfold(X)) as word-major bits, the dW operand
+//                 (rows: the same for a linear layer's X);
 //   weight bytes  sign(W) as +-1 bytes with per-line sums, the dX operand.
 // fqt_pack.hip launches them on their own; the layer backward runs them in spare blocks
 // of the AGP selection launch, whose two selection workgroups leave the chip idle.
@@ -491,6 +492,39 @@ __device__ __forceinline__ void wave_im2col_body(const void *__restrict__ x, con
       }
     }
   }
+}
+
+// ----------------------------------------------------------------------------- rows
+// sign(X) of a linear layer's input X[N][C] down the rows, word-major: bit l of word w of
+// column c is X[64 w + l][c] > 0, at dst[w * C + c] (the layout the dW product reads).  One
+// wave per work item (word w, 16 columns c0 .. c0 + 15; column groups fastest): lane l
+// loads its row's 16 elements back to back and one ballot per column gives that column's
+// word, kept by lane k for column c0 + k.
+__device__ __forceinline__ uint32_t rows_items(uint32_t N, uint32_t C) {
+  return ((N + 63) / 64) * ((C + 15) / 16);
+}
+template <int DT>
+__device__ __forceinline__ void rows_wave_body(const void *__restrict__ x, uint32_t N, uint32_t C,
+                                               uint64_t *__restrict__ dst, uint32_t item) {
+  const int lane = threadIdx.x & 63;
+  const uint32_t ncg = (C + 15) / 16;
+  if (item >= rows_items(N, C)) return;
+  const uint32_t w = item / ncg, c0 = (item - w * ncg) * 16;
+  const uint32_t r = w * 64 + uint32_t(lane);
+  const bool rin = r < N;
+  float v[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {   // element 0 outside X, so the loads issue back to back
+    const uint32_t c = c0 + k;
+    v[k] = load_elem<DT>(x, (rin && c < C) ? int64_t(r) * C + c : 0);
+  }
+  uint64_t mine = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const uint64_t m = __ballot(rin && c0 + k < C && v[k] > 0.0f);
+    if (lane == k) mine = m;
+  }
+  if (lane < 16 && c0 + uint32_t(lane) < C) dst[size_t(w) * C + c0 + lane] = mine;
 }
 
 // ----------------------------------------------------------------------------- weight bytes
