@@ -1153,6 +1153,7 @@ __global__ __launch_bounds__(SEL_NT) void k_select_fused(SelectArgs a) {
 // IM2COL_CPW channels (any convolution; work items in wave order); for a linear layer the
 // sign words of X down its rows (a wave per work item of rows_wave_body).
 enum SignForm { SIGN_BITS = 0, SIGN_BAND = 1, SIGN_WAVE = 2, SIGN_ROWS = 3 };
+constexpr uint32_t SIGN_IPB = 4;     // work items per workgroup of the wave and rows forms
 struct SignArgs {
   const void *x;
   BandGeom bg;
@@ -1166,6 +1167,7 @@ struct SignArgs {
   int8_t *wsb;
   int32_t *wlsum;
   uint32_t npw;
+  uint32_t ipb;          // work items per workgroup of the wave and rows forms (waves past it idle)
 };
 // DT: dtype of X; WDT: dtype of W; KH, KW: the kernel size of the band and wave forms
 // (0: read from the geometry).
@@ -1186,12 +1188,14 @@ __global__ __launch_bounds__(SEL_NT) __attribute__((amdgpu_waves_per_eu(8))) voi
     const uint32_t f = b - 2 - sg.npw;
     const uint32_t cb = fdiv(f, sg.divNwb);
     band_im2col_body<DT, KH, KW, SEL_NT>(sg.x, sg.bg, sg.xsign, f - cb * sg.nwb, cb, band);
-  } else if constexpr (FORM == SIGN_WAVE) {
-    wave_im2col_body<DT, KH, KW, true>(sg.x, sg.ig, sg.xsign,
-                                       (b - 2 - sg.npw) * SEL_NW + (threadIdx.x >> 6));
   } else {
-    rows_wave_body<DT>(sg.x, sg.ig.R, sg.ig.C, sg.xsign,
-                       (b - 2 - sg.npw) * SEL_NW + (threadIdx.x >> 6));
+    // Work items spread over workgroups: a CU's address unit, not the memory latency, bounds
+    // these gathers when one workgroup takes sixteen waves of them.
+    const uint32_t wave = threadIdx.x >> 6;
+    if (wave >= sg.ipb) return;
+    const uint32_t item = (b - 2 - sg.npw) * sg.ipb + wave;
+    if constexpr (FORM == SIGN_WAVE) wave_im2col_body<DT, KH, KW, true>(sg.x, sg.ig, sg.xsign, item);
+    else rows_wave_body<DT>(sg.x, sg.ig.R, sg.ig.C, sg.xsign, item);
   }
 }
 // Static LDS of k_select_signs<GP>: the selection's arrays and the weight-byte tile.
@@ -1563,7 +1567,7 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
   const bool with_wave = sign_ok && !with_bits && !with_band && L.kind == FQT_CONV2D;
   const bool with_rows = sign_ok && L.kind == FQT_LINEAR;
   if (with_bits || with_band || with_wave || with_rows) {
-    SignArgs sg;
+    SignArgs sg{};
     sg.x = signs->X; sg.xsign = signs->xsign;
     sg.w = signs->W; sg.pg = pack_w_geom(L); sg.wsb = signs->wsb; sg.wlsum = signs->wlsum;
     sg.npw = pack_w_blocks(L);
@@ -1574,13 +1578,15 @@ int launch_quantize(const Layer &L, const fqt_quant_cfg &cfg, const void *dY, co
       xblocks = bit_blocks(bt);
     } else if (with_wave) {
       sg.ig = im2col_geom(L);
-      xblocks = uint32_t((int64_t(sg.ig.cgroups) * sg.ig.nw + SEL_NW - 1) / SEL_NW);
+      sg.ipb = SIGN_IPB;
+      xblocks = uint32_t((int64_t(sg.ig.cgroups) * sg.ig.nw + SIGN_IPB - 1) / SIGN_IPB);
     } else if (with_rows) {
       sg.ig = Im2colGeom{};
       sg.ig.R = uint32_t(L.N);       // rows of X
       sg.ig.C = uint32_t(L.C);       // columns of X
+      sg.ipb = SIGN_IPB;
       const int64_t items = ((L.N + 63) / 64) * ((L.C + 15) / 16);
-      xblocks = uint32_t((items + SEL_NW - 1) / SEL_NW);
+      xblocks = uint32_t((items + SIGN_IPB - 1) / SIGN_IPB);
     } else {
       sg.bg = bg;
       sg.nwb = band_word_blocks(L, bg); sg.divNwb = make_fastdiv(sg.nwb);

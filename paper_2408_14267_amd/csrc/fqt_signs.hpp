@@ -125,8 +125,12 @@ __device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, con
   __syncthreads();
 
   const uint8_t *bb = reinterpret_cast<const uint8_t *>(band);
+  // KH > 0: BAND_CPW channels per wave.  KH = 0: the block's nch * taps lines split evenly
+  // over the waves, so that a block of few channels (a 3-channel stem) keeps every wave busy.
+  const uint32_t nl = nch * g.taps, lpw = (nl + NW - 1) / NW;
   const uint32_t cl_lo = wave * BAND_CPW, cl_hi = min(nch, cl_lo + BAND_CPW);
-  if (cl_hi <= cl_lo) return;
+  const uint32_t l_lo = min(nl, wave * lpw), l_hi = min(nl, l_lo + lpw);
+  if (KH > 0 ? cl_hi <= cl_lo : l_hi <= l_lo) return;
   for (uint32_t j = 0; j < nwords; ++j) {
     // This lane's output position in word j and its band byte offset for tap (0, 0).
     const uint32_t p = p0 + 64 * j + lane;
@@ -155,16 +159,22 @@ __device__ __forceinline__ void band_im2col_body(const void *__restrict__ x, con
 #pragma unroll
         for (int tap = 0; tap < KH * KW; ++tap)
           put(__ballot(b[tap] != 0), (c0 + cl) * (KH * KW) + tap);
-      } else {
-        for (uint32_t tap = 0; tap < g.taps; ++tap) {
-          const uint32_t i = fdiv(tap, g.divKw), jj = tap - i * g.kw;
-          put(__ballot(pl[i * g.WL + jj] != 0), (c0 + cl) * g.taps + tap);
+      }
+    }
+    if constexpr (KH == 0) {
+      uint32_t cl = l_lo / g.taps, tap = l_lo - cl * g.taps;
+      for (uint32_t l = l_lo; l < l_hi; ++l) {
+        const uint32_t i = fdiv(tap, g.divKw), jj = tap - i * g.kw;
+        put(__ballot(bb[cl * g.plane + base + i * g.WL + jj] != 0), c0 * g.taps + l);
+        if (++tap == g.taps) {
+          tap = 0;
+          ++cl;
         }
       }
     }
     if (filled > 0) {
       // The words left end at the wave's last line.
-      const uint32_t l_end = (c0 + cl_hi) * g.taps;
+      const uint32_t l_end = KH > 0 ? (c0 + cl_hi) * g.taps : c0 * g.taps + l_hi;
       if (lane < filled) out[l_end - filled + lane] = (uint64_t(mhi) << 32) | mlo;
     }
   }
