@@ -18,6 +18,7 @@
 // A tile holds whole 64-bit words of both packings: a PSQ word runs along the 64
 // channels of one row r, a PCQ word along the 64 rows of one channel.
 #include <climits>
+#include <type_traits>
 
 #include "fqt_internal.hpp"
 #include "fqt_signs.hpp"
@@ -205,6 +206,28 @@ __global__ __launch_bounds__(THREADS) void k_stats(const void *__restrict__ dy, 
         } else if (row_ok) {
           part_s[size_t(r0 + lane) * sg.ndt + byc] = make_int2(lo, hi);
         }
+      } else if (mks && (TILE % g.P) == 0) {
+        // P divides 64: every sample of the tile is an aligned group of P lanes.  A
+        // butterfly within the groups leaves each group's key in all of its lanes, and the
+        // first lane of each group merges it (one atomic instruction for all the samples).
+        if (!row_ok) {
+          lo = INT_MAX;
+          hi = INT_MIN;
+        }
+        auto fold = [&](auto m) {
+          constexpr int M = decltype(m)::value;
+          lo = min(lo, int(lane_xor<M>(uint32_t(lo))));
+          hi = max(hi, int(lane_xor<M>(uint32_t(hi))));
+        };
+        if (g.P > 1) fold(std::integral_constant<int, 1>());
+        if (g.P > 2) fold(std::integral_constant<int, 2>());
+        if (g.P > 4) fold(std::integral_constant<int, 4>());
+        if (g.P > 8) fold(std::integral_constant<int, 8>());
+        if (g.P > 16) fold(std::integral_constant<int, 16>());
+        if (g.P > 32) fold(std::integral_constant<int, 32>());
+        if (row_ok && (uint32_t(lane) & (g.P - 1)) == 0)
+          merge_key(mks + (byc % MKEY_REP) * MKEY_GROUPS + n_first + uint32_t(lane) / g.P, lo,
+                    hi);
       } else {
         for (uint32_t k = 0; k < sg.SL; ++k) {
           const int l = wave_min(slot == k ? lo : INT_MAX);
