@@ -36,6 +36,14 @@ CASES = [
      Recipe("student_t", df=3.0), "f32"),
     ("conv7x7_s2_b4", LayerShape("c", "conv2d", 4, 3, 64, 32, 32, 7, 7, 2, 2, 3, 3), 4, 0,
      Recipe("student_t", df=3.0), "f32"),
+    # Sign forms of the selection launch on ragged shapes: a wave per 64 positions with a
+    # partial channel group (3x3 and 1x1, stride 2, odd maps) and with W in another dtype.
+    ("conv_s2_c6_oddmap_b3", LayerShape("c", "conv2d", 5, 6, 20, 9, 9, 3, 3, 2, 2, 1, 1), 3, 0,
+     Recipe("channel_lognormal", sigma=1.0), "f32"),
+    ("conv1x1_s2_c7_b2", LayerShape("c", "conv2d", 3, 7, 10, 7, 7, 1, 1, 2, 2, 0, 0), 2, 0,
+     Recipe("sample_lognormal", sigma=1.0), "f32"),
+    ("conv_s2_c10_bf16_b4", LayerShape("c", "conv2d", 4, 10, 24, 12, 12, 3, 3, 2, 2, 1, 1), 4,
+     0, Recipe("student_t", df=3.0), "bf16"),
     ("linear_ragged_b8", LayerShape("fc", "linear", 37, 300, 77), 8, 0,
      Recipe("sample_lognormal", sigma=2.0), "f32"),
     ("linear_b1", LayerShape("fc", "linear", 64, 512, 128), 1, 0,
