@@ -32,6 +32,7 @@ MFMA_FP4_PEAK_TOPS = 10100.0   # MI355X dense fp4 MFMA
 # VALU popcount: 256 CUs x 64 lanes x 2.4 GHz lane-ops; AND + popcount-accumulate of a 64-bit
 # word pair is 4 lane-ops for 64 binary multiply-accumulates (128 binary ops).
 POPC_PEAK_TOPS = 256 * 64 * 2.4e9 / 4 * 128 / 1e12
+GRAPH_STEPS = 10               # layer steps per graph in the graph-mode timing
 SCRUB_BYTES = 1 << 30          # cold-cache runs overwrite this much (the last-level cache is 256 MB)
 
 # HBM traffic per launch of the products kernel from rocprofv3 counter runs of this benchmark
@@ -658,12 +659,17 @@ def main():
         step()
     ms_eager = _timed(torch, stream, step, args.steps)
     ms_graph = None
+    # Graph mode: GRAPH_STEPS back-to-back steps per graph (as a network's step is one graph
+    # of many layer calls), so that each replay's launch is shared by that many steps; the K
+    # timed steps are K / GRAPH_STEPS replays (one step per graph when K is not a multiple).
+    graph_steps = GRAPH_STEPS if args.steps % GRAPH_STEPS == 0 else 1
     if not args.no_graph:
         g = _graph_of(torch, stream,
-                      lambda st: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st), 1)
-        for _ in range(args.warmup):
+                      lambda st: fqt.fqt_layer_backward(desc, cfg, X, W, dY, dX, dW, ws, st),
+                      graph_steps)
+        for _ in range(max(1, args.warmup // graph_steps)):
             g.replay()
-        ms_graph = _timed(torch, stream, g.replay, args.steps)
+        ms_graph = _timed(torch, stream, g.replay, args.steps // graph_steps) / graph_steps
 
     # Cold cache: before each timed step, overwrite 1 GiB (four times the last-level cache),
     # then time the step alone between two events.
@@ -803,6 +809,7 @@ def main():
                    "timed_as": "cold" if args.cold else (
                        "hip_graph" if ms_graph is not None and ms_graph <= ms_eager else "eager"),
                    "ms_per_step_eager": ms_eager, "ms_per_step_graph": ms_graph,
+                   "graph_steps_per_replay": graph_steps,
                    "ms_per_step_cold": ms_cold, "per_entry_ms": per,
                    "binary_ops_per_step": ops_per_step,
                    "linear_32x256x128": cfg1, "networks": networks},
