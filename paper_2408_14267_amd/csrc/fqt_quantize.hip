@@ -514,12 +514,36 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
   const int b = a.bits;
   const int B = (1 << b) - 1;
 
-  // The first group of each thread is read once and kept in registers (G <= NT: all).
-  const int2 own = t < G ? S.key[t] : make_int2(0, 0);
-#define GROUP_KEY(i) ((i) == t ? own : S.key[(i)])
+  // Thread t owns the groups [i0, i1) (at most CH of them): their keys are read once, all
+  // loads issued together, and kept in registers (every loop below walks the same chunk,
+  // unrolled, so the indices into the key registers are compile-time constants).
+  constexpr int CH = (GP + NT - 1) / NT;
+  const int chunk = (G + NT - 1) / NT;       // <= CH
+  const int i0 = t * chunk;
+  const int i1 = min(i0 + chunk, G);
+  int2 keys[CH];
+#pragma unroll
+  for (int m = 0; m < CH; ++m)
+    keys[m] = (m < chunk && i0 + m < G) ? S.key[i0 + m] : make_int2(0, 0);
   float rmax = 0.0f;
-  for (int i = t; i < G; i += NT) rmax = fmaxf(rmax, group_range(GROUP_KEY(i)));
+#pragma unroll
+  for (int m = 0; m < CH; ++m)
+    if (i0 + m < i1) rmax = fmaxf(rmax, group_range(keys[m]));
   rmax = block_max_f<NT>(rmax, scr_f);
+  // The groups' AGP weights, once each while they fit in registers (up to 8 groups per
+  // thread; 16 would spill, and are recomputed at each use instead).
+  constexpr bool WCACHE = CH <= 8;
+  uint64_t wts[WCACHE ? CH : 1];
+  if constexpr (WCACHE) {
+#pragma unroll
+    for (int m = 0; m < CH; ++m)
+      wts[m] = (a.mode != FQT_AGP_OFF && i0 + m < i1) ? agp_weight(group_range(keys[m]), rmax)
+                                                       : 0ull;
+  }
+  auto wt = [&](int m) -> uint64_t {
+    if constexpr (WCACHE) return wts[m];
+    else return agp_weight(group_range(keys[m]), rmax);
+  };
 
   int64_t s_sat = 0;           // number of saturated groups (p capped at 1)
   uint64_t w_thr = 0;          // weight of the last saturated group
@@ -533,12 +557,13 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
     // sort below decides.  Equal weights pass or fail together, so the saturated groups
     // are exactly those with w >= w_thr, the smallest saturated weight.
     constexpr int SAT_ROUNDS = 8;
-    const int c0 = t * ((G + NT - 1) / NT);
-    const int c1 = min(c0 + (G + NT - 1) / NT, G);
+    const int c0 = i0, c1 = i1;
     uint64_t wsum = 0;
-    for (int i = c0; i < c1; ++i) {
-      const uint64_t w = agp_weight(group_range(GROUP_KEY(i)), rmax);
-      skey[i] = w;                        // this thread's weights, kept in LDS
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      if (c0 + m >= c1) break;
+      const uint64_t w = wt(m);
+      skey[c0 + m] = w;                   // this thread's weights, kept in LDS
       wsum += w;
     }
     uint64_t W = block_sum<NT, uint64_t>(wsum, scr_u);
@@ -583,8 +608,10 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
     __syncthreads();                      // the weights in skey are read; the sort reuses it
   }
   if (need_sort) {
-    for (int i = t; i < GP; i += NT)
-      skey[i] = i < G ? sort_key(agp_weight(group_range(GROUP_KEY(i)), rmax), i) : 0ull;
+#pragma unroll
+    for (int m = 0; m < CH; ++m)
+      if (i0 + m < i1) skey[i0 + m] = sort_key(wt(m), i0 + m);
+    for (int i = G + t; i < GP; i += NT) skey[i] = 0ull;
     __syncthreads();
     // Bitonic sort, descending.
     for (int k = 2; k <= GP; k <<= 1) {
@@ -631,17 +658,17 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
 
   // Masks in id order, then the stable partition kept-ascending | pruned-ascending.
   const int64_t A = int64_t(G) - int64_t(b) * s_sat;
-  const int chunk = (G + NT - 1) / NT;       // <= 16 for G <= 16384 and NT >= 1024
-  const int i0 = t * chunk;
-  const int i1 = min(i0 + chunk, G);
   uint32_t keepbits = 0;
   int32_t nkeep = 0;
-  for (int i = i0; i < i1; ++i) {
+#pragma unroll
+  for (int m = 0; m < CH; ++m) {
+    const int i = i0 + m;
+    if (i >= i1) break;
     bool keep;
     if (a.mode == FQT_AGP_OFF) {
       keep = true;
     } else {
-      const uint64_t w = agp_weight(group_range(GROUP_KEY(i)), rmax);
+      const uint64_t w = wt(m);
       if (a.mode == FQT_AGP_TOPK) {
         keep = sort_key(w, i) >= key_thr;
       } else if (s_sat > 0 && w > 0 && w >= w_thr) {
@@ -658,22 +685,25 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
         keep = false;
       }
     }
-    keepbits |= (keep ? 1u : 0u) << (i - i0);
+    keepbits |= (keep ? 1u : 0u) << m;
     nkeep += keep ? 1 : 0;
   }
   int32_t count;
   int32_t rank = block_exscan<NT, int32_t>(nkeep, scr_i, count);
   if (t == 0) *S.count = count;
-  for (int i = i0; i < i1; ++i) {
-    const bool keep = (keepbits >> (i - i0)) & 1u;
-    const int2 k = GROUP_KEY(i);
+#pragma unroll
+  for (int m = 0; m < CH; ++m) {
+    const int i = i0 + m;
+    if (i >= i1) break;
+    const bool keep = (keepbits >> m) & 1u;
+    const int2 k = keys[m];
     const float R = group_range(k);
     const float Z = key2f(k.x);
     float Sc = 0.0f, Zp = 0.0f, p = 0.0f;
     bool unit_p = a.mode != FQT_AGP_BERNOULLI;
     uint64_t w = 0;
     if (a.mode == FQT_AGP_BERNOULLI) {
-      w = agp_weight(R, rmax);
+      w = wt(m);
       unit_p = s_sat > 0 && w > 0 && w >= w_thr;
     }
     if (a.mode == FQT_AGP_OFF) {
@@ -714,7 +744,6 @@ __global__ __launch_bounds__(NT) void k_select(SelectArgs a) {
       S.kept[count + (i - rank)] = i;
     }
   }
-#undef GROUP_KEY
 }
 
 // AGP off (Section 5.2: every group kept, p = 1) over large group sets: one thread per
