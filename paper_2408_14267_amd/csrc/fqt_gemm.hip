@@ -531,6 +531,19 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) qv[v] = __shfl(qrow, acc_row(v, g));
         const uint32_t jt = j0 + 32 * rt;
+        // The rows' scales and offsets and this lane's store row, loaded once per row tile,
+        // all at once (inside the column-tile loop they would follow each tile's dW stores,
+        // which the compiler cannot move them across: a dependent round trip per tile).
+        float2 szv[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const uint32_t j = jt + uint32_t(acc_row(v, g));
+          szv[v] = make_float2(0.0f, 0.0f);
+          if (int(j) < count)
+            szv[v] = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[a.kept[j]], a.offset[a.kept[j]]);
+        }
+        const uint32_t jrow = jt + uint32_t(lane >> 1);
+        const size_t drow = jrow < a.D ? size_t(a.kept[jrow]) : 0;
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
           const int T = int(tcnt[ct]);
@@ -539,19 +552,17 @@ __device__ __forceinline__ void dw_big_body(const DwArgs &a, uint32_t bid) {
             const uint32_t j = jt + uint32_t(acc_row(v, g));
             float out = 0.0f;
             if (int(j) < count) {
-              const float2 sz = a.slot_sz ? a.slot_sz[j]
-                                          : make_float2(a.scale[a.kept[j]], a.offset[a.kept[j]]);
               const int I = 2 * (acc[rt][ct][v] + (B8 ? 128 * T : 0)) - qv[v];
-              out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
+              out = rescale(szv[v].x, I, szv[v].y, float(2 * T - int(a.R)));
             }
             st[acc_row(v, g) * 32 + i] = out;
           }
           __builtin_amdgcn_wave_barrier();    // LDS operations of a wave run in order
-          const uint32_t j = jt + uint32_t(lane >> 1);
+          const uint32_t j = jrow;
           const uint32_t c0 = k0 + 32 * ct + 16 * uint32_t(lane & 1);
           if (j < a.D && c0 < a.K) {
             const float *src = st + (lane >> 1) * 32 + 16 * (lane & 1);
-            float *dst = a.dW + size_t(a.kept[j]) * a.K + c0;
+            float *dst = a.dW + drow * a.K + c0;
             if (c0 + 16 <= a.K && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
               const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
               uint4 *d4 = reinterpret_cast<uint4 *>(dst);
