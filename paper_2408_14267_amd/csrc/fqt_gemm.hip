@@ -212,17 +212,32 @@ __device__ __forceinline__ void dw_write_direct(const DwArgs &a, uint32_t j0, ui
                                                 int count, const v16i &acc, int T) {
   const int g = (threadIdx.x & 63) >> 5;
   if (kc >= a.K) return;
+  // The rows' kept ids, scales and offsets first, all loads together (after a row's dW
+  // store the next row's loads could not move ahead of it).
+  uint32_t dv[16];
+  float2 szv[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t j = j0 + uint32_t(acc_row(v, g));
+    dv[v] = j < a.D ? uint32_t(a.kept[j]) : 0u;
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const uint32_t j = j0 + uint32_t(acc_row(v, g));
+    szv[v] = make_float2(0.0f, 0.0f);
+    if (int(j) < count)
+      szv[v] = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[dv[v]], a.offset[dv[v]]);
+  }
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const uint32_t j = j0 + uint32_t(acc_row(v, g));
     if (j >= a.D) continue;
-    const size_t d = size_t(a.kept[j]);
+    const size_t d = dv[v];
     int I = 0;
     float out = 0.0f;
     if (int(j) < count) {
-      const float2 sz = a.slot_sz ? a.slot_sz[j] : make_float2(a.scale[d], a.offset[d]);
       I = acc[v] + (B8 ? 128 * (2 * T - int(a.Rp)) : 0);
-      out = rescale(sz.x, I, sz.y, float(2 * T - int(a.R)));
+      out = rescale(szv[v].x, I, szv[v].y, float(2 * T - int(a.R)));
     }
     a.dW[d * a.K + kc] = out;
     if (a.I_out) a.I_out[d * a.K + kc] = I;
